@@ -1,0 +1,155 @@
+"""CPU oracle for candidate-batch scoring (test infrastructure).
+
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The HIP library never loads it and
+shares no code with it.  The arithmetic lives in ``orloj_oracle.c`` (plain
+fp64 C, one step per quantity the paper defines); this module only
+marshals numpy arrays.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+from . import build as _build
+
+_LIB = None
+
+_I32P = ctypes.POINTER(ctypes.c_int32)
+_U32P = ctypes.POINTER(ctypes.c_uint32)
+_F64P = ctypes.POINTER(ctypes.c_double)
+
+
+def lib(path: Optional[str] = None):
+    """Load the oracle library (built by ``oracle/build.py``).  ``path``
+    loads another build of the oracle source (used by the mutation tests)."""
+    global _LIB
+    if path is not None:
+        return _bind(ctypes.CDLL(path))
+    if _LIB is None:
+        if not os.path.exists(_build.LIB):
+            _build.build()
+        _LIB = _bind(ctypes.CDLL(_build.LIB))
+    return _LIB
+
+
+def _bind(L):
+    L.orloj_oracle_cdf.argtypes = [ctypes.c_int32, _U32P, _F64P]
+    L.orloj_oracle_cdf.restype = ctypes.c_int
+    L.orloj_oracle_batch_cdf.argtypes = [ctypes.c_int32, ctypes.c_int32, _U32P, _F64P]
+    L.orloj_oracle_batch_cdf.restype = ctypes.c_int
+    L.orloj_oracle_score_model.argtypes = [
+        ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _I32P, ctypes.c_double,
+        _U32P, ctypes.c_int64, _I32P, _F64P, ctypes.c_double, ctypes.c_double,
+        ctypes.c_int32, _F64P, _F64P, _F64P, _F64P, _F64P, _I32P, _I32P, _F64P]
+    L.orloj_oracle_score_model.restype = ctypes.c_int
+    return L
+
+
+def _p(a, t):
+    return a.ctypes.data_as(t)
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def cdf(counts_row, L=None) -> np.ndarray:
+    L = L or lib()
+    c = np.ascontiguousarray(counts_row, dtype=np.uint32)
+    out = np.empty(c.size + 1, dtype=np.float64)
+    rc = L.orloj_oracle_cdf(c.size, _p(c, _U32P), _p(out, _F64P))
+    if rc:
+        raise OracleError(f"orloj_oracle_cdf rc={rc}")
+    return out
+
+
+def batch_cdf(rows, L=None) -> np.ndarray:
+    """CDF of the batch latency at the grid points for member count rows
+    [n, K]."""
+    L = L or lib()
+    r = np.ascontiguousarray(rows, dtype=np.uint32)
+    if r.ndim != 2:
+        raise ValueError("rows must be [n_members, n_bins]")
+    out = np.empty(r.shape[1] + 1, dtype=np.float64)
+    rc = L.orloj_oracle_batch_cdf(r.shape[1], r.shape[0], _p(r, _U32P), _p(out, _F64P))
+    if rc:
+        raise OracleError(f"orloj_oracle_batch_cdf rc={rc}")
+    return out
+
+
+def ncap(batch_sizes, n_queue: int, prefix_mode: int = 0) -> np.ndarray:
+    bs = np.asarray(batch_sizes, dtype=np.int64)
+    return np.full(bs.size, n_queue, np.int64) if prefix_mode else np.minimum(bs, n_queue)
+
+
+def output_sizes(queue_off, batch_sizes, prefix_mode: int = 0):
+    """Candidate and member offsets per model: (cand_off[M+1], prob_off[M+1])."""
+    qo = np.asarray(queue_off, dtype=np.int64)
+    M = qo.size - 1
+    cand_off = np.zeros(M + 1, np.int64)
+    prob_off = np.zeros(M + 1, np.int64)
+    for q in range(M):
+        caps = ncap(batch_sizes, int(qo[q + 1] - qo[q]), prefix_mode)
+        cand_off[q + 1] = cand_off[q] + caps.sum()
+        prob_off[q + 1] = prob_off[q] + (caps * (caps + 1) // 2).sum()
+    return cand_off, prob_off
+
+
+def score_model(counts, batch_sizes, bin_width_ms, cls, deadline_ms, now_ms, b_expo,
+                prefix_mode: int = 0, want_priority: bool = False, L=None) -> dict:
+    """All candidates of one model (see orloj_oracle_score_model)."""
+    L = L or lib()
+    cnt = np.ascontiguousarray(counts, dtype=np.uint32)
+    B, C, K = cnt.shape
+    bs = np.ascontiguousarray(batch_sizes, dtype=np.int32)
+    cl = np.ascontiguousarray(cls, dtype=np.int32)
+    dl = np.ascontiguousarray(deadline_ms, dtype=np.float64)
+    caps = ncap(bs, cl.size, prefix_mode)
+    n_cand = int(caps.sum())
+    n_prob = int((caps * (caps + 1) // 2).sum())
+    P = np.empty(n_prob)
+    pr = np.empty(n_prob) if want_priority else None
+    E = np.empty(n_cand)
+    EL = np.empty(n_cand)
+    S = np.empty(n_cand)
+    sn = np.zeros(1, np.int32)
+    sb = np.zeros(1, np.int32)
+    ss = np.zeros(1)
+    rc = L.orloj_oracle_score_model(
+        C, K, B, _p(bs, _I32P), float(bin_width_ms), _p(cnt, _U32P), cl.size,
+        _p(cl, _I32P), _p(dl, _F64P), float(now_ms), float(b_expo), int(prefix_mode),
+        _p(P, _F64P), _p(pr, _F64P) if pr is not None else None, _p(E, _F64P),
+        _p(EL, _F64P), _p(S, _F64P), _p(sn, _I32P), _p(sb, _I32P), _p(ss, _F64P))
+    if rc:
+        raise OracleError(f"orloj_oracle_score_model rc={rc}")
+    out = dict(finish_prob=P, expected_finish=E, expected_latency_ms=EL, score=S,
+               sel_n=int(sn[0]), sel_bs=int(sb[0]), sel_score=float(ss[0]))
+    if pr is not None:
+        out["priority"] = pr
+    return out
+
+
+def score_workload(wl, prefix_mode: int = 0, models: Optional[Sequence[int]] = None,
+                   want_priority: bool = False, L=None) -> dict:
+    """Score every model of a workload (or the listed ones); outputs are
+    concatenated in model order, as the HIP library lays them out."""
+    models = list(range(wl.n_models)) if models is None else list(models)
+    parts = []
+    for q in models:
+        m = wl.model(q)
+        parts.append(score_model(m["counts"], wl.batch_sizes, m["bin_width_ms"], m["cls"],
+                                 m["deadline_ms"], m["now_ms"], wl.b_expo, prefix_mode,
+                                 want_priority, L))
+    cat = lambda k: (np.concatenate([p[k] for p in parts]) if parts else np.zeros(0))
+    out = {k: cat(k) for k in ("finish_prob", "expected_finish", "expected_latency_ms", "score")}
+    if want_priority:
+        out["priority"] = cat("priority")
+    out["sel_n"] = np.array([p["sel_n"] for p in parts], np.int32)
+    out["sel_bs"] = np.array([p["sel_bs"] for p in parts], np.int32)
+    out["sel_score"] = np.array([p["sel_score"] for p in parts])
+    out["per_model"] = parts
+    return out

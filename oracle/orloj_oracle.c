@@ -1,0 +1,258 @@
+/*
+ * CPU oracle for scoring candidate batches against latency SLOs
+ * (Orloj: "Predictably Serving Unpredictable DNNs", arXiv 2209.00159).
+ *
+ * TEST INFRASTRUCTURE.  This is the plain, slow, fp64 reference that the
+ * HIP library is checked against.  Only the test suite, the smoke check and
+ * the benchmark's CPU-baseline leg load it; the product path never does.
+ * It shares no code, header, table or helper with the HIP library.
+ *
+ * The quantity computed is exact under the paper's own model: member
+ * latencies are independent (§4.2.2), a padded batch runs as long as its
+ * slowest member (§4.2.1, the max of the members), and a histogram bin
+ * spreads its mass uniformly over the bin (the per-bin integration behind
+ * Eq. (2), §4.1).  The steps below follow the paper's order:
+ *
+ *   1. empirical CDF of each per-class, per-batch-size histogram at the
+ *      grid points (§4.2.1: the CDF is read off the histogram; one
+ *      distribution per application, §3.2 "Per-Application Tracking");
+ *   2. time left before each deadline, relative to now (§4.4, relative
+ *      timestamps);
+ *   3. CDF of the batch latency as the product of the members' CDFs: the
+ *      law of the maximum of independent variables (§4.2.1 for identical
+ *      members, §4.2.2 Eq. (8) for different ones, whose integral over a
+ *      bin is exactly the change of this product);
+ *   4. expected batch latency, Eq. (5) with the batch histogram;
+ *   5. each member's probability of finishing by its deadline (§3.1,
+ *      §4.1 cost function);
+ *   6. expected number of members finishing in time (scheduler objective,
+ *      §4.1);
+ *   7. each member's priority, Eq. (1) evaluated through the per-bin closed
+ *      form Eq. (2) with L the batch latency (§4.2: L is the execution time
+ *      of the whole batch), summed over the batch;
+ *   8. the highest-scoring candidate (the scheduler pops the top batch,
+ *      §3.2 Algorithm 1).
+ *
+ * Readings taken where the paper is silent or ambiguous:
+ *   - candidates are the prefixes of the deadline-ordered queue of length
+ *     n <= min(batch size, queue length); a shorter prefix is padded to the
+ *     batch size and uses that size's latency table.  prefix_mode = 1 also
+ *     scores n up to the queue length ("what-if"), never selected when
+ *     n exceeds the batch size;
+ *   - the bin frequency h of Eq. (2) is the bin's probability density
+ *     (mass / width), so the priority tends to P / E[L] as b -> 0;
+ *   - the second case of Eq. (2) uses the lower edge of the same bin;
+ *   - one grid [0, K*w) per model shared by all classes and batch sizes;
+ *     a deadline at or beyond K*w finishes with probability 1, one at or
+ *     before now with probability 0;
+ *   - inside a bin the batch CDF is linear (uniform mass per bin);
+ *   - the cost of a miss is c = 1;
+ *   - selection: the largest score; exact ties go to the larger prefix,
+ *     then the smaller batch size; no batch when the best score is <= 0.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+
+enum { ORACLE_OK = 0, ORACLE_E_INVALID = 1, ORACLE_E_DATA = 2, ORACLE_E_NOMEM = 4 };
+
+/* Step 1.  cdf[0] = 0 and cdf[k] = (counts[0] + ... + counts[k-1]) / total
+ * for k = 1..n_bins, so cdf[n_bins] = 1.  The running sum is an exact
+ * integer; the division is one correctly rounded fp64 division. */
+int orloj_oracle_cdf(int32_t n_bins, const uint32_t *counts, double *cdf)
+{
+    if (n_bins < 1 || !counts || !cdf)
+        return ORACLE_E_INVALID;
+    uint64_t total = 0;
+    for (int32_t k = 0; k < n_bins; ++k)
+        total += counts[k];
+    if (total == 0)
+        return ORACLE_E_DATA;
+    uint64_t running = 0;
+    cdf[0] = 0.0;
+    for (int32_t k = 0; k < n_bins; ++k) {
+        running += counts[k];
+        cdf[k + 1] = (double)running / (double)total;
+    }
+    return ORACLE_OK;
+}
+
+/* Step 3 for one batch: G[k] = prod_i F_i(x_k) over the members' count
+ * rows (rows[i * n_bins ...]).  Exposed for the tests. */
+int orloj_oracle_batch_cdf(int32_t n_bins, int32_t n_members, const uint32_t *rows,
+                           double *G)
+{
+    if (n_bins < 1 || n_members < 0 || !G || (n_members > 0 && !rows))
+        return ORACLE_E_INVALID;
+    double *F = (double *)malloc(sizeof(double) * (size_t)(n_bins + 1));
+    if (!F)
+        return ORACLE_E_NOMEM;
+    for (int32_t k = 0; k <= n_bins; ++k)
+        G[k] = 1.0;
+    for (int32_t i = 0; i < n_members; ++i) {
+        int rc = orloj_oracle_cdf(n_bins, rows + (size_t)i * (size_t)n_bins, F);
+        if (rc) {
+            free(F);
+            return rc;
+        }
+        for (int32_t k = 0; k <= n_bins; ++k)
+            G[k] *= F[k];
+    }
+    free(F);
+    return ORACLE_OK;
+}
+
+/* Step 5.  P(L_B <= tau) with the batch CDF G at the grid points and a
+ * linear CDF inside each bin. */
+static double finish_probability(const double *G, int32_t n_bins, double w, double tau)
+{
+    if (!(tau > 0.0))
+        return 0.0;
+    double u = tau / w;
+    if (u >= (double)n_bins)
+        return G[n_bins];
+    int32_t k = (int32_t)floor(u);
+    double theta = u - (double)k;
+    return (1.0 - theta) * G[k] + theta * G[k + 1];
+}
+
+/* Step 7.  Eq. (2) of §4.1 bin by bin, cost c = 1, for a request with
+ * tau = D - t left and batch-latency bin masses mass[i] on bins
+ * [l1, l2) = [i w, (i+1) w).  The exponentials e^{b l} e^{-b D} e^{b t} of
+ * Eq. (2) are combined into e^{-b (tau - l)} (relative timestamps, §4.4).
+ * Returns E[L] * p(t), i.e. Eq. (2) without its 1/E[L] factor. */
+static double priority_times_latency(const double *mass, int32_t n_bins, double w,
+                                     double tau, double b)
+{
+    double acc = 0.0;
+    for (int32_t i = 0; i < n_bins; ++i) {
+        double l1 = (double)i * w;
+        double l2 = (double)(i + 1) * w;
+        double h = mass[i] / w;                 /* bin density */
+        if (tau > l2)                           /* t < D - l2 */
+            acc += h / b * (exp(-b * (tau - l2)) - exp(-b * (tau - l1)));
+        else if (tau > l1)                      /* D - l2 <= t < D - l1 */
+            acc += h / b * (1.0 - exp(-b * (tau - l1)));
+        /* else D - l1 <= t: the bin contributes nothing */
+    }
+    return acc;
+}
+
+/*
+ * All candidates of one model.  counts is [n_bs][n_classes][n_bins]; the
+ * queue (cls, deadline_ms) is sorted by deadline.  Outputs, in candidate
+ * order (batch size major, prefix length n = 1.. minor):
+ *   expected_finish[cand], expected_latency_ms[cand], score[cand];
+ * and per member m = 1..n of each candidate:
+ *   finish_prob[slot], priority[slot] (priority may be NULL).
+ * sel_n = 0 means no batch.
+ */
+int orloj_oracle_score_model(int32_t n_classes, int32_t n_bins, int32_t n_bs,
+                             const int32_t *batch_sizes, double bin_width_ms,
+                             const uint32_t *counts, int64_t n_queue, const int32_t *cls,
+                             const double *deadline_ms, double now_ms, double b_expo,
+                             int32_t prefix_mode, double *finish_prob, double *priority,
+                             double *expected_finish, double *expected_latency_ms,
+                             double *score, int32_t *sel_n, int32_t *sel_bs,
+                             double *sel_score)
+{
+    const int32_t C = n_classes, K = n_bins;
+    const double w = bin_width_ms, b = b_expo;
+    if (C < 1 || K < 1 || n_bs < 1 || !batch_sizes || !counts || n_queue < 0 ||
+        !(w > 0.0) || !(b > 0.0) || (prefix_mode != 0 && prefix_mode != 1) ||
+        !sel_n || !sel_bs || !sel_score)
+        return ORACLE_E_INVALID;
+    if (n_queue > 0 && (!cls || !deadline_ms))
+        return ORACLE_E_INVALID;
+    for (int32_t i = 0; i < n_bs; ++i)
+        if (batch_sizes[i] < 1 || (i > 0 && batch_sizes[i] <= batch_sizes[i - 1]))
+            return ORACLE_E_INVALID;
+    for (int64_t i = 0; i < n_queue; ++i) {
+        if (cls[i] < 0 || cls[i] >= C || isnan(deadline_ms[i]))
+            return ORACLE_E_DATA;
+        if (i > 0 && deadline_ms[i] < deadline_ms[i - 1])
+            return ORACLE_E_DATA;
+    }
+
+    /* Step 1: every (batch size, class) CDF. */
+    size_t row = (size_t)K + 1;
+    double *F = (double *)malloc(sizeof(double) * row * (size_t)n_bs * (size_t)C);
+    double *G = (double *)malloc(sizeof(double) * row);
+    double *mass = (double *)malloc(sizeof(double) * (size_t)K);
+    if (!F || !G || !mass) {
+        free(F); free(G); free(mass);
+        return ORACLE_E_NOMEM;
+    }
+    for (int32_t bi = 0; bi < n_bs; ++bi)
+        for (int32_t c = 0; c < C; ++c) {
+            size_t t = (size_t)bi * (size_t)C + (size_t)c;
+            if (orloj_oracle_cdf(K, counts + t * (size_t)K, F + t * row)) {
+                free(F); free(G); free(mass);
+                return ORACLE_E_DATA;
+            }
+        }
+
+    int64_t cand = 0, slot = 0;
+    int have_best = 0;
+    double best = 0.0;
+    int64_t best_n = 0;
+    int32_t best_bs = 0;
+    for (int32_t bi = 0; bi < n_bs; ++bi) {
+        int64_t cap = prefix_mode ? n_queue
+                                  : (n_queue < batch_sizes[bi] ? n_queue : batch_sizes[bi]);
+        for (int32_t k = 0; k <= K; ++k)
+            G[k] = 1.0;                           /* empty product */
+        for (int64_t n = 1; n <= cap; ++n) {
+            /* Step 3: add member n to the batch. */
+            const double *Fn = F + ((size_t)bi * (size_t)C + (size_t)cls[n - 1]) * row;
+            for (int32_t k = 0; k <= K; ++k)
+                G[k] *= Fn[k];
+
+            /* Step 4: E[L_B] of the batch histogram (trapezoid of 1 - G). */
+            double el = 0.0;
+            for (int32_t k = 0; k < K; ++k)
+                el += 1.0 - 0.5 * (G[k] + G[k + 1]);
+            el *= w;
+            for (int32_t k = 0; k < K; ++k)
+                mass[k] = G[k + 1] - G[k];
+
+            double e_count = 0.0, s = 0.0;
+            for (int64_t m = 1; m <= n; ++m) {
+                double tau = deadline_ms[m - 1] - now_ms;            /* step 2 */
+                double P = finish_probability(G, K, w, tau);         /* step 5 */
+                double p = priority_times_latency(mass, K, w, tau, b) / el;  /* step 7 */
+                finish_prob[slot] = P;
+                if (priority)
+                    priority[slot] = p;
+                ++slot;
+                e_count += P;                                        /* step 6 */
+                s += p;
+            }
+            expected_finish[cand] = e_count;
+            expected_latency_ms[cand] = el;
+            score[cand] = s;
+            ++cand;
+
+            /* Step 8. */
+            if (n <= batch_sizes[bi]) {
+                if (!have_best || s > best || (s == best && n > best_n)) {
+                    have_best = 1;
+                    best = s;
+                    best_n = n;
+                    best_bs = batch_sizes[bi];
+                }
+            }
+        }
+    }
+    if (have_best && best > 0.0) {
+        *sel_n = (int32_t)best_n;
+        *sel_bs = best_bs;
+        *sel_score = best;
+    } else {
+        *sel_n = 0;
+        *sel_bs = 0;
+        *sel_score = 0.0;
+    }
+    free(F); free(G); free(mass);
+    return ORACLE_OK;
+}

@@ -1,0 +1,513 @@
+"""Pins for the CPU oracle.
+
+Each pin checks the oracle against something other than its own code: exact
+rational brute force, closed forms, numerical quadrature of the priority's
+definition, Monte Carlo of the batch maximum, the paper's Eq. (8), and
+invariants the mathematics fixes.  Every pin takes a loaded oracle library
+handle, so planted-mistake builds of the oracle source run through the very
+same checks (tests/test_oracle_mutants.py); a pin raises AssertionError
+when the oracle is wrong.
+"""
+from __future__ import annotations
+
+import itertools
+import math
+from fractions import Fraction
+
+import numpy as np
+from scipy import integrate, special
+
+import oracle
+from paper_2209_00159_amd import workloads as W
+
+
+def rng(seed):
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([2209_00159, 7, seed])))
+
+
+def run_model(L, class_rows, queue_cls, taus, w, b=1e-4, batch_sizes=None, now=1000.0,
+              prefix_mode=0, per_bs_rows=None):
+    """One model through the oracle.  ``class_rows`` [C, K] are used for
+    every batch size unless ``per_bs_rows`` [B, C, K] is given.  Returns the
+    oracle dict plus the effective time-to-deadline the oracle sees."""
+    queue_cls = np.asarray(queue_cls, np.int32)
+    if batch_sizes is None:
+        batch_sizes = [max(1, len(queue_cls))]
+    if per_bs_rows is None:
+        counts = np.repeat(np.asarray(class_rows, np.uint32)[None], len(batch_sizes), axis=0)
+    else:
+        counts = np.asarray(per_bs_rows, np.uint32)
+    dl = now + np.asarray(taus, np.float64)
+    out = oracle.score_model(counts, batch_sizes, w, queue_cls, dl, now, b, prefix_mode,
+                             want_priority=True, L=L)
+    out["tau"] = dl - now
+    return out
+
+
+def slot(n, m):
+    """Position of member m (1-based) of prefix n inside one batch size's
+    block of per-member outputs."""
+    return (n - 1) * n // 2 + (m - 1)
+
+
+# ---------------------------------------------------------------- exact helpers
+def enumerate_max_masses(rows):
+    """Exact probability that the slowest member lands in bin j, by brute
+    force over every tuple of member bins (members independent)."""
+    rows = np.asarray(rows)
+    n, K = rows.shape
+    tots = [int(r.sum()) for r in rows]
+    mass = [Fraction(0)] * K
+    for tup in itertools.product(range(K), repeat=n):
+        wgt = Fraction(1)
+        for i, k in enumerate(tup):
+            c = int(rows[i, k])
+            if c == 0:
+                wgt = Fraction(0)
+                break
+            wgt *= Fraction(c, tots[i])
+        if wgt:
+            mass[max(tup)] += wgt
+    return mass
+
+
+def exact_cdf_product(rows):
+    """prod_i F_i(x_k) with exact rationals (the law of the max of
+    independent variables), k = 0..K."""
+    rows = np.asarray(rows)
+    K = rows.shape[1]
+    G = [Fraction(1)] * (K + 1)
+    for r in rows:
+        tot = int(r.sum())
+        run = 0
+        Fi = [Fraction(0)]
+        for k in range(K):
+            run += int(r[k])
+            Fi.append(Fraction(run, tot))
+        G = [g * f for g, f in zip(G, Fi)]
+    return G
+
+
+def histogram_prob_below(mass, w, tau):
+    """P(L <= tau) for a histogram with uniform mass inside each bin."""
+    if tau <= 0:
+        return Fraction(0)
+    u = Fraction(tau) / Fraction(w)
+    K = len(mass)
+    if u >= K:
+        return sum(mass, Fraction(0))
+    k = math.floor(u)
+    return sum(mass[:k], Fraction(0)) + (u - k) * mass[k]
+
+
+def histogram_mean(mass, w):
+    return sum(((j + Fraction(1, 2)) * Fraction(w) * m for j, m in enumerate(mass)),
+               Fraction(0))
+
+
+def delay_gain_quadrature(mass, w, tau, b):
+    """P(L <= tau < L + delay), delay ~ Exp(b), for L with density
+    mass_j / w on bin j: the integral over l < tau of the density times
+    P(delay > tau - l) = exp(-b (tau - l)), by adaptive quadrature."""
+    total = 0.0
+    for j, m in enumerate(mass):
+        lo, hi = j * w, min((j + 1) * w, tau)
+        if hi <= lo or m == 0:
+            continue
+        val, _ = integrate.quad(lambda l: math.exp(-b * (tau - l)), lo, hi,
+                                epsabs=0.0, epsrel=1e-13, limit=200)
+        total += float(m) / w * val
+    return total
+
+
+# ---------------------------------------------------------------- pins
+def pin_enumeration(L):
+    """Batch CDF, bin masses, E[L_B], finish probabilities and priorities of
+    tiny batches against exact rational brute force over member bins and
+    quadrature of the priority's definition."""
+    for seed in range(6):
+        r = rng(seed)
+        K = int(r.integers(2, 7))
+        C = int(r.integers(1, 4))
+        n = int(r.integers(1, 5))
+        rows = r.integers(0, 9, size=(C, K))
+        rows[rows.sum(axis=1) == 0, -1] = 1
+        cls = r.integers(0, C, size=n)
+        w = float(r.uniform(0.5, 3.0))
+        taus = np.sort(r.uniform(-0.5 * w, (K + 1.5) * w, size=n))
+        b = float(r.choice([1e-4, 0.05, 0.7]))
+        out = run_model(L, rows, cls, taus, w, b=b)
+        for nn in range(1, n + 1):
+            mass = enumerate_max_masses(rows[cls[:nn]])
+            G = np.array([float(sum(mass[:k], Fraction(0))) for k in range(K + 1)])
+            Gor = oracle.batch_cdf(rows[cls[:nn]], L=L)
+            assert np.allclose(Gor, G, rtol=0, atol=1e-14), (seed, nn, Gor, G)
+            E = float(histogram_mean(mass, w))
+            assert abs(out["expected_latency_ms"][nn - 1] - E) <= 1e-12 * E, (seed, nn)
+            ef = 0.0
+            sc = 0.0
+            for m in range(1, nn + 1):
+                tau = float(out["tau"][m - 1])
+                P = float(histogram_prob_below(mass, w, tau))
+                ef += P
+                got = out["finish_prob"][slot(nn, m)]
+                assert abs(got - P) <= 1e-13, (seed, nn, m, got, P)
+                pr = delay_gain_quadrature(mass, w, tau, b) / E
+                sc += pr
+                gp = out["priority"][slot(nn, m)]
+                assert abs(gp - pr) <= 1e-11 * max(1.0, abs(pr)) + 1e-15, (seed, nn, m, gp, pr)
+            assert abs(out["expected_finish"][nn - 1] - ef) <= 1e-12
+            assert abs(out["score"][nn - 1] - sc) <= 1e-10 * max(1.0, sc)
+
+
+def pin_iid_power(L):
+    """Identical members: the batch CDF is F^n (§4.2.1)."""
+    r = rng(11)
+    K = 17
+    row = r.integers(0, 50, size=K)
+    row[-1] += 1
+    tot = int(row.sum())
+    cum = np.concatenate([[0], np.cumsum(row)])
+    for n in (1, 2, 3, 7, 12):
+        G = oracle.batch_cdf(np.repeat(row[None], n, axis=0), L=L)
+        ref = np.array([float(Fraction(int(c), tot) ** n) for c in cum])
+        assert np.allclose(G, ref, rtol=1e-14, atol=1e-300), n
+
+
+def pin_point_mass(L):
+    """Static models (all of a class's mass in one bin): the batch runs as
+    long as its slowest member's bin, deterministically (§4.2 static case):
+    P is a ramp across that bin, E[L_B] is the bin's midpoint, and as the
+    delay rate b -> 0 the priority equals P / E[L_B]."""
+    K, w = 12, 2.0
+    C = 4
+    pos = [1, 4, 4, 9]
+    rows = np.zeros((C, K), np.int64)
+    for c, j in enumerate(pos):
+        rows[c, j] = 7 + c
+    cls = np.array([0, 2, 1, 3, 0])
+    taus = np.array([1.0, 2.5, 9.0, 10.0, 30.0])
+    out = run_model(L, rows, cls, taus, w, b=1e-9)
+    for nn in range(1, len(cls) + 1):
+        jstar = max(pos[c] for c in cls[:nn])
+        E = (jstar + 0.5) * w
+        assert abs(out["expected_latency_ms"][nn - 1] - E) <= 1e-12 * E
+        for m in range(1, nn + 1):
+            tau = out["tau"][m - 1]
+            P = min(1.0, max(0.0, tau / w - jstar))
+            got = out["finish_prob"][slot(nn, m)]
+            assert abs(got - P) <= 1e-12, (nn, m, got, P)
+            pr = out["priority"][slot(nn, m)]
+            assert abs(pr * E - P) <= 1e-7, (nn, m, pr * E, P)
+
+
+def pin_quadrature_medium(L):
+    """Medium batches (beyond brute force): priorities against quadrature of
+    their definition on the exact-rational product of the member CDFs."""
+    r = rng(21)
+    K, C, n = 40, 5, 6
+    rows = r.integers(0, 30, size=(C, K))
+    rows[:, :3] = 0
+    rows[rows.sum(axis=1) == 0, -1] = 1
+    cls = r.integers(0, C, size=n)
+    w = 0.8
+    taus = np.sort(r.uniform(1.0, 45.0, size=n))
+    for b in (1e-4, 0.02, 0.3):
+        out = run_model(L, rows, cls, taus, w, b=b)
+        G = exact_cdf_product(rows[cls])
+        mass = [G[k + 1] - G[k] for k in range(K)]
+        E = float(histogram_mean(mass, w))
+        assert abs(out["expected_latency_ms"][n - 1] - E) <= 1e-12 * E
+        for m in range(1, n + 1):
+            tau = float(out["tau"][m - 1])
+            pr = delay_gain_quadrature(mass, w, tau, b) / E
+            got = out["priority"][slot(n, m)]
+            assert abs(got - pr) <= 1e-11 * max(1.0, pr) + 1e-16, (b, m, got, pr)
+
+
+def pin_b_to_zero(L):
+    """As the anticipated delay rate b -> 0 a member's priority times
+    E[L_B] tends to its finish probability (each bin's delay factor -> 1)."""
+    r = rng(31)
+    K, C, n = 30, 3, 5
+    rows = r.integers(0, 20, size=(C, K))
+    rows[rows.sum(axis=1) == 0, -1] = 1
+    cls = r.integers(0, C, size=n)
+    taus = np.sort(r.uniform(-2.0, 40.0, size=n))
+    out = run_model(L, rows, cls, taus, 1.1, b=1e-10)
+    for nn in range(1, n + 1):
+        E = out["expected_latency_ms"][nn - 1]
+        for m in range(1, nn + 1):
+            P = out["finish_prob"][slot(nn, m)]
+            pr = out["priority"][slot(nn, m)]
+            assert abs(pr * E - P) <= 1e-7, (nn, m, pr * E, P)
+
+
+def pin_monte_carlo_max(L):
+    """Monte Carlo of the slowest member: sample each member's latency from
+    its histogram (bin by count, uniform inside), take the max; at grid
+    deadlines the oracle's finish probability must lie within 4 sigma of
+    the empirical frequency."""
+    r = rng(41)
+    K, C, n = 24, 4, 5
+    rows = r.integers(0, 40, size=(C, K))
+    rows[rows.sum(axis=1) == 0, -1] = 1
+    cls = r.integers(0, C, size=n)
+    w = 1.0
+    now = 0.0
+    taus = np.arange(3, 3 + n, dtype=np.float64) * 4.0     # grid points
+    out = run_model(L, rows, cls, taus, w, b=1e-4, now=now)
+    S = 400_000
+    lat = np.zeros(S)
+    for c in cls:
+        p = rows[c] / rows[c].sum()
+        bins = r.choice(K, size=S, p=p)
+        lat = np.maximum(lat, (bins + r.random(S)) * w)
+    for m in range(1, n + 1):
+        tau = taus[m - 1]
+        emp = (lat <= tau).mean()
+        P = out["finish_prob"][slot(n, m)]
+        sig = math.sqrt(max(P * (1 - P), 1e-12) / S)
+        assert abs(emp - P) <= 4 * sig + 1e-9, (m, emp, P, sig)
+
+
+def pin_monte_carlo_priority(L):
+    """Monte Carlo of the priority's definition (Eq. (1)): with L drawn from
+    the batch histogram and the anticipated delay ~ Exp(b), the expected
+    cost saved by running now is P(L <= tau < L + delay); dividing by
+    E[L_B] must give the oracle's priority within 4 sigma."""
+    r = rng(51)
+    K, C, n = 20, 3, 4
+    rows = r.integers(0, 25, size=(C, K))
+    rows[rows.sum(axis=1) == 0, -1] = 1
+    cls = r.integers(0, C, size=n)
+    w, b = 1.5, 0.08
+    taus = np.sort(r.uniform(5.0, 35.0, size=n))
+    out = run_model(L, rows, cls, taus, w, b=b)
+    G = exact_cdf_product(rows[cls])
+    mass = np.array([float(G[k + 1] - G[k]) for k in range(K)])
+    S = 1_000_000
+    bins = r.choice(K, size=S, p=mass / mass.sum())
+    lat = (bins + r.random(S)) * w
+    delay = r.exponential(1.0 / b, size=S)
+    E = out["expected_latency_ms"][n - 1]
+    for m in range(1, n + 1):
+        tau = out["tau"][m - 1]
+        ev = ((lat <= tau) & (tau < lat + delay)).mean()
+        pr = out["priority"][slot(n, m)] * E
+        sig = math.sqrt(max(pr * (1 - pr), 1e-12) / S)
+        assert abs(ev - pr) <= 4 * sig + 1e-9, (m, ev, pr, sig)
+    assert abs(E - float(lat.mean())) <= 4 * float(lat.std()) / math.sqrt(S)
+
+
+def ozbey_density(Fs, fs):
+    """Density of the max of independent, non-identical variables by the
+    inclusion-exclusion formula the paper cites (§4.2.2, Eq. (8)): a sum
+    over subset sizes kappa of (-1)^(k-kappa) kappa^k / k! times, over the
+    subsets s of that size, k [F^s]^(k-1) f^s with F^s, f^s the subset
+    averages."""
+    k = len(Fs)
+    tot = 0.0
+    for kappa in range(1, k + 1):
+        coef = (-1) ** (k - kappa) * kappa ** k / math.factorial(k)
+        inner = 0.0
+        for s in itertools.combinations(range(k), kappa):
+            Fs_avg = sum(Fs[i] for i in s) / kappa
+            fs_avg = sum(fs[i] for i in s) / kappa
+            inner += k * Fs_avg ** (k - 1) * fs_avg
+        tot += coef * inner
+    return tot
+
+
+def pin_ozbey_eq8(L):
+    """The product of the member CDFs is the CDF of the batch maximum: its
+    change over each bin equals the integral of the paper's Eq. (8) density
+    (Özbey et al.) for analytic lognormal members, up to the quantisation of
+    the histograms (2^31 samples each)."""
+    params = [(30.0, 0.3), (45.0, 0.5), (25.0, 0.2), (60.0, 0.4)]
+    K, w = 64, 2.5
+    x = np.arange(K + 1) * w
+    rows = []
+    for med, s in params:
+        cdf = np.where(x > 0, special.ndtr((np.log(np.maximum(x, 1e-300)) - math.log(med)) / s),
+                       0.0)
+        rows.append(W.quantise_counts(cdf, total=1 << 31))
+    rows = np.array(rows)
+    G = oracle.batch_cdf(rows, L=L)
+    mass = np.diff(G)
+
+    def cdf_pdf(l):
+        Fs, fs = [], []
+        for med, s in params:
+            z = (math.log(l) - math.log(med)) / s
+            Fs.append(special.ndtr(z))
+            fs.append(math.exp(-0.5 * z * z) / (l * s * math.sqrt(2 * math.pi)))
+        return Fs, fs
+
+    for j in range(8, K - 1):
+        val, _ = integrate.quad(lambda l: ozbey_density(*cdf_pdf(l)), x[j], x[j + 1],
+                                epsabs=1e-13, epsrel=1e-10)
+        assert abs(val - mass[j]) <= 2e-8, (j, val, mass[j])
+
+
+def pin_invariants(L):
+    """G in [0, 1], non-decreasing along the grid, non-increasing as members
+    join; E[L_B] non-decreasing as members join (adding a member never makes
+    the batch faster); P non-decreasing in the time left; priorities and P
+    unchanged when every histogram is scaled by an integer."""
+    r = rng(61)
+    K, C, n = 33, 4, 9
+    rows = r.integers(0, 15, size=(C, K))
+    rows[r.random(rows.shape) < 0.4] = 0
+    rows[rows.sum(axis=1) == 0, -1] = 1
+    cls = r.integers(0, C, size=n)
+    prev = None
+    for nn in range(1, n + 1):
+        G = oracle.batch_cdf(rows[cls[:nn]], L=L)
+        assert G[0] == 0.0 and G[-1] == 1.0
+        assert np.all(np.diff(G) >= 0) and np.all((G >= 0) & (G <= 1))
+        if prev is not None:
+            assert np.all(G <= prev + 1e-15)
+        prev = G
+    taus = np.sort(r.uniform(-3.0, 45.0, size=n))
+    out = run_model(L, rows, cls, taus, 1.3, b=0.01)
+    EL = out["expected_latency_ms"]
+    assert np.all(np.diff(EL) >= -1e-12)
+    for nn in range(1, n + 1):
+        P = out["finish_prob"][slot(nn, 1):slot(nn, nn) + 1]
+        assert np.all(np.diff(P) >= -1e-15), nn
+    out3 = run_model(L, rows * 3, cls, taus, 1.3, b=0.01)
+    for k in ("finish_prob", "priority", "expected_latency_ms", "score"):
+        assert np.allclose(out[k], out3[k], rtol=1e-13, atol=1e-15), k
+
+
+def pin_continuity(L):
+    """Eq. (2) is continuous in t: at the milestones where a bin edge meets
+    the deadline (t = D - l) the priority and P have no jump."""
+    r = rng(71)
+    K, C = 16, 2
+    rows = r.integers(1, 20, size=(C, K))
+    w = 1.25
+    for edge in (3, 7, 12):
+        for b in (1e-4, 0.2):
+            vals = []
+            for eps in (-1e-9, 1e-9):
+                out = run_model(L, rows, [0, 1], [edge * w + eps, 30.0], w, b=b, now=0.0)
+                vals.append((out["priority"][slot(2, 1)], out["finish_prob"][slot(2, 1)]))
+            assert abs(vals[0][0] - vals[1][0]) <= 1e-7, (edge, b, vals)
+            assert abs(vals[0][1] - vals[1][1]) <= 1e-7, (edge, b, vals)
+
+
+def pin_edge_cases(L):
+    """Dead requests finish with probability 0 and add no priority; deadlines
+    beyond the grid finish with probability 1; a batch always takes at least
+    half a bin on average."""
+    K, w = 10, 1.0
+    rows = np.zeros((1, K), np.int64)
+    rows[0, 0] = 5
+    out = run_model(L, rows, [0, 0, 0], [-5.0, 0.0, 25.0], w, b=1e-3)
+    n = 3
+    assert out["finish_prob"][slot(n, 1)] == 0.0 and out["priority"][slot(n, 1)] == 0.0
+    assert out["finish_prob"][slot(n, 2)] == 0.0 and out["priority"][slot(n, 2)] == 0.0
+    assert out["finish_prob"][slot(n, 3)] == 1.0
+    assert abs(out["expected_latency_ms"][n - 1] - 0.5 * w) <= 1e-15
+
+
+def _brute_select(wl_model_out, batch_sizes, caps):
+    best = None
+    i = 0
+    for bi, b in enumerate(batch_sizes):
+        for n in range(1, caps[bi] + 1):
+            s = wl_model_out["score"][i]
+            i += 1
+            if n > b:
+                continue
+            key = (s, n, -b)
+            if best is None or key > best[0]:
+                best = (key, n, b, s)
+    if best is None or best[3] <= 0:
+        return 0, 0
+    return best[1], best[2]
+
+
+def pin_selection(L):
+    """Selection is the largest score over candidates n <= batch size; exact
+    ties go to the larger prefix, then the smaller batch size; no batch when
+    every score is <= 0."""
+    r = rng(81)
+    for seed in range(5):
+        wl = W.random_case(seed, n_models=1, queue_lens=[int(r.integers(1, 12))])
+        m = wl.model(0)
+        out = oracle.score_model(m["counts"], wl.batch_sizes, m["bin_width_ms"], m["cls"],
+                                 m["deadline_ms"], m["now_ms"], wl.b_expo, L=L)
+        caps = np.minimum(wl.batch_sizes, wl.queue_len(0))
+        assert (out["sel_n"], out["sel_bs"]) == _brute_select(out, wl.batch_sizes, caps)
+    # identical tables for every batch size and one member: equal scores,
+    # the smaller batch size wins.
+    rows = np.array([[0, 3, 5, 1, 0, 0]])
+    out = run_model(L, rows, [0], [4.0], 1.0, batch_sizes=[1, 2, 4])
+    assert out["score"][0] == out["score"][1] == out["score"][2] > 0
+    assert (out["sel_n"], out["sel_bs"]) == (1, 1)
+    # two identical members: prefix 2 ties prefix 1 only if scores equal;
+    # a dead queue selects nothing.
+    out = run_model(L, rows, [0, 0], [-1.0, -0.5], 1.0, batch_sizes=[1, 2])
+    assert out["sel_n"] == 0 and out["sel_bs"] == 0
+
+
+def pin_rect_mode(L):
+    """prefix_mode 1 scores prefixes up to the queue length at every batch
+    size; prefixes within the batch size match prefix_mode 0 and longer ones
+    are never selected."""
+    wl = W.random_case(3, n_models=1, queue_lens=[9], batch_sizes=(1, 2, 4))
+    m = wl.model(0)
+    args = (m["counts"], wl.batch_sizes, m["bin_width_ms"], m["cls"], m["deadline_ms"],
+            m["now_ms"], wl.b_expo)
+    tri = oracle.score_model(*args, prefix_mode=0, L=L)
+    rect = oracle.score_model(*args, prefix_mode=1, L=L)
+    ti = ri = 0
+    for b in wl.batch_sizes:
+        for n in range(1, 10):
+            if n <= b:
+                assert rect["score"][ri] == tri["score"][ti]
+                assert rect["expected_finish"][ri] == tri["expected_finish"][ti]
+                ti += 1
+            ri += 1
+    assert rect["sel_n"] <= rect["sel_bs"]
+    assert (rect["sel_n"], rect["sel_bs"]) == (tri["sel_n"], tri["sel_bs"])
+
+
+def pin_toy_example(L):
+    """The paper's toy example (§4.2.2): two distributions with the same
+    mean, one concentrated and one early-or-late, batch of two.  The batch
+    histogram is skewed to the right of both members (it dominates each
+    member's CDF), and a member's priority rises as its deadline nears and
+    falls to zero once even the fastest batch outcome can no longer make
+    it."""
+    K, w = 20, 1.0
+    concentrated = np.zeros(K, np.int64)
+    concentrated[9:11] = 50
+    early_late = np.zeros(K, np.int64)
+    early_late[2] = 50
+    early_late[17] = 50
+    rows = np.stack([concentrated, early_late])
+    G = oracle.batch_cdf(rows, L=L)
+    for row in rows:
+        F = oracle.cdf(row, L=L)
+        assert np.all(G <= F + 1e-15)
+    assert np.all(np.diff(G)[:9] == 0.0)          # no batch outcome below bin 9
+    # priority of a member vs time left (decreasing time left = time passes)
+    pri = []
+    taus = np.linspace(30.0, 0.5, 60)
+    for tau in taus:
+        out = run_model(L, rows, [0, 1], [tau, 40.0], w, b=0.05, now=0.0)
+        pri.append(out["priority"][slot(2, 1)])
+    pri = np.array(pri)
+    peak = int(np.argmax(pri))
+    assert 0 < peak < len(taus) - 1
+    assert np.all(np.diff(pri[:peak + 1]) >= -1e-12)       # rises
+    assert np.all(pri[taus <= 9.0] == 0.0)                 # then 0
+
+
+PINS = [pin_enumeration, pin_iid_power, pin_point_mass, pin_quadrature_medium, pin_b_to_zero,
+        pin_monte_carlo_max, pin_monte_carlo_priority, pin_ozbey_eq8, pin_invariants,
+        pin_continuity, pin_edge_cases, pin_selection, pin_rect_mode, pin_toy_example]
