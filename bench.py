@@ -1,0 +1,185 @@
+"""Benchmark: candidate-batch x histogram-bin evaluations per second.
+
+One step = one scheduling pass of the hot path over every model of the
+workload: orloj_score_candidates (scan over queue position of the members'
+log2 CDF rows, batch CDF, E[L_B], finish probabilities, priorities) and
+orloj_select_batch (one batch per model).  The log2 CDF tables are built
+once before timing (orloj_build_cdfs refreshes profiles off the scheduling
+path) and timed on their own.  Inputs are resident in HBM when the timed
+region starts.
+
+Default workload: configuration 5 in its saturated decision state (128
+models x 64 batch sizes x 32 classes x 4096 bins, every model holding a
+backlog deep enough for all 64-member prefixes).
+
+Prints ONE JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("candidate-batch × histogram-bin evaluations/sec; "
+          "scheduling decisions/sec")
+HBM_PEAK_GBS = 8000.0
+
+
+def algorithmic_bytes(wl, mode=0):
+    """Bytes one score launch must move at least: each distinct log2 CDF row
+    a (model, batch size) workgroup reads, each queued request read once
+    (class + deadline), the per-model scalars, and every output."""
+    K = wl.n_bins
+    rows = 0
+    reqs = 0
+    n_c = 0
+    n_p = 0
+    for q in range(wl.n_models):
+        a, b = int(wl.queue_off[q]), int(wl.queue_off[q + 1])
+        N = b - a
+        cls = wl.cls[a:b]
+        maxcap = 0
+        for s in wl.batch_sizes:
+            cap = N if mode else min(int(s), N)
+            maxcap = max(maxcap, cap)
+            rows += len(np.unique(cls[:cap]))
+            n_c += cap
+            n_p += cap * (cap + 1) // 2
+        reqs += maxcap
+    table = rows * K * 4
+    queue = reqs * 12 + wl.n_models * (8 + 8 + 8 * 4)
+    outputs = n_p * 4 + n_c * 16
+    return dict(total=table + queue + outputs, table=table, queue=queue, outputs=outputs,
+                distinct_rows=rows, n_cands=n_c, n_probs=n_p)
+
+
+def valid_candidates(wl):
+    return sum(min(int(s), wl.queue_len(q)) for q in range(wl.n_models) for s in wl.batch_sizes)
+
+
+def cpu_baseline(config_id, n_models, budget_s=20.0):
+    """The oracle, as it stands, on the first models of the workload (one
+    host thread).  Returns evals/s over the sample."""
+    import oracle
+    from paper_2209_00159_amd import workloads as W
+
+    wl = W.make(config_id, models=list(range(n_models)) if config_id in (4, 5) else None)
+    t0 = time.perf_counter()
+    done = 0
+    ev = 0
+    for q in range(wl.n_models):
+        oracle.score_workload(wl.subset([q]))
+        done += 1
+        ev += sum(min(int(s), wl.queue_len(q)) for s in wl.batch_sizes) * wl.n_bins
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return dict(value=ev / dt, unit="evals/s", cores=1, kind="oracle",
+                sample=f"{wl.name}: first {done} model(s), full triangles, fp64 C oracle, "
+                       f"{dt:.1f} s on one host thread",
+                seconds=dt, decisions_per_s=done / dt)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=5)
+    ap.add_argument("--cpu-models", type=int, default=24)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workers", type=int, default=16)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU: the scorer has no multi-GPU path "
+              f"(--gpus {args.gpus} requested)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2209_00159_amd import orloj as O
+    from paper_2209_00159_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+
+    t0 = time.perf_counter()
+    wl = W.make(args.config, workers=args.workers)
+    print(f"[bench] generated {wl.name} in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
+          flush=True)
+    ctx = O.Context(0)
+    sc = O.Scorer(wl, ctx)
+    ab = algorithmic_bytes(wl)
+    K = wl.n_bins
+    evals = valid_candidates(wl) * K
+
+    # profile refresh (off the scheduling path): timed on its own
+    sc.build()
+    ctx.sync()
+    b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    b0.record()
+    sc.build()
+    b1.record()
+    ctx.sync()
+    build_ms = b0.elapsed_time(b1)
+
+    for _ in range(args.warmup):
+        sc.score()
+        sc.select()
+    ctx.sync()
+    print(f"[bench] warmup done", file=sys.stderr, flush=True)
+
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for e0, e1 in evs:
+        e0.record()
+        sc.score()
+        e1.record()
+        sc.select()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ctx.sync()
+    score_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in evs]))
+    ms_per_step = wall * 1e3 / args.steps
+    print(f"[bench] timed {args.steps} steps: {ms_per_step:.4f} ms/step, score kernel "
+          f"{score_ms:.4f} ms", file=sys.stderr, flush=True)
+
+    achieved = ab["total"] / (score_ms * 1e-3) / 1e9
+    roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                frac=round(achieved / HBM_PEAK_GBS, 4), traffic=None,
+                kernel="score_kernel", kernel_ms=round(score_ms, 5),
+                algorithmic_bytes=ab["total"])
+    line = dict(
+        metric=METRIC, value=evals / (ms_per_step * 1e-3), unit="evals/s", n_gpus=1,
+        steps=args.steps, warmup=args.warmup, ms_per_step=round(ms_per_step, 5),
+        higher_is_better=True, scaling="weak", vs_baseline=None, dtype="f32",
+        data="synthetic",
+        config=dict(workload=wl.name, models=wl.n_models, classes=wl.n_classes, bins=K,
+                    batch_sizes=f"{int(wl.batch_sizes[0])}..{int(wl.batch_sizes[-1])}",
+                    candidates=valid_candidates(wl), evals_per_step=evals,
+                    prefix_mode="triangle", b_expo_per_ms=wl.b_expo),
+        decisions_per_s=wl.n_models / (ms_per_step * 1e-3),
+        build_cdfs_ms=round(build_ms, 4),
+        build_cdfs_gbs=round(wl.counts.nbytes * 2 / (build_ms * 1e-3) / 1e9, 1),
+        roofline=roof,
+    )
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(args.config, args.cpu_models)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

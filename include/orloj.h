@@ -1,0 +1,181 @@
+/*
+ * orloj.h - C ABI of the MI355X candidate-batch scorer.
+ *
+ * Scores candidate batches against latency SLOs with empirical
+ * distributions of request execution time, the hot path of Orloj
+ * ("Predictably Serving Unpredictable DNNs", arXiv 2209.00159):
+ *
+ *   orloj_build_cdfs        histogram -> log2 CDF table
+ *   orloj_output_sizes      host-side sizing of the per-candidate outputs
+ *   orloj_score_candidates  every prefix candidate at every batch size:
+ *                           batch CDF, E[L_B], finish probabilities,
+ *                           expected finish count, priority score
+ *   orloj_select_batch      highest-scoring candidate per model
+ *
+ * Conventions.  Pointers named d_* are device (HBM) pointers owned by the
+ * caller; h_* pointers and the structs are host memory read during the call
+ * only.  Every call is asynchronous on the context's HIP stream: it returns
+ * after validating its arguments and enqueueing kernels.  Argument problems
+ * return ORLOJ_E_INVALID (or ORLOJ_E_UNSUPPORTED for shapes beyond the
+ * compiled limits) before anything is launched; problems found in device
+ * data (a histogram with no samples, a class id out of range, a NaN or
+ * unsorted deadline) are recorded on the device and returned by
+ * orloj_sync() as ORLOJ_E_DATA.  HIP runtime failures return ORLOJ_E_HIP.
+ * orloj_last_error() describes the most recent failure of a context.
+ * Times are milliseconds throughout.  A context is not thread-safe; calls
+ * that share a context must be serialised by the caller.
+ */
+#ifndef ORLOJ_H
+#define ORLOJ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum orloj_status {
+    ORLOJ_OK = 0,
+    ORLOJ_E_INVALID = 1,      /* bad argument, detected on the host */
+    ORLOJ_E_DATA = 2,         /* bad device data, reported by orloj_sync */
+    ORLOJ_E_HIP = 3,          /* HIP runtime error */
+    ORLOJ_E_NOMEM = 4,        /* host or device allocation failed */
+    ORLOJ_E_UNSUPPORTED = 5   /* valid but beyond the compiled limits */
+};
+
+/* Candidate sets (the prefixes of each model's deadline-ordered queue).
+ * TRIANGLE: at batch size s, prefixes n = 1 .. min(s, N).  A prefix shorter
+ * than s is padded to s and uses s's latency table (a padded batch runs as
+ * long as its slowest member, §4.2.1).
+ * RECT: prefixes n = 1 .. N at every batch size ("what-if" scores for
+ * n > s, never selected). */
+enum orloj_prefix_mode { ORLOJ_PREFIX_TRIANGLE = 0, ORLOJ_PREFIX_RECT = 1 };
+
+/* Compiled limits. */
+#define ORLOJ_MAX_BINS 8192       /* histogram bins per table */
+#define ORLOJ_MAX_BATCH_SIZES 256 /* entries of the batch-size set */
+#define ORLOJ_MAX_PREFIX 256      /* longest prefix scored per batch size */
+
+typedef struct orloj_ctx orloj_ctx;
+
+/* Create a context on HIP device `hip_device` that enqueues on `hip_stream`
+ * (a hipStream_t; NULL = the null stream).  Allocates a small device status
+ * word.  Returns ORLOJ_OK and *out, or an error with *out = NULL. */
+int orloj_create(orloj_ctx **out, int32_t hip_device, void *hip_stream);
+
+/* Free a context (waits for its stream first).  NULL is a no-op. */
+void orloj_destroy(orloj_ctx *ctx);
+
+/* Switch the stream later calls enqueue on. */
+int orloj_set_stream(orloj_ctx *ctx, void *hip_stream);
+
+/* Text of the last error of `ctx` (never NULL; "" when none). */
+const char *orloj_last_error(const orloj_ctx *ctx);
+
+/* Wait for all work enqueued on the context's stream, then report and clear
+ * any device-detected data error (ORLOJ_E_DATA). */
+int orloj_sync(orloj_ctx *ctx);
+
+/*
+ * The shared grid of a launch.  Every model has n_classes request classes
+ * (applications, §3.2 "Per-Application Tracking") and one latency
+ * histogram per (batch size, class) on its own grid of n_bins bins of width
+ * bin_width_ms[q]: bin k covers [k w, (k+1) w).  Mass beyond the grid is
+ * expected in the last bin.
+ */
+typedef struct orloj_grid {
+    int32_t n_models;               /* M >= 0 */
+    int32_t n_classes;              /* C >= 1 */
+    int32_t n_bins;                 /* K in [1, ORLOJ_MAX_BINS] */
+    int32_t n_bs;                   /* |S| in [1, ORLOJ_MAX_BATCH_SIZES] */
+    const int32_t *batch_sizes;     /* host [n_bs], strictly increasing, >= 1 */
+    const double *d_bin_width_ms;   /* device [M], each > 0 */
+} orloj_grid;
+
+/*
+ * Pending requests (§3.1: release time, deadline = release + SLO), one
+ * queue per model, stored back to back (CSR).  Each queue is sorted by
+ * deadline, non-decreasing; equal deadlines keep the caller's order.
+ */
+typedef struct orloj_queues {
+    const int64_t *h_queue_off;     /* host [M+1], h_queue_off[0] = 0, non-decreasing */
+    const int64_t *d_queue_off;     /* device copy of h_queue_off */
+    const int32_t *d_class;         /* device [N], class id in [0, C) */
+    const double *d_deadline_ms;    /* device [N] absolute deadlines */
+    const double *d_now_ms;         /* device [M] current time per model */
+} orloj_queues;
+
+/*
+ * Histogram -> log-CDF table (§4.2.1: the CDF of a request's latency is read
+ * off its histogram).  For each of n_rows rows of n_bins uint32 counts:
+ *   d_log2cdf[r][k] = log2 F(x_{k+1}),  F(x_{k+1}) = (counts[0..k] summed) / total,
+ * so entry n_bins-1 is exactly 0, entries with F = 0 are -inf.  The running
+ * sums are exact 64-bit integers; the log keeps relative accuracy near
+ * F = 1 (it is taken of 1 - tail/total there).  Rows are laid out
+ * [model][batch size][class][bin] for orloj_score_candidates.  A row with
+ * total 0 is a data error (its entries are written as NaN).
+ * d_counts and d_log2cdf must not overlap.
+ */
+int orloj_build_cdfs(orloj_ctx *ctx, int64_t n_rows, int32_t n_bins,
+                     const uint32_t *d_counts, float *d_log2cdf);
+
+/*
+ * Output sizing (host only, no launch).  For model q with queue length N_q
+ * and batch size s_b, ncap(q,b) = min(s_b, N_q) (TRIANGLE) or N_q (RECT).
+ *   h_cand_off[q+1] - h_cand_off[q] = sum_b ncap(q,b)
+ *   h_prob_off[q+1] - h_prob_off[q] = sum_b ncap(q,b) (ncap(q,b) + 1) / 2
+ * Candidate (q, b, n) sits at h_cand_off[q] + sum_{b'<b} ncap(q,b') + n - 1.
+ * Member m (1..n) of that candidate sits at
+ *   h_prob_off[q] + sum_{b'<b} T(ncap(q,b')) + T(n-1) + m - 1,  T(j) = j(j+1)/2.
+ * h_cand_off / h_prob_off are host [M+1] outputs; either may be NULL.
+ */
+int orloj_output_sizes(const orloj_grid *grid, const orloj_queues *queues,
+                       int32_t prefix_mode, int64_t *n_cands, int64_t *n_probs,
+                       int64_t *h_cand_off, int64_t *h_prob_off);
+
+/*
+ * Score every candidate of every model in one launch (§4.1-§4.2).
+ * For candidate (q, b, n) with members i = 1..n of q's queue:
+ *   G(x_k)      = prod_i F_{c_i, b}(x_k)      batch-latency CDF: the max of
+ *                 independent member latencies (§4.2.1-§4.2.2), linear
+ *                 inside a bin;
+ *   E[L_B]      = sum_k (G(x_{k+1}) - G(x_k)) (x_k + w/2)        (Eq. (5));
+ *   P_m         = G(D_m - now)  (0 if the deadline has passed, 1 beyond
+ *                 the grid);
+ *   p_m         = Eq. (1)-(2) priority of member m with L = L_B, miss cost
+ *                 1, anticipated delay ~ Exp(b_expo_per_ms), bin frequency
+ *                 read as density;
+ *   outputs     d_finish_prob[member slot] = P_m           (float)
+ *               d_expected_finish[cand]   = sum_m P_m      (double)
+ *               d_expected_latency_ms[cand] = E[L_B]       (float)
+ *               d_score[cand]             = sum_m p_m      (float)
+ * d_log2cdf is the [M][n_bs][C][K] table of orloj_build_cdfs.  d_cand_off /
+ * d_prob_off are device copies of orloj_output_sizes' offsets.  Output
+ * buffers hold at least n_cands / n_probs elements.  b_expo_per_ms must be
+ * finite and > 0 (the paper uses 1e-4 per ms, §4.4).
+ * ORLOJ_E_UNSUPPORTED when a prefix would exceed ORLOJ_MAX_PREFIX.
+ */
+int orloj_score_candidates(orloj_ctx *ctx, const orloj_grid *grid, const float *d_log2cdf,
+                           const orloj_queues *queues, double b_expo_per_ms,
+                           int32_t prefix_mode, const int64_t *d_cand_off,
+                           const int64_t *d_prob_off, float *d_finish_prob,
+                           double *d_expected_finish, float *d_expected_latency_ms,
+                           float *d_score);
+
+/*
+ * Pick one batch per model (the scheduler pops the top batch, §3.2
+ * Algorithm 1): the candidate with the largest score among n <= batch size;
+ * exact ties go to the larger n, then the smaller batch size.  When the
+ * best score is <= 0 (or the queue is empty) there is no batch:
+ * d_sel_n[q] = 0, d_sel_bs[q] = 0, d_sel_score[q] = 0.
+ * Outputs are device [M].
+ */
+int orloj_select_batch(orloj_ctx *ctx, const orloj_grid *grid, const orloj_queues *queues,
+                       int32_t prefix_mode, const int64_t *d_cand_off, const float *d_score,
+                       int32_t *d_sel_n, int32_t *d_sel_bs, float *d_sel_score);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ORLOJ_H */

@@ -1,0 +1,265 @@
+"""Python binding of liborloj.so (include/orloj.h).
+
+Argument marshalling only: every step of the scoring path runs in the HIP
+kernels behind the C ABI.  PyTorch supplies device memory and the stream.
+There is no fallback: if the library is not built, or no GPU is visible,
+calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liborloj.so")
+
+ORLOJ_OK, ORLOJ_E_INVALID, ORLOJ_E_DATA, ORLOJ_E_HIP, ORLOJ_E_NOMEM, ORLOJ_E_UNSUPPORTED = range(6)
+PREFIX_TRIANGLE, PREFIX_RECT = 0, 1
+MAX_BINS, MAX_BATCH_SIZES, MAX_PREFIX = 8192, 256, 256
+
+_STATUS = {0: "OK", 1: "E_INVALID", 2: "E_DATA", 3: "E_HIP", 4: "E_NOMEM", 5: "E_UNSUPPORTED"}
+
+
+class OrlojError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"orloj {_STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class Grid(ctypes.Structure):
+    _fields_ = [("n_models", ctypes.c_int32), ("n_classes", ctypes.c_int32),
+                ("n_bins", ctypes.c_int32), ("n_bs", ctypes.c_int32),
+                ("batch_sizes", ctypes.POINTER(ctypes.c_int32)),
+                ("d_bin_width_ms", ctypes.c_void_p)]
+
+
+class Queues(ctypes.Structure):
+    _fields_ = [("h_queue_off", ctypes.POINTER(ctypes.c_int64)),
+                ("d_queue_off", ctypes.c_void_p), ("d_class", ctypes.c_void_p),
+                ("d_deadline_ms", ctypes.c_void_p), ("d_now_ms", ctypes.c_void_p)]
+
+
+_LIB = None
+_VP = ctypes.c_void_p
+_GP = ctypes.POINTER(Grid)
+_QP = ctypes.POINTER(Queues)
+_I64P = ctypes.POINTER(ctypes.c_int64)
+
+EXPORTS = ("orloj_create", "orloj_destroy", "orloj_set_stream", "orloj_last_error", "orloj_sync",
+           "orloj_build_cdfs", "orloj_output_sizes", "orloj_score_candidates",
+           "orloj_select_batch")
+
+
+def load(path: str = LIB_PATH):
+    """Load and bind liborloj.so (no GPU needed to load)."""
+    global _LIB
+    if _LIB is not None and path == LIB_PATH:
+        return _LIB
+    if not os.path.exists(path):
+        raise OrlojError(ORLOJ_E_INVALID,
+                         f"{path} is not built; run __graft_entry__.build() first")
+    L = ctypes.CDLL(path)
+    L.orloj_create.argtypes = [ctypes.POINTER(_VP), ctypes.c_int32, _VP]
+    L.orloj_create.restype = ctypes.c_int
+    L.orloj_destroy.argtypes = [_VP]
+    L.orloj_destroy.restype = None
+    L.orloj_set_stream.argtypes = [_VP, _VP]
+    L.orloj_set_stream.restype = ctypes.c_int
+    L.orloj_last_error.argtypes = [_VP]
+    L.orloj_last_error.restype = ctypes.c_char_p
+    L.orloj_sync.argtypes = [_VP]
+    L.orloj_sync.restype = ctypes.c_int
+    L.orloj_build_cdfs.argtypes = [_VP, ctypes.c_int64, ctypes.c_int32, _VP, _VP]
+    L.orloj_build_cdfs.restype = ctypes.c_int
+    L.orloj_output_sizes.argtypes = [_GP, _QP, ctypes.c_int32, _I64P, _I64P, _I64P, _I64P]
+    L.orloj_output_sizes.restype = ctypes.c_int
+    L.orloj_score_candidates.argtypes = [_VP, _GP, _VP, _QP, ctypes.c_double, ctypes.c_int32,
+                                         _VP, _VP, _VP, _VP, _VP, _VP]
+    L.orloj_score_candidates.restype = ctypes.c_int
+    L.orloj_select_batch.argtypes = [_VP, _GP, _QP, ctypes.c_int32, _VP, _VP, _VP, _VP, _VP]
+    L.orloj_select_batch.restype = ctypes.c_int
+    if path == LIB_PATH:
+        _LIB = L
+    return L
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _need_cuda(t: torch.Tensor, name: str, dtypes, device):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.device != device:
+        raise ValueError(f"{name} must live on {device}, not {t.device}")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+class Context:
+    """An orloj_ctx bound to one device and (by default) torch's current
+    stream on it."""
+
+    def __init__(self, device=None, stream: Optional[torch.cuda.Stream] = None):
+        if not torch.cuda.is_available():
+            raise OrlojError(ORLOJ_E_INVALID, "no GPU visible")
+        self.L = load()
+        self.device = torch.device("cuda", torch.cuda.current_device() if device is None
+                                   else torch.device(device).index or 0)
+        st = stream if stream is not None else torch.cuda.current_stream(self.device)
+        self.ctx = ctypes.c_void_p()
+        rc = self.L.orloj_create(ctypes.byref(self.ctx), self.device.index,
+                                 ctypes.c_void_p(st.cuda_stream))
+        if rc:
+            raise OrlojError(rc, "orloj_create failed")
+
+    def __del__(self):
+        import sys
+        if getattr(self, "ctx", None) and self.ctx.value and not sys.is_finalizing():
+            self.L.orloj_destroy(self.ctx)
+            self.ctx = None
+
+    def _check(self, rc: int):
+        if rc:
+            raise OrlojError(rc, self.L.orloj_last_error(self.ctx).decode())
+
+    def set_stream(self, stream: torch.cuda.Stream):
+        self._check(self.L.orloj_set_stream(self.ctx, ctypes.c_void_p(stream.cuda_stream)))
+
+    def sync(self):
+        self._check(self.L.orloj_sync(self.ctx))
+
+    # -- orloj_build_cdfs ------------------------------------------------------
+    def build_cdfs(self, counts: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """counts [..., K] (uint32 stored as int32 or uint32) -> log2 CDF float32."""
+        _need_cuda(counts, "counts", (torch.int32, torch.uint32), self.device)
+        K = counts.shape[-1]
+        if out is None:
+            out = torch.empty(counts.shape, dtype=torch.float32, device=self.device)
+        _need_cuda(out, "out", (torch.float32,), self.device)
+        if out.shape != counts.shape:
+            raise ValueError("out must have the shape of counts")
+        rows = counts.numel() // K if K else 0
+        self._check(self.L.orloj_build_cdfs(self.ctx, rows, K, _ptr(counts), _ptr(out)))
+        return out
+
+
+def make_grid(n_models, n_classes, n_bins, batch_sizes: np.ndarray,
+              d_bin_width_ms: Optional[torch.Tensor]):
+    bs = np.ascontiguousarray(batch_sizes, dtype=np.int32)
+    g = Grid(int(n_models), int(n_classes), int(n_bins), int(bs.size),
+             bs.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), _ptr(d_bin_width_ms))
+    g._keep = bs
+    return g
+
+
+def make_queues(h_queue_off: np.ndarray, d_queue_off, d_class, d_deadline_ms, d_now_ms):
+    ho = np.ascontiguousarray(h_queue_off, dtype=np.int64)
+    qs = Queues(ho.ctypes.data_as(_I64P), _ptr(d_queue_off), _ptr(d_class), _ptr(d_deadline_ms),
+                _ptr(d_now_ms))
+    qs._keep = ho
+    return qs
+
+
+def output_sizes(grid: Grid, queues: Queues, prefix_mode: int = PREFIX_TRIANGLE):
+    """(n_cands, n_probs, cand_off[M+1], prob_off[M+1]) computed by the
+    library on the host."""
+    L = load()
+    M = grid.n_models
+    nc = ctypes.c_int64()
+    npb = ctypes.c_int64()
+    co = np.zeros(M + 1, np.int64)
+    po = np.zeros(M + 1, np.int64)
+    rc = L.orloj_output_sizes(ctypes.byref(grid), ctypes.byref(queues), prefix_mode,
+                              ctypes.byref(nc), ctypes.byref(npb), co.ctypes.data_as(_I64P),
+                              po.ctypes.data_as(_I64P))
+    if rc:
+        raise OrlojError(rc, "orloj_output_sizes rejected its arguments")
+    return nc.value, npb.value, co, po
+
+
+class Scorer:
+    """A workload resident in HBM plus its output buffers: uploads the
+    histograms and queues once, then builds the log2 CDF tables, scores all
+    candidates and selects a batch per model through the C ABI."""
+
+    def __init__(self, wl, ctx: Optional[Context] = None, prefix_mode: int = PREFIX_TRIANGLE,
+                 counts_device: Optional[torch.Tensor] = None):
+        self.ctx = ctx or Context()
+        self.wl = wl
+        self.mode = prefix_mode
+        dev = self.ctx.device
+        if counts_device is not None:
+            self.counts = counts_device
+        else:
+            self.counts = torch.from_numpy(np.ascontiguousarray(wl.counts).view(np.int32)).to(dev)
+        self.log2cdf = torch.empty(self.counts.shape, dtype=torch.float32, device=dev)
+        self.width = torch.from_numpy(np.ascontiguousarray(wl.bin_width_ms, np.float64)).to(dev)
+        self.grid = make_grid(wl.n_models, wl.n_classes, wl.n_bins, wl.batch_sizes, self.width)
+        self.set_queues(wl.queue_off, wl.cls, wl.deadline_ms, wl.now_ms)
+        M = wl.n_models
+        self.sel_n = torch.zeros(M, dtype=torch.int32, device=dev)
+        self.sel_bs = torch.zeros(M, dtype=torch.int32, device=dev)
+        self.sel_score = torch.zeros(M, dtype=torch.float32, device=dev)
+
+    def set_queues(self, queue_off, cls, deadline_ms, now_ms):
+        dev = self.ctx.device
+        self.h_queue_off = np.ascontiguousarray(queue_off, np.int64)
+        self.d_queue_off = torch.from_numpy(self.h_queue_off).to(dev)
+        self.d_class = torch.from_numpy(np.ascontiguousarray(cls, np.int32)).to(dev)
+        self.d_deadline = torch.from_numpy(np.ascontiguousarray(deadline_ms, np.float64)).to(dev)
+        self.d_now = torch.from_numpy(np.ascontiguousarray(now_ms, np.float64)).to(dev)
+        self.queues = make_queues(self.h_queue_off, self.d_queue_off, self.d_class,
+                                  self.d_deadline, self.d_now)
+        self.n_cands, self.n_probs, self.h_cand_off, self.h_prob_off = output_sizes(
+            self.grid, self.queues, self.mode)
+        self.d_cand_off = torch.from_numpy(self.h_cand_off).to(dev)
+        self.d_prob_off = torch.from_numpy(self.h_prob_off).to(dev)
+        self.finish_prob = torch.empty(max(self.n_probs, 1), dtype=torch.float32, device=dev)
+        self.expected_finish = torch.empty(max(self.n_cands, 1), dtype=torch.float64, device=dev)
+        self.expected_latency = torch.empty(max(self.n_cands, 1), dtype=torch.float32, device=dev)
+        self.score_out = torch.empty(max(self.n_cands, 1), dtype=torch.float32, device=dev)
+
+    # -- the three entry points --------------------------------------------------
+    def build(self):
+        self.ctx.build_cdfs(self.counts, self.log2cdf)
+
+    def score(self, b_expo: Optional[float] = None):
+        b = self.wl.b_expo if b_expo is None else b_expo
+        c = self.ctx
+        c._check(c.L.orloj_score_candidates(
+            c.ctx, ctypes.byref(self.grid), _ptr(self.log2cdf), ctypes.byref(self.queues),
+            float(b), self.mode, _ptr(self.d_cand_off), _ptr(self.d_prob_off),
+            _ptr(self.finish_prob), _ptr(self.expected_finish), _ptr(self.expected_latency),
+            _ptr(self.score_out)))
+
+    def select(self):
+        c = self.ctx
+        c._check(c.L.orloj_select_batch(
+            c.ctx, ctypes.byref(self.grid), ctypes.byref(self.queues), self.mode,
+            _ptr(self.d_cand_off), _ptr(self.score_out), _ptr(self.sel_n), _ptr(self.sel_bs),
+            _ptr(self.sel_score)))
+
+    def run(self, build: bool = True, b_expo: Optional[float] = None) -> dict:
+        if build:
+            self.build()
+        self.score(b_expo)
+        self.select()
+        self.ctx.sync()
+        return self.fetch()
+
+    def fetch(self) -> dict:
+        torch.cuda.synchronize(self.ctx.device)
+        return dict(
+            finish_prob=self.finish_prob[:self.n_probs].cpu().numpy(),
+            expected_finish=self.expected_finish[:self.n_cands].cpu().numpy(),
+            expected_latency_ms=self.expected_latency[:self.n_cands].cpu().numpy(),
+            score=self.score_out[:self.n_cands].cpu().numpy(),
+            sel_n=self.sel_n.cpu().numpy(), sel_bs=self.sel_bs.cpu().numpy(),
+            sel_score=self.sel_score.cpu().numpy())

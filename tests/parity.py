@@ -1,0 +1,96 @@
+"""Element-wise comparison of the HIP path with the CPU oracle.
+
+Bars (fp32 outputs against the fp64 oracle):
+  finish probabilities P           |dP| <= 1e-5
+  expected finish counts           |dE| <= 1e-5
+  expected batch latency E[L_B]    |dEL| <= 1e-5 * EL   (fp32 sums of K terms)
+  priority score                   |dS| <= 1e-6 + 1e-5 * |S|
+  selections                       identical, unless the oracle's two best
+                                   scores are closer than 1e-5 (then the
+                                   GPU's pick must score within 1e-5 of the
+                                   oracle's best)
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+
+TOL_P = 1e-5
+TOL_E = 1e-5
+TOL_EL_REL = 1e-5
+TOL_S_ABS = 1e-6
+TOL_S_REL = 1e-5
+TIE = 1e-5
+
+
+def candidates(wl, q, mode):
+    """(n, batch size) of model q's candidates in output order."""
+    N = wl.queue_len(q)
+    out = []
+    for b in wl.batch_sizes:
+        cap = N if mode else min(int(b), N)
+        out += [(n, int(b)) for n in range(1, cap + 1)]
+    return out
+
+
+def check_selection(wl, q, mode, ora_scores, gpu_sel):
+    """ora_scores: oracle scores of model q's candidates (output order)."""
+    cands = candidates(wl, q, mode)
+    valid = [(s, n, b) for s, (n, b) in zip(ora_scores, cands) if n <= b]
+    if not valid:
+        assert gpu_sel == (0, 0), (q, gpu_sel)
+        return
+    order = sorted(valid, key=lambda t: (t[0], t[1], -t[2]), reverse=True)
+    best = order[0]
+    second = order[1][0] if len(order) > 1 else -np.inf
+    if best[0] <= 0.0:
+        if gpu_sel != (0, 0):     # only a near-zero best may flip to a pick
+            assert best[0] > -TIE
+            s = dict(((n, b), s) for s, n, b in valid)[gpu_sel]
+            assert s >= best[0] - TIE
+        return
+    if best[0] - second >= TIE and best[0] >= TIE:
+        assert gpu_sel == (best[1], best[2]), (q, gpu_sel, best[1:], best[0], second)
+    else:
+        if gpu_sel == (0, 0):
+            assert best[0] < TIE, (q, best)
+            return
+        s = dict(((n, b), s) for s, n, b in valid)[gpu_sel]
+        assert s >= best[0] - TIE, (q, gpu_sel, s, best)
+
+
+def compare(wl, gpu: dict, ora: dict, mode: int = 0, models=None, cand_off=None, prob_off=None):
+    """Compare all outputs; ``models`` restricts the check to a subset (the
+    oracle dict then holds only those models, in order).  Returns the max
+    errors seen."""
+    if models is None:
+        models = list(range(wl.n_models))
+        g = gpu
+    else:
+        co, po = cand_off, prob_off
+        g = {k: np.concatenate([gpu[k][co[q]:co[q + 1]] for q in models])
+             for k in ("expected_finish", "expected_latency_ms", "score")}
+        g["finish_prob"] = np.concatenate([gpu["finish_prob"][po[q]:po[q + 1]] for q in models])
+    err = {}
+    dP = np.abs(g["finish_prob"].astype(np.float64) - ora["finish_prob"])
+    dE = np.abs(g["expected_finish"] - ora["expected_finish"])
+    el = ora["expected_latency_ms"]
+    dEL = np.abs(g["expected_latency_ms"].astype(np.float64) - el)
+    sc = ora["score"]
+    dS = np.abs(g["score"].astype(np.float64) - sc)
+    err["P"] = float(dP.max(initial=0.0))
+    err["E"] = float(dE.max(initial=0.0))
+    err["EL_rel"] = float((dEL / np.maximum(el, 1e-300)).max(initial=0.0))
+    err["S"] = float(dS.max(initial=0.0))
+    err["S_excess"] = float((dS - (TOL_S_ABS + TOL_S_REL * np.abs(sc))).max(initial=-1.0))
+    assert np.all(np.isfinite(g["finish_prob"])) and np.all(np.isfinite(g["score"]))
+    assert err["P"] <= TOL_P, err
+    assert err["E"] <= TOL_E, err
+    assert err["EL_rel"] <= TOL_EL_REL, err
+    assert err["S_excess"] <= 0.0, err
+    for i, q in enumerate(models):
+        po = ora["per_model"][i]
+        check_selection(wl, q, mode, po["score"],
+                        (int(gpu["sel_n"][q]), int(gpu["sel_bs"][q])))
+    return err
