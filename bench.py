@@ -2,10 +2,10 @@
 
 One step = one scheduling pass of the hot path over every model of the
 workload: orloj_score_candidates (scan over queue position of the members'
-log2 CDF rows, batch CDF, E[L_B], finish probabilities, priorities) and
-orloj_select_batch (one batch per model).  The log2 CDF tables are built
-once before timing (orloj_build_cdfs refreshes profiles off the scheduling
-path) and timed on their own.  Inputs are resident in HBM when the timed
+CDF rows into the batch CDF, E[L_B], finish probabilities, priorities) and
+orloj_select_batch (one batch per model).  The CDF tables are built once
+before timing (orloj_build_cdfs refreshes profiles off the scheduling path)
+and timed on their own.  Inputs are resident in HBM when the timed
 region starts.
 
 Default workload: configuration 5 in its saturated decision state (128
@@ -33,7 +33,7 @@ HBM_PEAK_GBS = 8000.0
 
 
 def algorithmic_bytes(wl, mode=0):
-    """Bytes one score launch must move at least: each distinct log2 CDF row
+    """Bytes one score launch must move at least: each distinct CDF row
     a (model, batch size) workgroup reads, each queued request read once
     (class + deadline), the per-model scalars, and every output."""
     K = wl.n_bins
@@ -96,6 +96,9 @@ def main():
     ap.add_argument("--cpu-models", type=int, default=24)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workers", type=int, default=16)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="after timing, copy a 1 GiB buffer once (a plain copy kernel of "
+                         "known size, for scaling HBM traffic counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: the scorer has no multi-GPU path "
@@ -175,6 +178,14 @@ def main():
         build_cdfs_gbs=round(wl.counts.nbytes * 2 / (build_ms * 1e-3) / 1e9, 1),
         roofline=roof,
     )
+    if args.calibrate_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        line["calibration_copy_bytes"] = src.numel() * 4
+        del src, dst
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(args.config, args.cpu_models)

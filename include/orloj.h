@@ -5,7 +5,7 @@
  * distributions of request execution time, the hot path of Orloj
  * ("Predictably Serving Unpredictable DNNs", arXiv 2209.00159):
  *
- *   orloj_build_cdfs        histogram -> log2 CDF table
+ *   orloj_build_cdfs        histogram -> complementary CDF table
  *   orloj_output_sizes      host-side sizing of the per-candidate outputs
  *   orloj_score_candidates  every prefix candidate at every batch size:
  *                           batch CDF, E[L_B], finish probabilities,
@@ -106,18 +106,20 @@ typedef struct orloj_queues {
 } orloj_queues;
 
 /*
- * Histogram -> log-CDF table (§4.2.1: the CDF of a request's latency is read
- * off its histogram).  For each of n_rows rows of n_bins uint32 counts:
- *   d_log2cdf[r][k] = log2 F(x_{k+1}),  F(x_{k+1}) = (counts[0..k] summed) / total,
- * so entry n_bins-1 is exactly 0, entries with F = 0 are -inf.  The running
- * sums are exact 64-bit integers; the log keeps relative accuracy near
- * F = 1 (it is taken of 1 - tail/total there).  Rows are laid out
+ * Histogram -> CDF table (§4.2.1: the CDF of a request's latency is read off
+ * its histogram), stored as its complement.  For each of n_rows rows of
+ * n_bins uint32 counts:
+ *   d_ccdf[r][k] = 1 - F(x_{k+1}) = (total - counts[0..k] summed) / total,
+ * the probability that the latency exceeds the right edge of bin k.  Entry
+ * n_bins-1 is exactly 0.  The running sums are exact 64-bit integers and the
+ * complement keeps full relative precision where F is near 1, which the
+ * batch CDF (a product of many member CDFs) needs.  Rows are laid out
  * [model][batch size][class][bin] for orloj_score_candidates.  A row with
- * total 0 is a data error (its entries are written as NaN).
- * d_counts and d_log2cdf must not overlap.
+ * total 0 is a data error (its entries are written as NaN).  d_counts and
+ * d_ccdf must not overlap.
  */
 int orloj_build_cdfs(orloj_ctx *ctx, int64_t n_rows, int32_t n_bins,
-                     const uint32_t *d_counts, float *d_log2cdf);
+                     const uint32_t *d_counts, float *d_ccdf);
 
 /*
  * Output sizing (host only, no launch).  For model q with queue length N_q
@@ -149,13 +151,13 @@ int orloj_output_sizes(const orloj_grid *grid, const orloj_queues *queues,
  *               d_expected_finish[cand]   = sum_m P_m      (double)
  *               d_expected_latency_ms[cand] = E[L_B]       (float)
  *               d_score[cand]             = sum_m p_m      (float)
- * d_log2cdf is the [M][n_bs][C][K] table of orloj_build_cdfs.  d_cand_off /
+ * d_ccdf is the [M][n_bs][C][K] table of orloj_build_cdfs.  d_cand_off /
  * d_prob_off are device copies of orloj_output_sizes' offsets.  Output
  * buffers hold at least n_cands / n_probs elements.  b_expo_per_ms must be
  * finite and > 0 (the paper uses 1e-4 per ms, §4.4).
  * ORLOJ_E_UNSUPPORTED when a prefix would exceed ORLOJ_MAX_PREFIX.
  */
-int orloj_score_candidates(orloj_ctx *ctx, const orloj_grid *grid, const float *d_log2cdf,
+int orloj_score_candidates(orloj_ctx *ctx, const orloj_grid *grid, const float *d_ccdf,
                            const orloj_queues *queues, double b_expo_per_ms,
                            int32_t prefix_mode, const int64_t *d_cand_off,
                            const int64_t *d_prob_off, float *d_finish_prob,

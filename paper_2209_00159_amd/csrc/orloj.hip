@@ -4,16 +4,16 @@
 // ("Predictably Serving Unpredictable DNNs", arXiv 2209.00159) as three
 // hand-written HIP kernels for CDNA4:
 //
-//   cdf_kernel     histogram rows -> log2 CDF (exact 64-bit running sums)
+//   cdf_kernel     histogram rows -> 1 - CDF (exact 64-bit running sums)
 //   score_kernel   one workgroup per (model, batch size): scan over queue
-//                  position of the members' log2 CDF rows, 2^S = batch CDF,
+//                  position of the members' CDF rows into the batch CDF,
 //                  E[L_B], finish probabilities and Eq. (2) priorities of
 //                  every prefix candidate, all in one pass
 //   select_kernel  one workgroup per model: argmax over its candidates
 //
 // The work is a scan plus reductions over HBM-resident tables, not a dense
-// contraction, so it runs on the vector ALUs (no MFMA): coalesced row
-// loads, fp64 running sums in registers, wave64 shuffle scans and
+// contraction, so it runs on the vector ALUs (no MFMA): row loads
+// prefetched into registers, fp64 running products, wave64 DPP scans and
 // reductions, and LDS for the per-step snapshot the member lookups read.
 
 #include <hip/hip_runtime.h>
@@ -26,7 +26,7 @@
 
 #include <new>
 
-#include "../../include/orloj.h"
+#include "/root/repo/include/orloj.h"
 
 namespace {
 
@@ -39,8 +39,6 @@ constexpr int kErrClassRange = 2;
 constexpr int kErrDeadlineNaN = 4;
 constexpr int kErrUnsorted = 8;
 constexpr int kErrNowNaN = 16;
-
-constexpr float kLog2e = 1.4426950408889634f;
 
 // ---------------------------------------------------------------------------
 // wave64 helpers
@@ -57,20 +55,15 @@ __device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t x, int lane) {
 // ---------------------------------------------------------------------------
 // cdf_kernel: one workgroup per histogram row.  Thread t owns the VPT
 // consecutive bins [t*VPT, t*VPT + VPT): it loads them once, the workgroup
-// scans the per-thread sums (64-bit, exact), and each thread turns its
-// running sums into log2 F.
+// scans the per-thread sums (64-bit, exact), and each thread writes the
+// complementary CDF 1 - F(x_{k+1}) = (total - running sum) / total.  The
+// complement keeps full relative precision where F is close to 1, which is
+// where the batch CDF (a product over up to hundreds of members) is most
+// sensitive.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float log2_cdf(uint64_t cum, uint64_t tot, double rtot) {
-    if (cum == 0) return -INFINITY;
+__device__ __forceinline__ float survival(uint64_t cum, uint64_t tot, double rtot) {
     if (cum >= tot) return 0.0f;
-    if (2 * cum <= tot) {
-        // F <= 1/2: |log2 F| >= 1, so the rounding of F costs < 1 ulp.
-        return log2f((float)((double)cum * rtot));
-    }
-    // F > 1/2: take log of 1 - tail/total so that F near 1 keeps its
-    // relative accuracy.
-    const float qf = (float)((double)(tot - cum) * rtot);
-    return log1pf(-qf) * kLog2e;
+    return (float)((double)(tot - cum) * rtot);
 }
 
 template <int VPT>
@@ -122,7 +115,7 @@ __global__ __launch_bounds__(kThreads) void cdf_kernel(const uint32_t* __restric
 #pragma unroll
         for (int j = 0; j < VPT; ++j) {
             cum += v[j];
-            o[j] = log2_cdf(cum, tot, rtot);
+            o[j] = survival(cum, tot, rtot);
         }
         if (vec && base + VPT <= K) {
 #pragma unroll
@@ -204,7 +197,7 @@ __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2
 // score_kernel
 // ---------------------------------------------------------------------------
 struct ScoreArgs {
-    const float* tab;          // [M][nbs][C][K] log2 F(x_{k+1})
+    const float* tab;          // [M][nbs][C][K] 1 - F(x_{k+1})
     const int64_t* queue_off;  // [M+1]
     const int32_t* cls;        // [N]
     const double* deadline;    // [N]
@@ -222,28 +215,71 @@ struct ScoreArgs {
     int bs[ORLOJ_MAX_BATCH_SIZES];
 };
 
-// Per-member data kept in LDS for the whole scan.
+// Per-member lookup plan, built once per workgroup in LDS (it depends on
+// the deadline only, not on the step).  For member m with deadline bin k
+// and offset theta, every step the member wave reads from the snapshot
+//   gk  = G(x_k) (bin k-1),   gk1 = G(x_{k+1}) (bin k),
+// and assembles the discounted prefix Z(k-2) = sum_{i <= k-2} G(x_{i+1}) d^(k-2-i)
+// from the wave prefixes, the lane prefix A, the quarter-end value of the
+// thread's chunk and the G values of one 4-bin quarter:
+//   zq  = fb * (fa * pre[wsel] + A[la]) + fq * zqe[izq] + sum_r wq[r] g4[r]
+// then combines with fixed coefficients:
+//   P   = gk + theta (gk1 - gk)
+//   num = cg * (gk - omd * zq) + psi (gk1 - gk)
+// An index of -1 reads as 0; beyond-the-grid members add one = 1 to both G
+// values.  Dead requests and the k < 2 edge cases need no branch.
 struct Member {
-    int k;        // bin of the deadline; -1 passed; >= K beyond the grid
     int cls;      // class id (clamped into range)
+    int ig0;      // snapshot index of G(x_k)     (-1: k = 0, dead or beyond)
+    int ig1;      // snapshot index of G(x_{k+1}) (-1: dead or beyond)
+    int ig4;      // float4 slot of the quarter holding bin k-2 (-1: k < 2 or dead)
+    int izq;      // quarter-end snapshot index before that quarter (-1: none)
+    int la;       // lane whose wave-internal scan precedes bin k-2 (-1: none)
+    int wsel;     // which wave prefix (0: none, 1..3)
+    float fa;     // d^(CPL (la - 64 wsel + 1)): weight of the wave prefix
+    float fb;     // d^(j+1): weight of the lane prefix at bin k-2 (j = its chunk offset)
+    float fq;     // d^(r+1): weight of the previous quarter end (r = offset in quarter)
+    float wq[4];  // d^(r - r') for r' <= r, else 0
     float theta;  // position inside bin k
-    float decay;  // exp(-b theta w), or exp(-b (tau - K w)) beyond the grid
+    float cg;     // gamma * exp(-b theta w), or gamma * exp(-b (tau - K w))
     float psi;    // (1 - exp(-b theta w)) / (b w)
+    float one;    // 1 for beyond-the-grid members (P = 1), else 0
 };
 
 // LDS layout of one workgroup (floats unless noted):
-//   g[2][256 CPL]  batch CDF G(x_{k+1}) of the current prefix, by step parity
-//   z[2][256 CPL]  in-chunk discounted running sums of g
-//   A[2][256]      wave-internal discounted scan of the chunk totals
-//   e[2][4]        per-wave sums of (1 - g)
-//   mem[maxcap]    Member
+//   g[2][256 CPL]   batch CDF G(x_{k+1}) of the current prefix, by step parity
+//   zqe[2][256 NQ]  in-chunk discounted prefix of g at each quarter end
+//   A[2][256]       wave-internal discounted scan of the chunk totals
+//   e[2][4]         per-wave sums of (1 - g)
+//   mem[maxcap]     Member
+// g is stored float4-interleaved: the j-th float4 of thread t's chunk sits
+// at float4 slot j * 256 + t, so a wave's snapshot stores are contiguous
+// (no bank conflicts) and bin k is found by snap_index().
+template <int CPL>
+struct Quarters {
+    static constexpr int QW = CPL < 4 ? CPL : 4;   // bins per quarter
+    static constexpr int NQ = CPL / QW;            // quarters per thread
+};
+
 template <int CPL>
 __host__ __device__ constexpr size_t score_smem_floats() {
-    return 4 * (size_t)kThreads * CPL + 2 * kThreads + 2 * kWaves;
+    // + 8 padding keeps Member 16-byte aligned
+    return 2 * (size_t)kThreads * CPL + 2 * (size_t)kThreads * Quarters<CPL>::NQ +
+           2 * kThreads + 2 * kWaves + 8;
+}
+
+template <int CPL>
+__device__ __forceinline__ int snap_index(int k) {
+    if constexpr (CPL >= 4) {
+        const int t = k / CPL, j = k - t * CPL;
+        return ((j >> 2) * kThreads + t) * 4 + (j & 3);
+    } else {
+        return k;
+    }
 }
 
 // Branch-free load of one thread's CPL bins of a row.  EXACT: the row
-// fills the workgroup (K = 256 CPL), so the loads are whole float4s.
+// fills the sweep waves (K = 256 CPL), so the loads are whole float4s.
 // Otherwise indices past the end of the row are clamped to a valid address
 // and their values are masked at use.  Every load is issued
 // unconditionally so the prefetch ring keeps fixed registers.
@@ -264,22 +300,31 @@ __device__ __forceinline__ void load_chunk(float (&v)[CPL], const float* __restr
 }
 
 // One workgroup scores every prefix of one model's queue at one batch size.
-// Thread t owns the CPL consecutive bins [t CPL, t CPL + CPL) and keeps the
-// fp64 running sums S_n(k) = sum_{i <= n} log2 F_{c_i}(x_{k+1}) for them.
-// Step n: add member n's row (prefetched PF steps earlier), G = 2^S, the
-// per-thread sums of (1 - G) and of discounted G, and a snapshot of G and
-// the discounted prefix in LDS.  One barrier later, wave n mod 4 reads the
-// snapshot to score the n+1 members and writes the candidate's outputs,
-// while the other waves already run step n+1 on the other snapshot buffer.
+// Waves 0-3 (the sweep waves) own the bins: thread t keeps the batch CDF
+// G_n(x_{k+1}) = prod_{i <= n} F_{c_i}(x_{k+1}) of its CPL consecutive bins
+// as an fp64 running product (the table holds 1 - F, so a step is one fma).
+// Step n: fold in member n's row (prefetched PF steps earlier), the
+// per-thread sums of (1 - G) and of discounted G (split into 4-bin quarters
+// so the dependency chains stay short), and a snapshot of G and of the
+// quarter-end discounted prefixes in LDS, then one LDS barrier.  Wave 4 (the
+// member wave) reads that snapshot after the barrier, scores the n+1
+// members and writes the candidate's outputs while the sweep waves run
+// step n+1 into the other snapshot buffer.  Only the member wave stores to
+// global memory, so the sweep waves' outstanding-load counts stay exact and
+// the prefetch ring is never drained early.
+constexpr int kScoreThreads = kThreads + 64;
+
 template <int CPL, int PF, bool EXACT>
-__global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
+__global__ __launch_bounds__(kScoreThreads) void score_kernel(const ScoreArgs a) {
+    using Q = Quarters<CPL>;
     extern __shared__ __align__(16) float smem[];
     constexpr int KP = kThreads * CPL;
+    constexpr int QP = kThreads * Q::NQ;
     float* s_g = smem;
-    float* s_z = s_g + 2 * KP;
-    float* s_A = s_z + 2 * KP;
+    float* s_zq = s_g + 2 * KP;
+    float* s_A = s_zq + 2 * QP;
     float* s_e = s_A + 2 * kThreads;
-    Member* s_mem = reinterpret_cast<Member*>(s_e + 2 * kWaves);
+    Member* s_mem = reinterpret_cast<Member*>(s_e + 2 * kWaves + 8);
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
 
@@ -293,22 +338,21 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
     if (cap64 <= 0 || cap64 > a.maxcap) return;   // the host sizes maxcap
     const int ncap = (int)cap64;
 
-    int64_t cand = a.cand_off[q], prob = a.prob_off[q];
-    for (int j = 0; j < bi; ++j) {
-        const int64_t c = a.rect ? N : (N < a.bs[j] ? N : (int64_t)a.bs[j]);
-        cand += c;
-        prob += c * (c + 1) / 2;
-    }
-
     const double w = a.width[q];
     const double nowq = a.now[q];
     const double b = a.b;
     const double bw = b * w;
     const int K = a.K;
 
-    // Members: bin, offset and delay factors of each deadline (fp64 time,
-    // relative to now).
-    for (int m = tid; m < ncap; m += kThreads) {
+    // Per-bin discount d = exp(-b w) and the powers the scans need.
+    const float d = (float)exp(-bw);
+    const float log2d = (float)(-bw * 1.4426950408889634);
+    const int nsteps = (ncap + PF - 1) / PF * PF;
+    const float gamma = (float)(-expm1(-bw) / bw);   // (1 - d) / (b w)
+
+    // Members: bin and offset of each deadline (fp64 time, relative to
+    // now) and their lookup plans.
+    for (int m = tid; m < ncap; m += kScoreThreads) {
         int c = a.cls[q0 + m];
         const double D = a.deadline[q0 + m];
         int flag = 0;
@@ -319,160 +363,208 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const ScoreArgs a) {
         if (flag) atomicOr(a.err, flag);
         Member mb;
         mb.cls = c;
-        mb.theta = 0.0f;
-        mb.decay = 0.0f;
-        mb.psi = 0.0f;
+        mb.ig0 = mb.ig1 = mb.ig4 = mb.izq = mb.la = -1;
+        mb.wsel = 0;
+        mb.fa = mb.fb = mb.fq = 0.0f;
+        mb.wq[0] = mb.wq[1] = mb.wq[2] = mb.wq[3] = 0.0f;
+        mb.theta = mb.cg = mb.psi = mb.one = 0.0f;
         const double tau = D - nowq;
-        if (!(tau > 0.0)) {
-            mb.k = -1;
-        } else {
+        int kz = -1;   // bin whose discounted prefix Z the priority needs
+        if (tau > 0.0) {
             const double u = tau / w;
-            if (u >= (double)K) {
-                mb.k = K;
-                mb.decay = (float)exp(-b * (tau - (double)K * w));
+            if (u >= (double)K) {                  // beyond the grid: P = 1
+                mb.one = 1.0f;
+                mb.cg = gamma * (float)exp(-b * (tau - (double)K * w));
+                kz = K - 2;
             } else {
                 const double kf = floor(u);
                 const double th = u - kf;
-                mb.k = (int)kf;
+                const int k = (int)kf;
                 mb.theta = (float)th;
-                mb.decay = (float)exp(-b * th * w);
+                mb.cg = gamma * (float)exp(-b * th * w);
                 mb.psi = (float)(-expm1(-b * th * w) / bw);
+                mb.ig1 = snap_index<CPL>(k);
+                if (k >= 1) mb.ig0 = snap_index<CPL>(k - 1);
+                kz = k - 2;
+            }
+        }
+        if (kz >= 0) {
+            const int L = kz / CPL, j = kz - L * CPL;
+            const int qq = j / Q::QW, r = j - qq * Q::QW;
+            mb.ig4 = (qq * kThreads + L) * Q::QW;          // start of the quarter's G values
+            if (qq > 0) mb.izq = L * Q::NQ + qq - 1;
+            mb.fq = exp2f(log2d * (float)(r + 1));
+            for (int rr = 0; rr <= r; ++rr) mb.wq[rr] = exp2f(log2d * (float)(r - rr));
+            mb.fb = exp2f(log2d * (float)(j + 1));
+            if (L > 0) {
+                const int Lp = L - 1, wl = Lp >> 6;
+                mb.la = Lp;
+                mb.wsel = wl;
+                mb.fa = exp2f(log2d * (float)(CPL * (Lp - 64 * wl + 1)));
             }
         }
         s_mem[m] = mb;
     }
 
-    // Per-bin discount d = exp(-b w) and the powers the scans need.
-    const float d = (float)exp(-bw);
-    const float omd = (float)(-expm1(-bw));          // 1 - d
-    const float gamma = (float)(-expm1(-bw) / bw);   // (1 - d) / (b w)
-    const float log2d = (float)(-bw * 1.4426950408889634);
-    float rp[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) rp[i] = exp2_hw(log2d * (float)(CPL << i));
-    const float w15 = exp2_hw(log2d * (float)(CPL * ((lane & 15) + 1)));
-    const float w31 = exp2_hw(log2d * (float)(CPL * (lane >= 32 ? lane - 31 : 0)));
-    const float d64c = exp2_hw(log2d * (float)(64 * CPL));
-
     lds_barrier();
 
-    const int base = tid * CPL;
-    const float* tab_qb = a.tab + ((size_t)q * (size_t)a.nbs + (size_t)bi) * (size_t)a.C * (size_t)K;
-    double Sacc[CPL];
+    if (wv < kWaves) {
+        // ======================= sweep waves =======================
+        float rp[4];
 #pragma unroll
-    for (int j = 0; j < CPL; ++j) Sacc[j] = 0.0;
-
-    // Prefetch ring: buf[i] holds the row of step n0 + i.  The tail is padded
-    // to a multiple of PF with ghost steps (their rows repeat the last
-    // member's and they write nothing).
-    float buf[PF][CPL];
+        for (int i = 0; i < 4; ++i) rp[i] = exp2_hw(log2d * (float)(CPL << i));
+        const float w15 = exp2_hw(log2d * (float)(CPL * ((lane & 15) + 1)));
+        const float w31 = exp2_hw(log2d * (float)(CPL * (lane >= 32 ? lane - 31 : 0)));
+        const float dQ = exp2_hw(log2d * (float)Q::QW);
+        const int base = tid * CPL;
+        const float* tab_qb =
+            a.tab + ((size_t)q * (size_t)a.nbs + (size_t)bi) * (size_t)a.C * (size_t)K;
+        double Gacc[CPL];   // G(x_{k+1}) of the current prefix, fp64 running product
 #pragma unroll
-    for (int i = 0; i < PF; ++i)
-        load_chunk<CPL, EXACT>(buf[i], tab_qb + (size_t)s_mem[min(i, ncap - 1)].cls * (size_t)K, base, K);
-    const int nsteps = (ncap + PF - 1) / PF * PF;
+        for (int j = 0; j < CPL; ++j) Gacc[j] = 1.0;
 
-    for (int n0 = 0; n0 < nsteps; n0 += PF) {
+        // Prefetch ring: buf[i] holds the row of step n0 + i.  The tail is
+        // padded to a multiple of PF with ghost steps (their rows repeat the
+        // last member's and nobody reads their snapshot).
+        float buf[PF][CPL];
 #pragma unroll
         for (int i = 0; i < PF; ++i) {
-            const int n = n0 + i;
-            {
+            load_chunk<CPL, EXACT>(buf[i], tab_qb + (size_t)s_mem[min(i, ncap - 1)].cls * (size_t)K,
+                                   base, K);
+            // keep the priming loads in ring order, as the loop issues them
+            __builtin_amdgcn_sched_barrier(0);
+        }
+
+        for (int n0 = 0; n0 < nsteps; n0 += PF) {
+#pragma unroll
+            for (int i = 0; i < PF; ++i) {
+                const int n = n0 + i;
                 const int par = n & 1;
                 float* g_out = s_g + par * KP;
-                float* z_out = s_z + par * KP;
-                // ---- scan step n
-                float e = 0.0f, z = 0.0f;
-                float gv[CPL], zv[CPL];
+                // G <- G * F = G - G (1 - F), in fp64; per-quarter sums
+                double gs[Q::QW];
+                float zqv[Q::NQ];
+                float gv[CPL];
 #pragma unroll
-                for (int j = 0; j < CPL; ++j) {
-                    const float x = (EXACT || base + j < K) ? buf[i][j] : 0.0f;
-                    Sacc[j] += (double)x;
-                    const float g = exp2_hw((float)Sacc[j]);
-                    e += 1.0f - g;
-                    z = fmaf(z, d, g);
-                    gv[j] = g;
-                    zv[j] = z;
+                for (int r = 0; r < Q::QW; ++r) gs[r] = 0.0;
+#pragma unroll
+                for (int qq = 0; qq < Q::NQ; ++qq) {
+                    float zz = 0.0f;
+#pragma unroll
+                    for (int r = 0; r < Q::QW; ++r) {
+                        const int j = qq * Q::QW + r;
+                        const float t = (EXACT || base + j < K) ? buf[i][j] : 0.0f;
+                        Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
+                        gs[r] += Gacc[j];
+                        const float g = (float)Gacc[j];
+                        zz = fmaf(zz, d, g);
+                        gv[j] = g;
+                    }
+                    zqv[qq] = zz;
                 }
-                load_chunk<CPL, EXACT>(buf[i],
-                                tab_qb + (size_t)s_mem[min(n + PF, ncap - 1)].cls * (size_t)K,
-                                base, K);
-                if (CPL % 4 == 0) {
+                load_chunk<CPL, EXACT>(
+                    buf[i], tab_qb + (size_t)s_mem[min(n + PF, ncap - 1)].cls * (size_t)K, base, K);
+                // quarter ends of the in-chunk discounted prefix, and its total
+                float zc = 0.0f;
+#pragma unroll
+                for (int qq = 0; qq < Q::NQ; ++qq) {
+                    zc = fmaf(zc, dQ, zqv[qq]);
+                    zqv[qq] = zc;
+                }
+                double gsum = 0.0;
+#pragma unroll
+                for (int r = 0; r < Q::QW; ++r) gsum += gs[r];
+                // sum over this thread's bins of 1 - G (padding bins hold G = 1)
+                const float e = (float)((double)CPL - gsum);
+                if constexpr (CPL >= 4) {
 #pragma unroll
                     for (int j = 0; j < CPL; j += 4) {
-                        *reinterpret_cast<float4*>(g_out + base + j) =
+                        const int slot = ((j >> 2) * kThreads + tid) * 4;
+                        *reinterpret_cast<float4*>(g_out + slot) =
                             make_float4(gv[j], gv[j + 1], gv[j + 2], gv[j + 3]);
-                        *reinterpret_cast<float4*>(z_out + base + j) =
-                            make_float4(zv[j], zv[j + 1], zv[j + 2], zv[j + 3]);
                     }
                 } else {
 #pragma unroll
-                    for (int j = 0; j < CPL; ++j) {
-                        g_out[base + j] = gv[j];
-                        z_out[base + j] = zv[j];
-                    }
+                    for (int j = 0; j < CPL; ++j) g_out[base + j] = gv[j];
+                }
+                float* zq_out = s_zq + par * QP + tid * Q::NQ;
+                if constexpr (Q::NQ == 4) {
+                    *reinterpret_cast<float4*>(zq_out) = make_float4(zqv[0], zqv[1], zqv[2], zqv[3]);
+                } else {
+#pragma unroll
+                    for (int qq = 0; qq < Q::NQ; ++qq) zq_out[qq] = zqv[qq];
                 }
                 const float esum = wave_scan_sum(e);
-                const float A = wave_wscan(z, rp, w15, w31);
+                const float A = wave_wscan(zc, rp, w15, w31);
+
                 s_A[par * kThreads + tid] = A;
                 if (lane == 63) s_e[par * kWaves + wv] = esum;
                 lds_barrier();
-
-                // ---- member lookups for the prefix of n+1 members (one wave)
-                if (n < ncap && wv == (n & (kWaves - 1))) {
-                    const float* g = g_out;
-                    const float* zs = z_out;
-                    const float* As = s_A + par * kThreads;
-                    const float T0 = As[63], T1 = As[127], T2 = As[191];
-                    const float W2 = fmaf(T0, d64c, T1);
-                    const float W3 = fmaf(W2, d64c, T2);
-                    const double es = (double)s_e[par * kWaves + 0] + (double)s_e[par * kWaves + 1] +
-                                      (double)s_e[par * kWaves + 2] + (double)s_e[par * kWaves + 3];
-                    const double el = w * (0.5 + es);
-                    // Z[i] = sum_{i' <= i} g[i'] d^(i - i')
-                    auto zval = [&](int idx) -> float {
-                        const int L = idx / CPL, j = idx - L * CPL;
-                        float prev = 0.0f;
-                        if (L > 0) {
-                            const int Lp = L - 1, wl = Lp >> 6;
-                            const float wpre = wl == 0 ? 0.0f : (wl == 1 ? T0 : (wl == 2 ? W2 : W3));
-                            prev = fmaf(exp2_hw(log2d * (float)(CPL * (Lp - 64 * wl + 1))), wpre,
-                                        As[Lp]);
-                        }
-                        return fmaf(prev, exp2_hw(log2d * (float)(j + 1)), zs[idx]);
-                    };
-                    const int nn = n + 1;
-                    double pP = 0.0;
-                    float pN = 0.0f;
-                    for (int m = lane; m < nn; m += 64) {
-                        const Member mb = s_mem[m];
-                        float P, num;
-                        if (mb.k < 0) {
-                            P = 0.0f;
-                            num = 0.0f;
-                        } else if (mb.k >= K) {
-                            P = 1.0f;
-                            const float Q = (K >= 2) ? zval(K - 2) : 0.0f;
-                            num = gamma * mb.decay * (1.0f - omd * Q);
-                        } else {
-                            const int k = mb.k;
-                            const float gk = (k >= 1) ? g[k - 1] : 0.0f;
-                            const float gk1 = g[k];
-                            const float h = gk1 - gk;
-                            P = fmaf(mb.theta, h, gk);
-                            const float Q = (k >= 2) ? zval(k - 2) : 0.0f;
-                            num = fmaf(gamma * mb.decay, gk - omd * Q, h * mb.psi);
-                        }
-                        a.P[prob + (int64_t)n * nn / 2 + m] = P;
-                        pP += (double)P;
-                        pN += num;
-                    }
-                    pP = wave_scan_sum64(pP);
-                    pN = wave_scan_sum(pN);
-                    if (lane == 63) {
-                        a.E[cand + n] = pP;
-                        a.EL[cand + n] = (float)el;
-                        a.S[cand + n] = (float)((double)pN / el);
-                    }
+            }
+        }
+    } else {
+        // ======================= member wave =======================
+        const float omd = (float)(-expm1(-bw));          // 1 - d
+        const float d64c = exp2_hw(log2d * (float)(64 * CPL));
+        int64_t cand = a.cand_off[q], prob = a.prob_off[q];
+        for (int j = 0; j < bi; ++j) {
+            const int64_t c = a.rect ? N : (N < a.bs[j] ? N : (int64_t)a.bs[j]);
+            cand += c;
+            prob += c * (c + 1) / 2;
+        }
+        for (int n = 0; n < nsteps; ++n) {
+            lds_barrier();
+            if (n >= ncap) continue;
+            const int par = n & 1;
+            const float* g = s_g + par * KP;
+            const float* zq = s_zq + par * QP;
+            const float* As = s_A + par * kThreads;
+            // discounted totals at the end of waves 0..2
+            const float T0 = As[63], T1 = As[127], T2 = As[191];
+            const float W2 = fmaf(T0, d64c, T1);
+            const float W3 = fmaf(W2, d64c, T2);
+            const double es = (double)s_e[par * kWaves + 0] + (double)s_e[par * kWaves + 1] +
+                              (double)s_e[par * kWaves + 2] + (double)s_e[par * kWaves + 3];
+            const double el = w * (0.5 + es);
+            const int nn = n + 1;
+            double pP = 0.0;
+            float pN = 0.0f;
+            for (int m = lane; m < nn; m += 64) {
+                const Member mb = s_mem[m];
+                const float g0 = g[max(mb.ig0, 0)];
+                const float g1 = g[max(mb.ig1, 0)];
+                const float al0 = As[max(mb.la, 0)];
+                const float zq0 = zq[max(mb.izq, 0)];
+                float g4[4];
+                if constexpr (Q::QW == 4) {
+                    const float4 t4 = *reinterpret_cast<const float4*>(g + max(mb.ig4, 0));
+                    g4[0] = t4.x; g4[1] = t4.y; g4[2] = t4.z; g4[3] = t4.w;
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) g4[r] = r < Q::QW ? g[max(mb.ig4, 0) + r] : 0.0f;
                 }
+                const float gk = (mb.ig0 >= 0 ? g0 : 0.0f) + mb.one;
+                const float gk1 = (mb.ig1 >= 0 ? g1 : 0.0f) + mb.one;
+                const float al = mb.la >= 0 ? al0 : 0.0f;
+                const float zqp = mb.izq >= 0 ? zq0 : 0.0f;
+                const float pre = mb.wsel == 1 ? T0 : (mb.wsel == 2 ? W2 : (mb.wsel == 3 ? W3 : 0.0f));
+                float zin = mb.fq * zqp;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) zin = fmaf(mb.wq[r], g4[r], zin);
+                const float zqv = fmaf(mb.fb, fmaf(mb.fa, pre, al), mb.ig4 >= 0 ? zin : 0.0f);
+                const float h = gk1 - gk;
+                const float P = fmaf(mb.theta, h, gk);
+                const float num = fmaf(mb.cg, fmaf(-omd, zqv, gk), h * mb.psi);
+                a.P[prob + (int64_t)n * nn / 2 + m] = P;
+                pP += (double)P;
+                pN += num;
+            }
+            pP = wave_scan_sum64(pP);
+            pN = wave_scan_sum(pN);
+            if (lane == 63) {
+                a.E[cand + n] = pP;
+                a.EL[cand + n] = (float)el;
+                a.S[cand + n] = (float)((double)pN / el);
             }
         }
     }
@@ -641,9 +733,13 @@ int chunk_per_lane(int K) {
     return c;
 }
 
+#ifndef ORLOJ_SCORE_PREFETCH
+#define ORLOJ_SCORE_PREFETCH 2   // rows in flight per sweep thread at 16+ bins per thread
+#endif
+
 template <int CPL, bool EXACT>
 hipError_t launch_score_v(const ScoreArgs& a, unsigned grid, hipStream_t st) {
-    constexpr int PF = CPL >= 16 ? 2 : 3;
+    constexpr int PF = CPL >= 16 ? ORLOJ_SCORE_PREFETCH : 3;
     const size_t sm = score_smem_floats<CPL>() * sizeof(float) + (size_t)a.maxcap * sizeof(Member);
     static size_t attr_bytes = 0;   // per template instance; device-independent
     if (sm > attr_bytes) {
@@ -652,7 +748,7 @@ hipError_t launch_score_v(const ScoreArgs& a, unsigned grid, hipStream_t st) {
         if (e != hipSuccess) return e;
         attr_bytes = sm;
     }
-    hipLaunchKernelGGL((score_kernel<CPL, PF, EXACT>), dim3(grid), dim3(kThreads), sm, st, a);
+    hipLaunchKernelGGL((score_kernel<CPL, PF, EXACT>), dim3(grid), dim3(kScoreThreads), sm, st, a);
     return hipGetLastError();
 }
 
@@ -738,29 +834,29 @@ int orloj_sync(orloj_ctx* ctx) {
 }
 
 int orloj_build_cdfs(orloj_ctx* ctx, int64_t n_rows, int32_t n_bins, const uint32_t* d_counts,
-                     float* d_log2cdf) {
+                     float* d_ccdf) {
     if (!ctx) return ORLOJ_E_INVALID;
     if (n_rows < 0) return fail(ctx, ORLOJ_E_INVALID, "n_rows < 0");
     if (n_bins < 1) return fail(ctx, ORLOJ_E_INVALID, "n_bins < 1");
     if (n_bins > ORLOJ_MAX_BINS)
         return fail(ctx, ORLOJ_E_UNSUPPORTED, "n_bins %d > %d", n_bins, ORLOJ_MAX_BINS);
     if (n_rows == 0) return ORLOJ_OK;
-    if (!d_counts || !d_log2cdf) return fail(ctx, ORLOJ_E_INVALID, "NULL buffer");
+    if (!d_counts || !d_ccdf) return fail(ctx, ORLOJ_E_INVALID, "NULL buffer");
     const char* cb = (const char*)d_counts;
-    const char* ob = (const char*)d_log2cdf;
+    const char* ob = (const char*)d_ccdf;
     const size_t bytes = (size_t)n_rows * (size_t)n_bins * 4;
     if (cb < ob + bytes && ob < cb + bytes)
-        return fail(ctx, ORLOJ_E_INVALID, "d_counts and d_log2cdf overlap");
+        return fail(ctx, ORLOJ_E_INVALID, "d_counts and d_ccdf overlap");
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
     const int vpt = chunk_per_lane(n_bins);
     switch (vpt) {
-        case 1: e = launch_cdf<1>(d_counts, d_log2cdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
-        case 2: e = launch_cdf<2>(d_counts, d_log2cdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
-        case 4: e = launch_cdf<4>(d_counts, d_log2cdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
-        case 8: e = launch_cdf<8>(d_counts, d_log2cdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
-        case 16: e = launch_cdf<16>(d_counts, d_log2cdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
-        default: e = launch_cdf<32>(d_counts, d_log2cdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
+        case 1: e = launch_cdf<1>(d_counts, d_ccdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
+        case 2: e = launch_cdf<2>(d_counts, d_ccdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
+        case 4: e = launch_cdf<4>(d_counts, d_ccdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
+        case 8: e = launch_cdf<8>(d_counts, d_ccdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
+        case 16: e = launch_cdf<16>(d_counts, d_ccdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
+        default: e = launch_cdf<32>(d_counts, d_ccdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
     }
     if (e != hipSuccess) return hip_fail(ctx, e, "cdf_kernel launch");
     return ORLOJ_OK;
@@ -793,7 +889,7 @@ int orloj_output_sizes(const orloj_grid* grid, const orloj_queues* queues, int32
     return ORLOJ_OK;
 }
 
-int orloj_score_candidates(orloj_ctx* ctx, const orloj_grid* grid, const float* d_log2cdf,
+int orloj_score_candidates(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
                            const orloj_queues* queues, double b_expo_per_ms, int32_t prefix_mode,
                            const int64_t* d_cand_off, const int64_t* d_prob_off,
                            float* d_finish_prob, double* d_expected_finish,
@@ -822,14 +918,14 @@ int orloj_score_candidates(orloj_ctx* ctx, const orloj_grid* grid, const float* 
         return fail(ctx, ORLOJ_E_UNSUPPORTED, "prefix of %lld members > %d",
                     (long long)maxcap, ORLOJ_MAX_PREFIX);
     if (total == 0) return ORLOJ_OK;
-    if (!d_log2cdf || !d_cand_off || !d_prob_off || !d_finish_prob || !d_expected_finish ||
+    if (!d_ccdf || !d_cand_off || !d_prob_off || !d_finish_prob || !d_expected_finish ||
         !d_expected_latency_ms || !d_score)
         return fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
     const int64_t nblk = (int64_t)M * grid->n_bs;
     if (nblk > 0x7fffffff) return fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (model, batch size) pairs");
 
     ScoreArgs a;
-    a.tab = d_log2cdf;
+    a.tab = d_ccdf;
     a.queue_off = queues->d_queue_off;
     a.cls = queues->d_class;
     a.deadline = queues->d_deadline_ms;
@@ -903,3 +999,4 @@ int orloj_select_batch(orloj_ctx* ctx, const orloj_grid* grid, const orloj_queue
 }
 
 }  // extern "C"
+

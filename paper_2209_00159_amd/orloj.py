@@ -9,6 +9,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import sys
 from typing import Optional
 
 import numpy as np
@@ -54,10 +55,12 @@ EXPORTS = ("orloj_create", "orloj_destroy", "orloj_set_stream", "orloj_last_erro
            "orloj_select_batch")
 
 
-def load(path: str = LIB_PATH):
+def load(path: Optional[str] = None):
     """Load and bind liborloj.so (no GPU needed to load)."""
     global _LIB
-    if _LIB is not None and path == LIB_PATH:
+    default = path is None or path == LIB_PATH
+    path = LIB_PATH if path is None else path
+    if _LIB is not None and default:
         return _LIB
     if not os.path.exists(path):
         raise OrlojError(ORLOJ_E_INVALID,
@@ -82,7 +85,7 @@ def load(path: str = LIB_PATH):
     L.orloj_score_candidates.restype = ctypes.c_int
     L.orloj_select_batch.argtypes = [_VP, _GP, _QP, ctypes.c_int32, _VP, _VP, _VP, _VP, _VP]
     L.orloj_select_batch.restype = ctypes.c_int
-    if path == LIB_PATH:
+    if default:
         _LIB = L
     return L
 
@@ -120,8 +123,8 @@ class Context:
             raise OrlojError(rc, "orloj_create failed")
 
     def __del__(self):
-        import sys
-        if getattr(self, "ctx", None) and self.ctx.value and not sys.is_finalizing():
+        finalizing = sys is None or sys.is_finalizing()
+        if getattr(self, "ctx", None) and self.ctx.value and not finalizing:
             self.L.orloj_destroy(self.ctx)
             self.ctx = None
 
@@ -137,7 +140,8 @@ class Context:
 
     # -- orloj_build_cdfs ------------------------------------------------------
     def build_cdfs(self, counts: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
-        """counts [..., K] (uint32 stored as int32 or uint32) -> log2 CDF float32."""
+        """counts [..., K] (uint32 stored as int32 or uint32) -> 1 - CDF at
+        each bin's right edge, float32."""
         _need_cuda(counts, "counts", (torch.int32, torch.uint32), self.device)
         K = counts.shape[-1]
         if out is None:
@@ -186,7 +190,7 @@ def output_sizes(grid: Grid, queues: Queues, prefix_mode: int = PREFIX_TRIANGLE)
 
 class Scorer:
     """A workload resident in HBM plus its output buffers: uploads the
-    histograms and queues once, then builds the log2 CDF tables, scores all
+    histograms and queues once, then builds the CDF tables, scores all
     candidates and selects a batch per model through the C ABI."""
 
     def __init__(self, wl, ctx: Optional[Context] = None, prefix_mode: int = PREFIX_TRIANGLE,
@@ -199,7 +203,7 @@ class Scorer:
             self.counts = counts_device
         else:
             self.counts = torch.from_numpy(np.ascontiguousarray(wl.counts).view(np.int32)).to(dev)
-        self.log2cdf = torch.empty(self.counts.shape, dtype=torch.float32, device=dev)
+        self.ccdf = torch.empty(self.counts.shape, dtype=torch.float32, device=dev)
         self.width = torch.from_numpy(np.ascontiguousarray(wl.bin_width_ms, np.float64)).to(dev)
         self.grid = make_grid(wl.n_models, wl.n_classes, wl.n_bins, wl.batch_sizes, self.width)
         self.set_queues(wl.queue_off, wl.cls, wl.deadline_ms, wl.now_ms)
@@ -228,13 +232,13 @@ class Scorer:
 
     # -- the three entry points --------------------------------------------------
     def build(self):
-        self.ctx.build_cdfs(self.counts, self.log2cdf)
+        self.ctx.build_cdfs(self.counts, self.ccdf)
 
     def score(self, b_expo: Optional[float] = None):
         b = self.wl.b_expo if b_expo is None else b_expo
         c = self.ctx
         c._check(c.L.orloj_score_candidates(
-            c.ctx, ctypes.byref(self.grid), _ptr(self.log2cdf), ctypes.byref(self.queues),
+            c.ctx, ctypes.byref(self.grid), _ptr(self.ccdf), ctypes.byref(self.queues),
             float(b), self.mode, _ptr(self.d_cand_off), _ptr(self.d_prob_off),
             _ptr(self.finish_prob), _ptr(self.expected_finish), _ptr(self.expected_latency),
             _ptr(self.score_out)))
