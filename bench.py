@@ -96,6 +96,8 @@ def main():
     ap.add_argument("--cpu-models", type=int, default=24)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workers", type=int, default=16)
+    ap.add_argument("--no-trim", action="store_true",
+                    help="score without the table support (every table entry is read)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after timing, copy a 1 GiB buffer once (a plain copy kernel of "
                          "known size, for scaling HBM traffic counters)")
@@ -121,7 +123,7 @@ def main():
     print(f"[bench] generated {wl.name} in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
           flush=True)
     ctx = O.Context(0)
-    sc = O.Scorer(wl, ctx)
+    sc = O.Scorer(wl, ctx, trim=not args.no_trim)
     ab = algorithmic_bytes(wl)
     K = wl.n_bins
     evals = valid_candidates(wl) * K

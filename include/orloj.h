@@ -115,11 +115,16 @@ typedef struct orloj_queues {
  * complement keeps full relative precision where F is near 1, which the
  * batch CDF (a product of many member CDFs) needs.  Rows are laid out
  * [model][batch size][class][bin] for orloj_score_candidates.  A row with
- * total 0 is a data error (its entries are written as NaN).  d_counts and
- * d_ccdf must not overlap.
+ * total 0 is a data error (its entries are written as NaN).
+ *
+ * d_support (optional, NULL = not written): int32 [n_rows][2], the first and
+ * the last bin holding mass.  Entries before the first are exactly 1 and
+ * entries from the last on are exactly 0, so orloj_score_candidates can skip
+ * reading them.  A row with total 0 gets {0, 0}.
+ * d_counts, d_ccdf and d_support must not overlap.
  */
 int orloj_build_cdfs(orloj_ctx *ctx, int64_t n_rows, int32_t n_bins,
-                     const uint32_t *d_counts, float *d_ccdf);
+                     const uint32_t *d_counts, float *d_ccdf, int32_t *d_support);
 
 /*
  * Output sizing (host only, no launch).  For model q with queue length N_q
@@ -151,14 +156,18 @@ int orloj_output_sizes(const orloj_grid *grid, const orloj_queues *queues,
  *               d_expected_finish[cand]   = sum_m P_m      (double)
  *               d_expected_latency_ms[cand] = E[L_B]       (float)
  *               d_score[cand]             = sum_m p_m      (float)
- * d_ccdf is the [M][n_bs][C][K] table of orloj_build_cdfs.  d_cand_off /
+ * d_ccdf is the [M][n_bs][C][K] table of orloj_build_cdfs, and d_support
+ * (optional) the support it wrote for that same table: with it, table
+ * entries known to be exactly 0 or 1 are not read (the results are the same
+ * bits either way); NULL reads every entry.  A d_support that does not
+ * belong to d_ccdf gives wrong results.  d_cand_off /
  * d_prob_off are device copies of orloj_output_sizes' offsets.  Output
  * buffers hold at least n_cands / n_probs elements.  b_expo_per_ms must be
  * finite and > 0 (the paper uses 1e-4 per ms, §4.4).
  * ORLOJ_E_UNSUPPORTED when a prefix would exceed ORLOJ_MAX_PREFIX.
  */
 int orloj_score_candidates(orloj_ctx *ctx, const orloj_grid *grid, const float *d_ccdf,
-                           const orloj_queues *queues, double b_expo_per_ms,
+                           const int32_t *d_support, const orloj_queues *queues, double b_expo_per_ms,
                            int32_t prefix_mode, const int64_t *d_cand_off,
                            const int64_t *d_prob_off, float *d_finish_prob,
                            double *d_expected_finish, float *d_expected_latency_ms,

@@ -26,7 +26,7 @@
 
 #include <new>
 
-#include "/root/repo/include/orloj.h"
+#include "../../include/orloj.h"
 
 namespace {
 
@@ -39,6 +39,7 @@ constexpr int kErrClassRange = 2;
 constexpr int kErrDeadlineNaN = 4;
 constexpr int kErrUnsorted = 8;
 constexpr int kErrNowNaN = 16;
+constexpr int kErrWidth = 32;
 
 // ---------------------------------------------------------------------------
 // wave64 helpers
@@ -59,18 +60,28 @@ __device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t x, int lane) {
 // complementary CDF 1 - F(x_{k+1}) = (total - running sum) / total.  The
 // complement keeps full relative precision where F is close to 1, which is
 // where the batch CDF (a product over up to hundreds of members) is most
-// sensitive.
+// sensitive.  Optionally the row's support is recorded as well: the first
+// bin holding mass (every earlier entry is exactly 1) and the last bin
+// holding mass (it and every later entry are exactly 0).
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float survival(uint64_t cum, uint64_t tot, double rtot) {
     if (cum >= tot) return 0.0f;
     return (float)((double)(tot - cum) * rtot);
 }
 
+__device__ __forceinline__ int wave_min_i32(int x) {
+#pragma unroll
+    for (int s = 1; s < 64; s <<= 1) x = min(x, __shfl_xor(x, s, 64));
+    return x;
+}
+
 template <int VPT>
 __global__ __launch_bounds__(kThreads) void cdf_kernel(const uint32_t* __restrict__ counts,
-                                                       float* __restrict__ out, int64_t n_rows,
+                                                       float* __restrict__ out,
+                                                       int32_t* __restrict__ support, int64_t n_rows,
                                                        int K, int* __restrict__ err) {
     __shared__ uint64_t s_wave[kWaves];
+    __shared__ int s_sup[2][kWaves];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int base = tid * VPT;
     const bool vec = (VPT % 4 == 0) && ((K & 3) == 0);
@@ -100,8 +111,31 @@ __global__ __launch_bounds__(kThreads) void cdf_kernel(const uint32_t* __restric
             if (w < wv) off += t;
             tot += t;
         }
-        __syncthreads();   // s_wave is reused by the next row
         float* orow = out + (size_t)r * (size_t)K;
+        if (support) {
+            // first bin with mass; last bin with mass (K when the row is empty)
+            int lo = K, hi = -1;
+#pragma unroll
+            for (int j = 0; j < VPT; ++j) {
+                if (v[j] != 0u) {
+                    lo = min(lo, base + j);
+                    hi = max(hi, base + j);
+                }
+            }
+            lo = wave_min_i32(lo);
+            hi = -wave_min_i32(-hi);
+            if (lane == 0) { s_sup[0][wv] = lo; s_sup[1][wv] = hi; }
+            __syncthreads();
+            if (tid == 0) {
+                for (int w = 1; w < kWaves; ++w) {
+                    lo = min(lo, s_sup[0][w]);
+                    hi = max(hi, s_sup[1][w]);
+                }
+                support[2 * r] = hi < 0 ? 0 : lo;
+                support[2 * r + 1] = hi < 0 ? 0 : hi;
+            }
+        }
+        __syncthreads();   // s_wave and s_sup are reused by the next row
         if (tot == 0) {
             if (tid == 0) atomicOr(err, kErrEmptyHistogram);
 #pragma unroll
@@ -182,14 +216,6 @@ __device__ __forceinline__ double wave_scan_sum64(double x) {
     return x;
 }
 
-// Barrier that orders LDS only: global loads issued before it stay in
-// flight (the prefetched rows of later steps).
-__device__ __forceinline__ void lds_barrier() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
 // 2^x by the hardware instruction; results below 2^-126 flush to 0.
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -209,85 +235,103 @@ struct ScoreArgs {
     double* E;
     float* EL;
     float* S;
+    const int32_t* sup;        // [M][nbs][C][2] first / last bin with mass, or NULL
     int* err;
     double b;
     int M, C, K, nbs, rect, maxcap;
     int bs[ORLOJ_MAX_BATCH_SIZES];
 };
 
+// Stand-in rows for lane chunks that lie wholly outside a row's support:
+// there every entry of 1 - F is exactly 0 (past the last bin with mass) or
+// exactly 1 (before the first), so the update G <- G - G (1 - F) gives the
+// same bits whether it reads the table or these constants.  They stay in
+// cache, so trimmed chunks cost no HBM traffic.
+__constant__ __align__(64) float kFill[2][16] = {
+    {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f},
+    {1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f}};
+
 // Per-member lookup plan, built once per workgroup in LDS (it depends on
-// the deadline only, not on the step).  For member m with deadline bin k
-// and offset theta, every step the member wave reads from the snapshot
-//   gk  = G(x_k) (bin k-1),   gk1 = G(x_{k+1}) (bin k),
-// and assembles the discounted prefix Z(k-2) = sum_{i <= k-2} G(x_{i+1}) d^(k-2-i)
-// from the wave prefixes, the lane prefix A, the quarter-end value of the
-// thread's chunk and the G values of one 4-bin quarter:
-//   zq  = fb * (fa * pre[wsel] + A[la]) + fq * zqe[izq] + sum_r wq[r] g4[r]
-// then combines with fixed coefficients:
-//   P   = gk + theta (gk1 - gk)
-//   num = cg * (gk - omd * zq) + psi (gk1 - gk)
-// An index of -1 reads as 0; beyond-the-grid members add one = 1 to both G
-// values.  Dead requests and the k < 2 edge cases need no branch.
+// the deadline only, not on the step).
+//
+// The bins are swept in panels of 64 CPL bins (one chunk of CPL
+// consecutive bins per lane); a member with deadline bin k is handled in the
+// pass over its home panel hp (the panel of bin k; dead requests in pass 0,
+// beyond-the-grid requests in the last pass).  Deadline order makes the
+// members of each panel a contiguous range.  In that pass, at step n, the
+// wave has
+//   W     = Z at the last bin of panel hp-1   (discounted prefix carried in)
+//   gl    = G at the last bin of panel hp-1
+//   A[]   = in-panel discounted scan of the lane chunk totals
+//   g[], zq[]  snapshot of G and of each chunk's quarter-end prefixes
+// and assembles
+//   G(x_k)     = g[ig0]  (ig0 = kPrevPanel: gl; kNone: 0)
+//   G(x_{k+1}) = g[ig1]  (kNone: 0, the deadline has passed)
+//   both 1 when ig1 = kBeyond (the deadline lies beyond the grid)
+//   Z(k-2) = cW W + cG gl + cA A[la] + fq zq[izq] + sum_r wq[r] g[ig4 + r]
+//   P   = G(x_k) + theta (G(x_{k+1}) - G(x_k))
+//   num = cg (G(x_k) - (1 - d) Z(k-2)) + psi (G(x_{k+1}) - G(x_k))
+// Index kNone reads as 0.
+constexpr int kNone = -1;
+constexpr int kMaxPanels = 63;   // panels per row (their first members sit in one lane each)
+constexpr int kPrevPanel = -2;
+constexpr int kBeyond = -2;
+
 struct Member {
-    int cls;      // class id (clamped into range)
-    int ig0;      // snapshot index of G(x_k)     (-1: k = 0, dead or beyond)
-    int ig1;      // snapshot index of G(x_{k+1}) (-1: dead or beyond)
-    int ig4;      // float4 slot of the quarter holding bin k-2 (-1: k < 2 or dead)
-    int izq;      // quarter-end snapshot index before that quarter (-1: none)
-    int la;       // lane whose wave-internal scan precedes bin k-2 (-1: none)
-    int wsel;     // which wave prefix (0: none, 1..3)
-    float fa;     // d^(CPL (la - 64 wsel + 1)): weight of the wave prefix
-    float fb;     // d^(j+1): weight of the lane prefix at bin k-2 (j = its chunk offset)
-    float fq;     // d^(r+1): weight of the previous quarter end (r = offset in quarter)
-    float wq[4];  // d^(r - r') for r' <= r, else 0
-    float theta;  // position inside bin k
-    float cg;     // gamma * exp(-b theta w), or gamma * exp(-b (tau - K w))
-    float psi;    // (1 - exp(-b theta w)) / (b w)
-    float one;    // 1 for beyond-the-grid members (P = 1), else 0
+    int cls;        // class id (clamped into range)
+    int16_t hp;     // home panel
+    int16_t ig0;    // snapshot index of G(x_k), or kNone / kPrevPanel
+    int16_t ig1;    // snapshot index of G(x_{k+1}), or kNone / kBeyond
+    int16_t ig4;    // snapshot index of the quarter holding bin k-2, or kNone
+    int16_t izq;    // quarter-end index before that quarter, or kNone
+    int16_t la;     // lane whose in-panel scan precedes bin k-2, or kNone
+    float cW;       // weight of W
+    float cG;       // weight of gl
+    float cA;       // weight of A[la]
+    float fq;       // weight of zq[izq]
+    float wq[4];    // weights of the quarter's G values
+    float theta;    // position inside bin k
+    float cg;       // gamma exp(-b theta w), or gamma exp(-b (tau - K w))
+    float psi;      // (1 - exp(-b theta w)) / (b w)
 };
 
-// LDS layout of one workgroup (floats unless noted):
-//   g[2][256 CPL]   batch CDF G(x_{k+1}) of the current prefix, by step parity
-//   zqe[2][256 NQ]  in-chunk discounted prefix of g at each quarter end
-//   A[2][256]       wave-internal discounted scan of the chunk totals
-//   e[2][4]         per-wave sums of (1 - g)
-//   mem[maxcap]     Member
-// g is stored float4-interleaved: the j-th float4 of thread t's chunk sits
-// at float4 slot j * 256 + t, so a wave's snapshot stores are contiguous
-// (no bank conflicts) and bin k is found by snap_index().
 template <int CPL>
 struct Quarters {
     static constexpr int QW = CPL < 4 ? CPL : 4;   // bins per quarter
-    static constexpr int NQ = CPL / QW;            // quarters per thread
+    static constexpr int NQ = CPL / QW;            // quarters per lane chunk
 };
 
+// LDS layout of one workgroup (one wave):
+//   g[64 CPL]   snapshot of G over the current panel (float4-interleaved)
+//   zq[64 NQ]   quarter-end discounted prefixes of each lane chunk
+//   A[64]       in-panel discounted scan of the lane chunk totals
+//   mlo[]       first member of each panel
+//   mem[maxcap] Member
 template <int CPL>
-__host__ __device__ constexpr size_t score_smem_floats() {
-    // + 8 padding keeps Member 16-byte aligned
-    return 2 * (size_t)kThreads * CPL + 2 * (size_t)kThreads * Quarters<CPL>::NQ +
-           2 * kThreads + 2 * kWaves + 8;
+__host__ __device__ constexpr size_t score_fixed_bytes() {
+    return 4 * (64 * (size_t)CPL + 64 * (size_t)Quarters<CPL>::NQ + 64 + kMaxPanels + 1);
 }
+__host__ __device__ constexpr size_t score_bytes_per_member() { return sizeof(Member); }
 
 template <int CPL>
-__device__ __forceinline__ int snap_index(int k) {
+__device__ __forceinline__ int snap_index(int r) {   // r: bin offset inside the panel
     if constexpr (CPL >= 4) {
-        const int t = k / CPL, j = k - t * CPL;
-        return ((j >> 2) * kThreads + t) * 4 + (j & 3);
+        const int l = r / CPL, j = r - l * CPL;
+        return ((j >> 2) * 64 + l) * 4 + (j & 3);
     } else {
-        return k;
+        return r;
     }
 }
 
-// Branch-free load of one thread's CPL bins of a row.  EXACT: the row
-// fills the sweep waves (K = 256 CPL), so the loads are whole float4s.
-// Otherwise indices past the end of the row are clamped to a valid address
-// and their values are masked at use.  Every load is issued
-// unconditionally so the prefetch ring keeps fixed registers.
+// Branch-free load of one lane's CPL entries starting at p.  EXACT: the
+// panels tile the row exactly, so the loads are whole float4s.  Otherwise
+// offsets past lim (the row's last entry) are clamped to it and their
+// values are masked at use.  Every load is issued unconditionally so the
+// prefetch ring keeps fixed registers.
 template <int CPL, bool EXACT>
-__device__ __forceinline__ void load_chunk(float (&v)[CPL], const float* __restrict__ row,
-                                           int base, int K) {
+__device__ __forceinline__ void load_chunk(float (&v)[CPL], const float* __restrict__ p, int lim) {
     if constexpr (EXACT && CPL % 4 == 0) {
-        const float4* r4 = reinterpret_cast<const float4*>(row + base);
+        const float4* r4 = reinterpret_cast<const float4*>(p);
 #pragma unroll
         for (int j = 0; j < CPL / 4; ++j) {
             const float4 t = r4[j];
@@ -295,38 +339,102 @@ __device__ __forceinline__ void load_chunk(float (&v)[CPL], const float* __restr
         }
     } else {
 #pragma unroll
-        for (int j = 0; j < CPL; ++j) v[j] = row[min(base + j, K - 1)];
+        for (int j = 0; j < CPL; ++j) v[j] = p[min(j, lim)];
     }
 }
 
-// One workgroup scores every prefix of one model's queue at one batch size.
-// Waves 0-3 (the sweep waves) own the bins: thread t keeps the batch CDF
-// G_n(x_{k+1}) = prod_{i <= n} F_{c_i}(x_{k+1}) of its CPL consecutive bins
-// as an fp64 running product (the table holds 1 - F, so a step is one fma).
-// Step n: fold in member n's row (prefetched PF steps earlier), the
-// per-thread sums of (1 - G) and of discounted G (split into 4-bin quarters
-// so the dependency chains stay short), and a snapshot of G and of the
-// quarter-end discounted prefixes in LDS, then one LDS barrier.  Wave 4 (the
-// member wave) reads that snapshot after the barrier, scores the n+1
-// members and writes the candidate's outputs while the sweep waves run
-// step n+1 into the other snapshot buffer.  Only the member wave stores to
-// global memory, so the sweep waves' outstanding-load counts stay exact and
-// the prefetch ring is never drained early.
-constexpr int kScoreThreads = kThreads + 64;
+// Value of lane 63 in every lane.
+__device__ __forceinline__ float lane63(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+__device__ __forceinline__ double lane63(double v) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 63);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
 
-template <int CPL, int PF, bool EXACT>
-__global__ __launch_bounds__(kScoreThreads) void score_kernel(const ScoreArgs a) {
+// Same-wave LDS ordering point: keeps the compiler from moving LDS accesses
+// across it (the hardware already executes one wave's LDS operations in
+// order).
+__device__ __forceinline__ void wave_lds_fence() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+}
+
+// Per-step state carried from one panel pass to the next, spread over the
+// lanes: step n lives in lane n % 64 of register n / 64.  Reads and writes
+// take a wave-uniform step index.
+template <int CR>
+struct LaneCarry {
+    float v[CR];
+    __device__ __forceinline__ void zero() {
+#pragma unroll
+        for (int r = 0; r < CR; ++r) v[r] = 0.0f;
+    }
+    __device__ __forceinline__ float get(int n) const {
+        float out = 0.0f;
+#pragma unroll
+        for (int r = 0; r < CR; ++r) {
+            const float x = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v[r]), n & 63));
+            out = (n >> 6) == r ? x : out;
+        }
+        return out;
+    }
+    __device__ __forceinline__ void set(int n, float x) {
+        const int l = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+#pragma unroll
+        for (int r = 0; r < CR; ++r) v[r] = (l + 64 * r) == n ? x : v[r];
+    }
+    // value of step r * 64 + lane
+    __device__ __forceinline__ float mine(int r) const { return v[r]; }
+};
+
+template <int CR>
+struct LaneCarry64 {
+    LaneCarry<CR> lo, hi;
+    __device__ __forceinline__ void zero() { lo.zero(); hi.zero(); }
+    __device__ __forceinline__ double get(int n) const {
+        const uint32_t l = __builtin_bit_cast(uint32_t, lo.get(n));
+        const uint32_t h = __builtin_bit_cast(uint32_t, hi.get(n));
+        return __builtin_bit_cast(double, ((uint64_t)h << 32) | l);
+    }
+    __device__ __forceinline__ void set(int n, double x) {
+        const uint64_t u = __builtin_bit_cast(uint64_t, x);
+        lo.set(n, __builtin_bit_cast(float, (uint32_t)u));
+        hi.set(n, __builtin_bit_cast(float, (uint32_t)(u >> 32)));
+    }
+    __device__ __forceinline__ double mine(int r) const {
+        const uint32_t l = __builtin_bit_cast(uint32_t, lo.mine(r));
+        const uint32_t h = __builtin_bit_cast(uint32_t, hi.mine(r));
+        return __builtin_bit_cast(double, ((uint64_t)h << 32) | l);
+    }
+};
+
+// One workgroup (a single wave) scores every prefix of one model's queue at
+// one batch size.  Lane l of pass p owns bins [(p*64 + l) CPL, +CPL) and
+// keeps their batch CDF G_n(x_{k+1}) = prod_{i <= n} F_{c_i}(x_{k+1}) as an
+// fp64 running product over the steps n (the table holds 1 - F, so a step
+// is one fma per bin).  Per step: the sums of 1 - G and the discounted
+// prefix over the panel (4-bin quarters keep the dependency chains short,
+// a DPP scan joins the lanes), the carries into the next panel, and, if
+// some member's deadline falls in this panel, a snapshot in LDS that the
+// same wave then reads to score those members.  Rows are prefetched PF
+// iterations ahead through a register ring.
+template <int CPL, int PF, bool EXACT, int CR>
+__global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     using Q = Quarters<CPL>;
-    extern __shared__ __align__(16) float smem[];
-    constexpr int KP = kThreads * CPL;
-    constexpr int QP = kThreads * Q::NQ;
-    float* s_g = smem;
-    float* s_zq = s_g + 2 * KP;
-    float* s_A = s_zq + 2 * QP;
-    float* s_e = s_A + 2 * kThreads;
-    Member* s_mem = reinterpret_cast<Member*>(s_e + 2 * kWaves + 8);
+    constexpr int PW = 64 * CPL;                   // bins per panel
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    float* s_g = reinterpret_cast<float*>(smem_raw);
+    float* s_zq = s_g + 64 * CPL;
+    float* s_A = s_zq + 64 * Q::NQ;
+    int* s_mlo = reinterpret_cast<int*>(s_A + 64);          // kMaxPanels + 1 ints
+    Member* s_mem = reinterpret_cast<Member*>(s_mlo + kMaxPanels + 1);
+    const int maxcap = a.maxcap;
 
-    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int lane = threadIdx.x;
 
     // Largest batch sizes first: their workgroups run longest.
     const int bi = a.nbs - 1 - (int)(blockIdx.x / (unsigned)a.M);
@@ -335,24 +443,24 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(const ScoreArgs a)
     const int64_t N = a.queue_off[q + 1] - q0;
     const int bsz = a.bs[bi];
     const int64_t cap64 = a.rect ? N : (N < bsz ? N : (int64_t)bsz);
-    if (cap64 <= 0 || cap64 > a.maxcap) return;   // the host sizes maxcap
+    if (cap64 <= 0 || cap64 > maxcap || cap64 > 64 * CR) return;   // the host sizes both
     const int ncap = (int)cap64;
 
     const double w = a.width[q];
+    const bool wok = w > 0.0 && w < HUGE_VAL;        // else a data error
     const double nowq = a.now[q];
     const double b = a.b;
     const double bw = b * w;
     const int K = a.K;
+    const int NP = (K + PW - 1) / PW;
 
-    // Per-bin discount d = exp(-b w) and the powers the scans need.
-    const float d = (float)exp(-bw);
+    const float d = (float)exp(-bw);                  // discount per bin
     const float log2d = (float)(-bw * 1.4426950408889634);
-    const int nsteps = (ncap + PF - 1) / PF * PF;
     const float gamma = (float)(-expm1(-bw) / bw);   // (1 - d) / (b w)
+    const float omd = (float)(-expm1(-bw));          // 1 - d
 
-    // Members: bin and offset of each deadline (fp64 time, relative to
-    // now) and their lookup plans.
-    for (int m = tid; m < ncap; m += kScoreThreads) {
+    // ---- member lookup plans (fp64 time relative to now)
+    for (int m = lane; m < ncap; m += 64) {
         int c = a.cls[q0 + m];
         const double D = a.deadline[q0 + m];
         int flag = 0;
@@ -360,212 +468,312 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(const ScoreArgs a)
         if (isnan(D)) flag |= kErrDeadlineNaN;
         if (m > 0 && D < a.deadline[q0 + m - 1]) flag |= kErrUnsorted;
         if (m == 0 && isnan(nowq)) flag |= kErrNowNaN;
+        if (m == 0 && !wok) flag |= kErrWidth;
         if (flag) atomicOr(a.err, flag);
         Member mb;
         mb.cls = c;
-        mb.ig0 = mb.ig1 = mb.ig4 = mb.izq = mb.la = -1;
-        mb.wsel = 0;
-        mb.fa = mb.fb = mb.fq = 0.0f;
+        int hp = 0, ig0 = kNone, ig1 = kNone, ig4 = kNone, izq = kNone, la = kNone;
+        mb.cW = mb.cG = mb.cA = mb.fq = 0.0f;
         mb.wq[0] = mb.wq[1] = mb.wq[2] = mb.wq[3] = 0.0f;
-        mb.theta = mb.cg = mb.psi = mb.one = 0.0f;
+        mb.theta = mb.cg = mb.psi = 0.0f;
         const double tau = D - nowq;
         int kz = -1;   // bin whose discounted prefix Z the priority needs
-        if (tau > 0.0) {
+        if (tau > 0.0 && wok) {
             const double u = tau / w;
             if (u >= (double)K) {                  // beyond the grid: P = 1
-                mb.one = 1.0f;
+                ig1 = kBeyond;
                 mb.cg = gamma * (float)exp(-b * (tau - (double)K * w));
+                hp = NP - 1;
                 kz = K - 2;
             } else {
                 const double kf = floor(u);
                 const double th = u - kf;
                 const int k = (int)kf;
+                hp = k / PW;
                 mb.theta = (float)th;
                 mb.cg = gamma * (float)exp(-b * th * w);
                 mb.psi = (float)(-expm1(-b * th * w) / bw);
-                mb.ig1 = snap_index<CPL>(k);
-                if (k >= 1) mb.ig0 = snap_index<CPL>(k - 1);
+                ig1 = snap_index<CPL>(k - hp * PW);
+                if (k >= 1) ig0 = k - 1 >= hp * PW ? snap_index<CPL>(k - 1 - hp * PW) : kPrevPanel;
                 kz = k - 2;
             }
         }
         if (kz >= 0) {
-            const int L = kz / CPL, j = kz - L * CPL;
-            const int qq = j / Q::QW, r = j - qq * Q::QW;
-            mb.ig4 = (qq * kThreads + L) * Q::QW;          // start of the quarter's G values
-            if (qq > 0) mb.izq = L * Q::NQ + qq - 1;
-            mb.fq = exp2f(log2d * (float)(r + 1));
-            for (int rr = 0; rr <= r; ++rr) mb.wq[rr] = exp2f(log2d * (float)(r - rr));
-            mb.fb = exp2f(log2d * (float)(j + 1));
-            if (L > 0) {
-                const int Lp = L - 1, wl = Lp >> 6;
-                mb.la = Lp;
-                mb.wsel = wl;
-                mb.fa = exp2f(log2d * (float)(CPL * (Lp - 64 * wl + 1)));
+            const int p0 = hp * PW;                // first bin of the home panel
+            if (kz >= p0) {
+                const int r = kz - p0, l = r / CPL, j = r - l * CPL;
+                const int qq = j / Q::QW, rq = j - qq * Q::QW;
+                mb.cW = hp > 0 ? exp2f(log2d * (float)(kz - p0 + 1)) : 0.0f;
+                if (l > 0) {
+                    la = l - 1;
+                    mb.cA = exp2f(log2d * (float)(j + 1));
+                }
+                if (qq > 0) {
+                    izq = l * Q::NQ + qq - 1;
+                    mb.fq = exp2f(log2d * (float)(rq + 1));
+                }
+                ig4 = snap_index<CPL>(r - rq);     // first bin of the quarter
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr)
+                    mb.wq[rr] = rr <= rq ? exp2f(log2d * (float)(rq - rr)) : 0.0f;
+            } else if (kz == p0 - 1) {             // last bin of the previous panel
+                mb.cW = 1.0f;
+            } else {                               // kz = p0 - 2: step back one bin
+                mb.cW = (float)exp(bw);
+                mb.cG = -(float)exp(bw);
             }
         }
+        mb.hp = (int16_t)hp; mb.ig0 = (int16_t)ig0; mb.ig1 = (int16_t)ig1;
+        mb.ig4 = (int16_t)ig4; mb.izq = (int16_t)izq; mb.la = (int16_t)la;
         s_mem[m] = mb;
     }
+    wave_lds_fence();
+    // first member of each panel (home panels are non-decreasing in m)
+    for (int p = 0; p <= NP; ++p) {
+        int cnt = 0;
+        for (int m0 = 0; m0 < ncap; m0 += 64) {
+            const int m = m0 + lane;
+            const bool below = m < ncap && s_mem[m].hp < p;
+            cnt += __builtin_popcountll(__ballot(below));
+        }
+        if (lane == 0) s_mlo[p] = cnt;
+    }
 
-    lds_barrier();
-
-    if (wv < kWaves) {
-        // ======================= sweep waves =======================
-        float rp[4];
+    // ---- scan constants
+    float rp[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) rp[i] = exp2_hw(log2d * (float)(CPL << i));
-        const float w15 = exp2_hw(log2d * (float)(CPL * ((lane & 15) + 1)));
-        const float w31 = exp2_hw(log2d * (float)(CPL * (lane >= 32 ? lane - 31 : 0)));
-        const float dQ = exp2_hw(log2d * (float)Q::QW);
-        const int base = tid * CPL;
-        const float* tab_qb =
-            a.tab + ((size_t)q * (size_t)a.nbs + (size_t)bi) * (size_t)a.C * (size_t)K;
-        double Gacc[CPL];   // G(x_{k+1}) of the current prefix, fp64 running product
-#pragma unroll
-        for (int j = 0; j < CPL; ++j) Gacc[j] = 1.0;
+    for (int i = 0; i < 4; ++i) rp[i] = exp2_hw(log2d * (float)(CPL << i));
+    const float w15 = exp2_hw(log2d * (float)(CPL * ((lane & 15) + 1)));
+    const float w31 = exp2_hw(log2d * (float)(CPL * (lane >= 32 ? lane - 31 : 0)));
+    const float dQ = exp2_hw(log2d * (float)Q::QW);
+    const float dPW = exp2_hw(log2d * (float)PW);
 
-        // Prefetch ring: buf[i] holds the row of step n0 + i.  The tail is
-        // padded to a multiple of PF with ghost steps (their rows repeat the
-        // last member's and nobody reads their snapshot).
-        float buf[PF][CPL];
+    int64_t cand = a.cand_off[q], prob = a.prob_off[q];
+    for (int j = 0; j < bi; ++j) {
+        const int64_t c = a.rect ? N : (N < a.bs[j] ? N : (int64_t)a.bs[j]);
+        cand += c;
+        prob += c * (c + 1) / 2;
+    }
+    const float* tab_qb = a.tab + ((size_t)q * (size_t)a.nbs + (size_t)bi) * (size_t)a.C * (size_t)K;
+    wave_lds_fence();
+
+    // class and support of member n in lane n % 64 of register n / 64;
+    // first member of each panel in lane p
+    LaneCarry<CR> cls_r, lo_r, hi_r;
+    const int32_t* sup_qb = a.sup ? a.sup + ((size_t)q * (size_t)a.nbs + (size_t)bi) * (size_t)a.C * 2 : nullptr;
+#pragma unroll
+    for (int r = 0; r < CR; ++r) {
+        const int m = min(r * 64 + lane, ncap - 1);
+        const int c = s_mem[m].cls;
+        cls_r.v[r] = __builtin_bit_cast(float, c);
+        lo_r.v[r] = __builtin_bit_cast(float, sup_qb ? sup_qb[2 * c] : 0);
+        hi_r.v[r] = __builtin_bit_cast(float, sup_qb ? sup_qb[2 * c + 1] : K);
+    }
+    const int mlo_r = s_mlo[min(lane, NP)];
+    // Load the lane chunk starting at bin c0 of member n's row; chunks wholly
+    // outside the row's support, and every chunk when `none` (the row's
+    // values cannot change G), read a constant row instead.
+    auto load_step = [&](float (&v)[CPL], int n, int c0, bool none) {
+        const int c = __builtin_bit_cast(int, cls_r.get(n));
+        const int lo = __builtin_bit_cast(int, lo_r.get(n));
+        const int hi = __builtin_bit_cast(int, hi_r.get(n));
+        const bool ones = !none && c0 + CPL <= lo, zeros = none || c0 >= hi;
+        const float* src = tab_qb + (size_t)c * (size_t)K + c0;
+        int lim = K - 1 - c0;
+        if (ones || zeros) {
+            src = kFill[ones ? 1 : 0];
+            lim = CPL - 1;
+        }
+        load_chunk<CPL, EXACT>(v, src, lim);
+    };
+
+    LaneCarry<CR> cW, cGl, cN;
+    LaneCarry64<CR> cE, cP;
+    cW.zero(); cGl.zero(); cN.zero(); cE.zero(); cP.zero();
+
+    // One flat loop over (panel p, step n), n fastest, padded at the end to a
+    // multiple of PF with ghost iterations (p == NP) so that ring slot i
+    // always holds iteration it0 + i.  The row of iteration it + PF is
+    // loaded PF iterations ahead; (p, n) and the prefetch position advance
+    // by counting.
+    const int total = NP * ncap;
+    const int iters = (total + PF - 1) / PF * PF;
+    const int base = lane * CPL;
+
+    double Gacc[CPL];
+    float buf[PF][CPL];
+    int pf_p = 0, pf_n = 0;                               // prefetch position
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+        load_step(buf[i], pf_n, pf_p * PW + base, false);
+        // keep the priming loads in ring order, as the loop issues them
+        __builtin_amdgcn_sched_barrier(0);
+        if (++pf_n == ncap) { pf_n = 0; pf_p = min(pf_p + 1, NP - 1); }
+    }
+    int p = 0, n = 0;
+    int mlo = __builtin_amdgcn_readlane(mlo_r, 0);
+    int mend = __builtin_amdgcn_readlane(mlo_r, 1);
+    // Trivial steps.  Where a panel lies wholly past the last bin with mass
+    // of member n's row (every 1 - F there is exactly 0), or where G is
+    // already exactly 0 over the whole panel (an earlier member's row had
+    // no mass up to its end), step n leaves G unchanged bit for bit; if no
+    // member of the panel needs scoring at that step, its panel sums are
+    // those of step n-1 and the update, its loads and its reductions are
+    // skipped.
+    bool pass_zero = false;                  // G == 0 on every bin of this pass's panel
+    float etot_prev = 0.0f, T_prev = 0.0f, gl_prev = 0.0f;
+
+    for (int it0 = 0; it0 < iters; it0 += PF) {
 #pragma unroll
         for (int i = 0; i < PF; ++i) {
-            load_chunk<CPL, EXACT>(buf[i], tab_qb + (size_t)s_mem[min(i, ncap - 1)].cls * (size_t)K,
-                                   base, K);
-            // keep the priming loads in ring order, as the loop issues them
-            __builtin_amdgcn_sched_barrier(0);
-        }
-
-        for (int n0 = 0; n0 < nsteps; n0 += PF) {
+            if (n == 0) {
+                // a real branch (the asm keeps it from becoming selects)
+                asm volatile("" ::: "memory");
 #pragma unroll
-            for (int i = 0; i < PF; ++i) {
-                const int n = n0 + i;
-                const int par = n & 1;
-                float* g_out = s_g + par * KP;
-                // G <- G * F = G - G (1 - F), in fp64; per-quarter sums
-                double gs[Q::QW];
-                float zqv[Q::NQ];
-                float gv[CPL];
-#pragma unroll
-                for (int r = 0; r < Q::QW; ++r) gs[r] = 0.0;
+                for (int j = 0; j < CPL; ++j) Gacc[j] = 1.0;
+                pass_zero = false;
+            }
+            const int p0 = p * PW;                        // first bin of the panel
+            const int pbase = p0 + base;                  // first bin of this lane chunk
+            const int hi_n = __builtin_bit_cast(int, hi_r.get(n));
+            const int lo_n = __builtin_bit_cast(int, lo_r.get(n));
+            const int mhi = min(mend, n + 1);             // members of this panel among the first n+1
+            const bool skip = p >= NP || (n > 0 && (pass_zero || p0 >= hi_n) && !(mlo < mhi));
+            // G <- G * F = G - G (1 - F), in fp64; per-quarter sums
+            double gs[Q::QW];
+            float zqv[Q::NQ];
+            if (!skip) {
 #pragma unroll
                 for (int qq = 0; qq < Q::NQ; ++qq) {
                     float zz = 0.0f;
 #pragma unroll
                     for (int r = 0; r < Q::QW; ++r) {
                         const int j = qq * Q::QW + r;
-                        const float t = (EXACT || base + j < K) ? buf[i][j] : 0.0f;
+                        const float t = (EXACT || pbase + j < K) ? buf[i][j] : 0.0f;
                         Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
-                        gs[r] += Gacc[j];
+                        gs[r] = qq == 0 ? Gacc[j] : gs[r] + Gacc[j];
                         const float g = (float)Gacc[j];
-                        zz = fmaf(zz, d, g);
-                        gv[j] = g;
+                        zz = r == 0 ? g : fmaf(zz, d, g);
                     }
                     zqv[qq] = zz;
                 }
-                load_chunk<CPL, EXACT>(
-                    buf[i], tab_qb + (size_t)s_mem[min(n + PF, ncap - 1)].cls * (size_t)K, base, K);
-                // quarter ends of the in-chunk discounted prefix, and its total
-                float zc = 0.0f;
+            }
+            // the slot is refilled only after the update has consumed it, so
+            // the ring keeps its registers (no copies, no wait on the loads
+            // just issued)
 #pragma unroll
-                for (int qq = 0; qq < Q::NQ; ++qq) {
-                    zc = fmaf(zc, dQ, zqv[qq]);
-                    zqv[qq] = zc;
-                }
-                double gsum = 0.0;
+            for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(Gacc[j])::"memory");
+            // G == 0 over the pass from here on: later steps of it need no row
+            const bool zero_after = pass_zero || min(p0 + PW, K) <= lo_n;
+            load_step(buf[i], pf_n, pf_p * PW + base, zero_after && pf_p == p);
+            if (++pf_n == ncap) { pf_n = 0; pf_p = min(pf_p + 1, NP - 1); }
+            if (p < NP) {                                 // else a ghost iteration
+                float etot = etot_prev, T = T_prev, glast_here = gl_prev;
+                const float Win = cW.get(n);              // carries in from the previous
+                const float glin = cGl.get(n);            // panel pass (zero in the first)
+                if (!skip) {
+                    // quarter ends of the in-chunk discounted prefix, and its total
+                    float zc = zqv[0];
 #pragma unroll
-                for (int r = 0; r < Q::QW; ++r) gsum += gs[r];
-                // sum over this thread's bins of 1 - G (padding bins hold G = 1)
-                const float e = (float)((double)CPL - gsum);
-                if constexpr (CPL >= 4) {
-#pragma unroll
-                    for (int j = 0; j < CPL; j += 4) {
-                        const int slot = ((j >> 2) * kThreads + tid) * 4;
-                        *reinterpret_cast<float4*>(g_out + slot) =
-                            make_float4(gv[j], gv[j + 1], gv[j + 2], gv[j + 3]);
+                    for (int qq = 1; qq < Q::NQ; ++qq) {
+                        zc = fmaf(zc, dQ, zqv[qq]);
+                        zqv[qq] = zc;
                     }
-                } else {
+                    double gsum = gs[0];
 #pragma unroll
-                    for (int j = 0; j < CPL; ++j) g_out[base + j] = gv[j];
-                }
-                float* zq_out = s_zq + par * QP + tid * Q::NQ;
-                if constexpr (Q::NQ == 4) {
-                    *reinterpret_cast<float4*>(zq_out) = make_float4(zqv[0], zqv[1], zqv[2], zqv[3]);
-                } else {
-#pragma unroll
-                    for (int qq = 0; qq < Q::NQ; ++qq) zq_out[qq] = zqv[qq];
-                }
-                const float esum = wave_scan_sum(e);
-                const float A = wave_wscan(zc, rp, w15, w31);
+                    for (int r = 1; r < Q::QW; ++r) gsum += gs[r];
+                    // 1 - G summed over the lane's bins (padding bins hold G = 1)
+                    const float e = (float)((double)CPL - gsum);
+                    etot = lane63(wave_scan_sum(e));
+                    const float A = wave_wscan(zc, rp, w15, w31);
+                    T = lane63(A);                        // discounted prefix at the panel end
+                    glast_here = lane63((float)Gacc[CPL - 1]);
+                    etot_prev = etot; T_prev = T; gl_prev = glast_here;
 
-                s_A[par * kThreads + tid] = A;
-                if (lane == 63) s_e[par * kWaves + wv] = esum;
-                lds_barrier();
-            }
-        }
-    } else {
-        // ======================= member wave =======================
-        const float omd = (float)(-expm1(-bw));          // 1 - d
-        const float d64c = exp2_hw(log2d * (float)(64 * CPL));
-        int64_t cand = a.cand_off[q], prob = a.prob_off[q];
-        for (int j = 0; j < bi; ++j) {
-            const int64_t c = a.rect ? N : (N < a.bs[j] ? N : (int64_t)a.bs[j]);
-            cand += c;
-            prob += c * (c + 1) / 2;
-        }
-        for (int n = 0; n < nsteps; ++n) {
-            lds_barrier();
-            if (n >= ncap) continue;
-            const int par = n & 1;
-            const float* g = s_g + par * KP;
-            const float* zq = s_zq + par * QP;
-            const float* As = s_A + par * kThreads;
-            // discounted totals at the end of waves 0..2
-            const float T0 = As[63], T1 = As[127], T2 = As[191];
-            const float W2 = fmaf(T0, d64c, T1);
-            const float W3 = fmaf(W2, d64c, T2);
-            const double es = (double)s_e[par * kWaves + 0] + (double)s_e[par * kWaves + 1] +
-                              (double)s_e[par * kWaves + 2] + (double)s_e[par * kWaves + 3];
-            const double el = w * (0.5 + es);
-            const int nn = n + 1;
-            double pP = 0.0;
-            float pN = 0.0f;
-            for (int m = lane; m < nn; m += 64) {
-                const Member mb = s_mem[m];
-                const float g0 = g[max(mb.ig0, 0)];
-                const float g1 = g[max(mb.ig1, 0)];
-                const float al0 = As[max(mb.la, 0)];
-                const float zq0 = zq[max(mb.izq, 0)];
-                float g4[4];
-                if constexpr (Q::QW == 4) {
-                    const float4 t4 = *reinterpret_cast<const float4*>(g + max(mb.ig4, 0));
-                    g4[0] = t4.x; g4[1] = t4.y; g4[2] = t4.z; g4[3] = t4.w;
-                } else {
+                    if (mlo < mhi) {
+                        // snapshot of G over the panel (rounded again from the
+                        // fp64 values, rather than kept live through the scans)
+                        float gv[CPL];
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) g4[r] = r < Q::QW ? g[max(mb.ig4, 0) + r] : 0.0f;
+                        for (int j = 0; j < CPL; ++j) gv[j] = (float)Gacc[j];
+                        if constexpr (CPL >= 4) {
+#pragma unroll
+                            for (int j = 0; j < CPL; j += 4) {
+                                const int slot = ((j >> 2) * 64 + lane) * 4;
+                                *reinterpret_cast<float4*>(s_g + slot) =
+                                    make_float4(gv[j], gv[j + 1], gv[j + 2], gv[j + 3]);
+                            }
+                        } else {
+#pragma unroll
+                            for (int j = 0; j < CPL; ++j) s_g[base + j] = gv[j];
+                        }
+#pragma unroll
+                        for (int qq = 0; qq < Q::NQ; ++qq) s_zq[lane * Q::NQ + qq] = zqv[qq];
+                        s_A[lane] = A;
+                        wave_lds_fence();
+                        double pP = 0.0;
+                        float pN = 0.0f;
+                        const int nn = n + 1;
+                        for (int m = mlo + lane; m < mhi; m += 64) {
+                            const Member mb = s_mem[m];
+                            const float g0 = s_g[max((int)mb.ig0, 0)];
+                            const float g1 = s_g[max((int)mb.ig1, 0)];
+                            const float al0 = s_A[max((int)mb.la, 0)];
+                            const float zq0 = s_zq[max((int)mb.izq, 0)];
+                            float g4[4];
+                            if constexpr (Q::QW == 4) {
+                                const float4 t4 = *reinterpret_cast<const float4*>(s_g + max((int)mb.ig4, 0));
+                                g4[0] = t4.x; g4[1] = t4.y; g4[2] = t4.z; g4[3] = t4.w;
+                            } else {
+#pragma unroll
+                                for (int r = 0; r < 4; ++r) g4[r] = r < Q::QW ? s_g[max((int)mb.ig4, 0) + r] : 0.0f;
+                            }
+                            const bool beyond = mb.ig1 == kBeyond;
+                            const float gk = beyond ? 1.0f
+                                                    : (mb.ig0 >= 0 ? g0 : (mb.ig0 == kPrevPanel ? glin : 0.0f));
+                            const float gk1 = beyond ? 1.0f : (mb.ig1 >= 0 ? g1 : 0.0f);
+                            float zin = mb.fq * (mb.izq >= 0 ? zq0 : 0.0f);
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) zin = fmaf(mb.wq[r], mb.ig4 >= 0 ? g4[r] : 0.0f, zin);
+                            const float Zv = fmaf(mb.cW, Win, fmaf(mb.cG, glin, fmaf(mb.cA, mb.la >= 0 ? al0 : 0.0f, zin)));
+                            const float h = gk1 - gk;
+                            const float P = fmaf(mb.theta, h, gk);
+                            const float num = fmaf(mb.cg, fmaf(-omd, Zv, gk), h * mb.psi);
+                            a.P[prob + (int64_t)n * nn / 2 + m] = P;
+                            pP += (double)P;
+                            pN += num;
+                        }
+                        pP = wave_scan_sum64(pP);
+                        pN = wave_scan_sum(pN);
+                        cP.set(n, cP.get(n) + lane63(pP));
+                        cN.set(n, cN.get(n) + lane63(pN));
+                        wave_lds_fence();
+                    }
                 }
-                const float gk = (mb.ig0 >= 0 ? g0 : 0.0f) + mb.one;
-                const float gk1 = (mb.ig1 >= 0 ? g1 : 0.0f) + mb.one;
-                const float al = mb.la >= 0 ? al0 : 0.0f;
-                const float zqp = mb.izq >= 0 ? zq0 : 0.0f;
-                const float pre = mb.wsel == 1 ? T0 : (mb.wsel == 2 ? W2 : (mb.wsel == 3 ? W3 : 0.0f));
-                float zin = mb.fq * zqp;
+                pass_zero = zero_after;
+                // carries out to the next panel pass, per-step sums
+                cW.set(n, fmaf(Win, dPW, T));
+                cGl.set(n, glast_here);
+                cE.set(n, cE.get(n) + (double)etot);
+            }
+            if (++n == ncap) {
+                n = 0;
+                ++p;
+                mlo = __builtin_amdgcn_readlane(mlo_r, min(p, NP));
+                mend = __builtin_amdgcn_readlane(mlo_r, min(p + 1, NP));
+            }
+        }
+    }
+
+    // ---- candidate outputs: lane l holds steps l, l + 64, ...
 #pragma unroll
-                for (int r = 0; r < 4; ++r) zin = fmaf(mb.wq[r], g4[r], zin);
-                const float zqv = fmaf(mb.fb, fmaf(mb.fa, pre, al), mb.ig4 >= 0 ? zin : 0.0f);
-                const float h = gk1 - gk;
-                const float P = fmaf(mb.theta, h, gk);
-                const float num = fmaf(mb.cg, fmaf(-omd, zqv, gk), h * mb.psi);
-                a.P[prob + (int64_t)n * nn / 2 + m] = P;
-                pP += (double)P;
-                pN += num;
-            }
-            pP = wave_scan_sum64(pP);
-            pN = wave_scan_sum(pN);
-            if (lane == 63) {
-                a.E[cand + n] = pP;
-                a.EL[cand + n] = (float)el;
-                a.S[cand + n] = (float)((double)pN / el);
-            }
+    for (int r = 0; r < CR; ++r) {
+        const int n = r * 64 + lane;
+        if (n < ncap) {
+            const double el = w * (0.5 + cE.mine(r));
+            a.E[cand + n] = cP.mine(r);
+            a.EL[cand + n] = (float)el;
+            a.S[cand + n] = (float)((double)cN.mine(r) / el);
         }
     }
 }
@@ -734,35 +942,56 @@ int chunk_per_lane(int K) {
 }
 
 #ifndef ORLOJ_SCORE_PREFETCH
-#define ORLOJ_SCORE_PREFETCH 2   // rows in flight per sweep thread at 16+ bins per thread
+#define ORLOJ_SCORE_PREFETCH 2   // iterations a row is loaded ahead of its use
 #endif
 
-template <int CPL, bool EXACT>
+template <int CPL, bool EXACT, int CR>
 hipError_t launch_score_v(const ScoreArgs& a, unsigned grid, hipStream_t st) {
-    constexpr int PF = CPL >= 16 ? ORLOJ_SCORE_PREFETCH : 3;
-    const size_t sm = score_smem_floats<CPL>() * sizeof(float) + (size_t)a.maxcap * sizeof(Member);
+    constexpr int PF = ORLOJ_SCORE_PREFETCH;
+    const size_t sm = score_fixed_bytes<CPL>() + (size_t)a.maxcap * score_bytes_per_member();
     static size_t attr_bytes = 0;   // per template instance; device-independent
     if (sm > attr_bytes) {
-        hipError_t e = hipFuncSetAttribute((const void*)score_kernel<CPL, PF, EXACT>,
+        hipError_t e = hipFuncSetAttribute((const void*)score_kernel<CPL, PF, EXACT, CR>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
         if (e != hipSuccess) return e;
         attr_bytes = sm;
     }
-    hipLaunchKernelGGL((score_kernel<CPL, PF, EXACT>), dim3(grid), dim3(kScoreThreads), sm, st, a);
+    hipLaunchKernelGGL((score_kernel<CPL, PF, EXACT, CR>), dim3(grid), dim3(64), sm, st, a);
     return hipGetLastError();
+}
+
+// Bins per lane chunk: panels of 64 chunks of CPL bins, at most kMaxChunk
+// bins per lane (larger rows take more panels).  A panel pass re-reads the
+// slice of each member's row once per member; narrow panels keep those
+// slices in L2 between the re-reads of a class.
+constexpr int kMaxChunk = 16;
+
+int score_chunk(int K) {
+    int c = 1;
+    while (c < kMaxChunk && 64 * c < K) c <<= 1;
+    return c;
+}
+
+// Step carries: one register per 64 steps (longest prefix up to 64, or up to
+// the compiled limit).
+template <int CPL, bool EXACT>
+hipError_t launch_score_c(const ScoreArgs& a, unsigned grid, hipStream_t st) {
+    return a.maxcap <= 64 ? launch_score_v<CPL, EXACT, 1>(a, grid, st)
+                          : launch_score_v<CPL, EXACT, (ORLOJ_MAX_PREFIX + 63) / 64>(a, grid, st);
 }
 
 template <int CPL>
 hipError_t launch_score(const ScoreArgs& a, unsigned grid, hipStream_t st) {
-    return a.K == kThreads * CPL ? launch_score_v<CPL, true>(a, grid, st)
-                                 : launch_score_v<CPL, false>(a, grid, st);
+    return a.K % (64 * CPL) == 0 ? launch_score_c<CPL, true>(a, grid, st)
+                                 : launch_score_c<CPL, false>(a, grid, st);
 }
 
 template <int VPT>
-hipError_t launch_cdf(const uint32_t* c, float* o, int64_t rows, int K, int* err, hipStream_t st) {
+hipError_t launch_cdf(const uint32_t* c, float* o, int32_t* sup, int64_t rows, int K, int* err,
+                      hipStream_t st) {
     const int64_t cap = 1 << 20;
     const unsigned grid = (unsigned)(rows < cap ? rows : cap);
-    hipLaunchKernelGGL(cdf_kernel<VPT>, dim3(grid), dim3(kThreads), 0, st, c, o, rows, K, err);
+    hipLaunchKernelGGL(cdf_kernel<VPT>, dim3(grid), dim3(kThreads), 0, st, c, o, sup, rows, K, err);
     return hipGetLastError();
 }
 
@@ -823,18 +1052,19 @@ int orloj_sync(orloj_ctx* ctx) {
     if (flags) {
         e = hipMemset(ctx->d_err, 0, sizeof(int));
         if (e != hipSuccess) return hip_fail(ctx, e, "clearing the device status word");
-        return fail(ctx, ORLOJ_E_DATA, "device data error:%s%s%s%s%s",
+        return fail(ctx, ORLOJ_E_DATA, "device data error:%s%s%s%s%s%s",
                     (flags & kErrEmptyHistogram) ? " histogram-with-no-samples" : "",
                     (flags & kErrClassRange) ? " class-id-out-of-range" : "",
                     (flags & kErrDeadlineNaN) ? " NaN-deadline" : "",
                     (flags & kErrUnsorted) ? " deadlines-not-sorted" : "",
-                    (flags & kErrNowNaN) ? " NaN-now" : "");
+                    (flags & kErrNowNaN) ? " NaN-now" : "",
+                    (flags & kErrWidth) ? " bin-width-not-positive" : "");
     }
     return ORLOJ_OK;
 }
 
 int orloj_build_cdfs(orloj_ctx* ctx, int64_t n_rows, int32_t n_bins, const uint32_t* d_counts,
-                     float* d_ccdf) {
+                     float* d_ccdf, int32_t* d_support) {
     if (!ctx) return ORLOJ_E_INVALID;
     if (n_rows < 0) return fail(ctx, ORLOJ_E_INVALID, "n_rows < 0");
     if (n_bins < 1) return fail(ctx, ORLOJ_E_INVALID, "n_bins < 1");
@@ -847,16 +1077,22 @@ int orloj_build_cdfs(orloj_ctx* ctx, int64_t n_rows, int32_t n_bins, const uint3
     const size_t bytes = (size_t)n_rows * (size_t)n_bins * 4;
     if (cb < ob + bytes && ob < cb + bytes)
         return fail(ctx, ORLOJ_E_INVALID, "d_counts and d_ccdf overlap");
+    if (d_support) {
+        const char* sb = (const char*)d_support;
+        const size_t sbytes = (size_t)n_rows * 8;
+        if ((sb < ob + bytes && ob < sb + sbytes) || (sb < cb + bytes && cb < sb + sbytes))
+            return fail(ctx, ORLOJ_E_INVALID, "d_support overlaps d_counts or d_ccdf");
+    }
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
     const int vpt = chunk_per_lane(n_bins);
     switch (vpt) {
-        case 1: e = launch_cdf<1>(d_counts, d_ccdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
-        case 2: e = launch_cdf<2>(d_counts, d_ccdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
-        case 4: e = launch_cdf<4>(d_counts, d_ccdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
-        case 8: e = launch_cdf<8>(d_counts, d_ccdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
-        case 16: e = launch_cdf<16>(d_counts, d_ccdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
-        default: e = launch_cdf<32>(d_counts, d_ccdf, n_rows, n_bins, ctx->d_err, ctx->stream); break;
+        case 1: e = launch_cdf<1>(d_counts, d_ccdf, d_support, n_rows, n_bins, ctx->d_err, ctx->stream); break;
+        case 2: e = launch_cdf<2>(d_counts, d_ccdf, d_support, n_rows, n_bins, ctx->d_err, ctx->stream); break;
+        case 4: e = launch_cdf<4>(d_counts, d_ccdf, d_support, n_rows, n_bins, ctx->d_err, ctx->stream); break;
+        case 8: e = launch_cdf<8>(d_counts, d_ccdf, d_support, n_rows, n_bins, ctx->d_err, ctx->stream); break;
+        case 16: e = launch_cdf<16>(d_counts, d_ccdf, d_support, n_rows, n_bins, ctx->d_err, ctx->stream); break;
+        default: e = launch_cdf<32>(d_counts, d_ccdf, d_support, n_rows, n_bins, ctx->d_err, ctx->stream); break;
     }
     if (e != hipSuccess) return hip_fail(ctx, e, "cdf_kernel launch");
     return ORLOJ_OK;
@@ -890,7 +1126,7 @@ int orloj_output_sizes(const orloj_grid* grid, const orloj_queues* queues, int32
 }
 
 int orloj_score_candidates(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
-                           const orloj_queues* queues, double b_expo_per_ms, int32_t prefix_mode,
+                           const int32_t* d_support, const orloj_queues* queues, double b_expo_per_ms, int32_t prefix_mode,
                            const int64_t* d_cand_off, const int64_t* d_prob_off,
                            float* d_finish_prob, double* d_expected_finish,
                            float* d_expected_latency_ms, float* d_score) {
@@ -926,6 +1162,7 @@ int orloj_score_candidates(orloj_ctx* ctx, const orloj_grid* grid, const float* 
 
     ScoreArgs a;
     a.tab = d_ccdf;
+    a.sup = d_support;
     a.queue_off = queues->d_queue_off;
     a.cls = queues->d_class;
     a.deadline = queues->d_deadline_ms;
@@ -951,13 +1188,14 @@ int orloj_score_candidates(orloj_ctx* ctx, const orloj_grid* grid, const float* 
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
     const unsigned g = (unsigned)nblk;
-    switch (chunk_per_lane(grid->n_bins)) {
+    static_assert(kMaxChunk == 16, "launch table below");
+    static_assert((ORLOJ_MAX_BINS + 64 * kMaxChunk - 1) / (64 * kMaxChunk) <= kMaxPanels, "panels");
+    switch (score_chunk(grid->n_bins)) {
         case 1: e = launch_score<1>(a, g, ctx->stream); break;
         case 2: e = launch_score<2>(a, g, ctx->stream); break;
         case 4: e = launch_score<4>(a, g, ctx->stream); break;
         case 8: e = launch_score<8>(a, g, ctx->stream); break;
-        case 16: e = launch_score<16>(a, g, ctx->stream); break;
-        default: e = launch_score<32>(a, g, ctx->stream); break;
+        default: e = launch_score<16>(a, g, ctx->stream); break;
     }
     if (e != hipSuccess) return hip_fail(ctx, e, "score_kernel launch");
     return ORLOJ_OK;
@@ -999,4 +1237,3 @@ int orloj_select_batch(orloj_ctx* ctx, const orloj_grid* grid, const orloj_queue
 }
 
 }  // extern "C"
-

@@ -76,11 +76,11 @@ def load(path: Optional[str] = None):
     L.orloj_last_error.restype = ctypes.c_char_p
     L.orloj_sync.argtypes = [_VP]
     L.orloj_sync.restype = ctypes.c_int
-    L.orloj_build_cdfs.argtypes = [_VP, ctypes.c_int64, ctypes.c_int32, _VP, _VP]
+    L.orloj_build_cdfs.argtypes = [_VP, ctypes.c_int64, ctypes.c_int32, _VP, _VP, _VP]
     L.orloj_build_cdfs.restype = ctypes.c_int
     L.orloj_output_sizes.argtypes = [_GP, _QP, ctypes.c_int32, _I64P, _I64P, _I64P, _I64P]
     L.orloj_output_sizes.restype = ctypes.c_int
-    L.orloj_score_candidates.argtypes = [_VP, _GP, _VP, _QP, ctypes.c_double, ctypes.c_int32,
+    L.orloj_score_candidates.argtypes = [_VP, _GP, _VP, _VP, _QP, ctypes.c_double, ctypes.c_int32,
                                          _VP, _VP, _VP, _VP, _VP, _VP]
     L.orloj_score_candidates.restype = ctypes.c_int
     L.orloj_select_batch.argtypes = [_VP, _GP, _QP, ctypes.c_int32, _VP, _VP, _VP, _VP, _VP]
@@ -139,9 +139,11 @@ class Context:
         self._check(self.L.orloj_sync(self.ctx))
 
     # -- orloj_build_cdfs ------------------------------------------------------
-    def build_cdfs(self, counts: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    def build_cdfs(self, counts: torch.Tensor, out: Optional[torch.Tensor] = None,
+                   support: Optional[torch.Tensor] = None) -> torch.Tensor:
         """counts [..., K] (uint32 stored as int32 or uint32) -> 1 - CDF at
-        each bin's right edge, float32."""
+        each bin's right edge, float32.  If `support` (int32 [..., 2]) is
+        given, each row's first and last bin holding mass are written to it."""
         _need_cuda(counts, "counts", (torch.int32, torch.uint32), self.device)
         K = counts.shape[-1]
         if out is None:
@@ -149,8 +151,13 @@ class Context:
         _need_cuda(out, "out", (torch.float32,), self.device)
         if out.shape != counts.shape:
             raise ValueError("out must have the shape of counts")
+        if support is not None:
+            _need_cuda(support, "support", (torch.int32,), self.device)
+            if support.shape != counts.shape[:-1] + (2,):
+                raise ValueError("support must have shape counts.shape[:-1] + (2,)")
         rows = counts.numel() // K if K else 0
-        self._check(self.L.orloj_build_cdfs(self.ctx, rows, K, _ptr(counts), _ptr(out)))
+        self._check(self.L.orloj_build_cdfs(self.ctx, rows, K, _ptr(counts), _ptr(out),
+                                            _ptr(support)))
         return out
 
 
@@ -194,16 +201,18 @@ class Scorer:
     candidates and selects a batch per model through the C ABI."""
 
     def __init__(self, wl, ctx: Optional[Context] = None, prefix_mode: int = PREFIX_TRIANGLE,
-                 counts_device: Optional[torch.Tensor] = None):
+                 counts_device: Optional[torch.Tensor] = None, trim: bool = True):
         self.ctx = ctx or Context()
         self.wl = wl
         self.mode = prefix_mode
+        self.trim = trim
         dev = self.ctx.device
         if counts_device is not None:
             self.counts = counts_device
         else:
             self.counts = torch.from_numpy(np.ascontiguousarray(wl.counts).view(np.int32)).to(dev)
         self.ccdf = torch.empty(self.counts.shape, dtype=torch.float32, device=dev)
+        self.support = torch.empty(self.counts.shape[:-1] + (2,), dtype=torch.int32, device=dev)
         self.width = torch.from_numpy(np.ascontiguousarray(wl.bin_width_ms, np.float64)).to(dev)
         self.grid = make_grid(wl.n_models, wl.n_classes, wl.n_bins, wl.batch_sizes, self.width)
         self.set_queues(wl.queue_off, wl.cls, wl.deadline_ms, wl.now_ms)
@@ -232,13 +241,14 @@ class Scorer:
 
     # -- the three entry points --------------------------------------------------
     def build(self):
-        self.ctx.build_cdfs(self.counts, self.ccdf)
+        self.ctx.build_cdfs(self.counts, self.ccdf, self.support)
 
     def score(self, b_expo: Optional[float] = None):
         b = self.wl.b_expo if b_expo is None else b_expo
         c = self.ctx
         c._check(c.L.orloj_score_candidates(
-            c.ctx, ctypes.byref(self.grid), _ptr(self.ccdf), ctypes.byref(self.queues),
+            c.ctx, ctypes.byref(self.grid), _ptr(self.ccdf),
+            _ptr(self.support) if self.trim else None, ctypes.byref(self.queues),
             float(b), self.mode, _ptr(self.d_cand_off), _ptr(self.d_prob_off),
             _ptr(self.finish_prob), _ptr(self.expected_finish), _ptr(self.expected_latency),
             _ptr(self.score_out)))

@@ -76,13 +76,13 @@ def test_output_sizes_rejects_bad_arguments(lib):
 
 def test_null_context_is_rejected_without_touching_the_gpu(lib):
     g, qs, _ = _grid_queues([1, 2], [3])
-    rc = lib.orloj_score_candidates(None, ctypes.byref(g), None, ctypes.byref(qs), 1e-4, 0,
+    rc = lib.orloj_score_candidates(None, ctypes.byref(g), None, None, ctypes.byref(qs), 1e-4, 0,
                                     None, None, None, None, None, None)
     assert rc == O.ORLOJ_E_INVALID
     rc = lib.orloj_select_batch(None, ctypes.byref(g), ctypes.byref(qs), 0, None, None, None,
                                 None, None)
     assert rc == O.ORLOJ_E_INVALID
-    assert lib.orloj_build_cdfs(None, 1, 4, None, None) == O.ORLOJ_E_INVALID
+    assert lib.orloj_build_cdfs(None, 1, 4, None, None, None) == O.ORLOJ_E_INVALID
     assert lib.orloj_sync(None) == O.ORLOJ_E_INVALID
     assert lib.orloj_last_error(None)
     lib.orloj_destroy(None)

@@ -32,10 +32,15 @@ def ctx():
     return O.Context()
 
 
-def run_gpu(wl, ctx, mode=0, b_expo=None):
-    sc = O.Scorer(wl, ctx, prefix_mode=mode)
+def run_gpu(wl, ctx, mode=0, b_expo=None, trim=True):
+    sc = O.Scorer(wl, ctx, prefix_mode=mode, trim=trim)
     out = sc.run(build=True, b_expo=b_expo)
     return sc, out
+
+
+def assert_same_bits(a, b):
+    for k in a:
+        assert np.array_equal(a[k].view(np.uint8), b[k].view(np.uint8)), k
 
 
 # ---------------------------------------------------------------- build_cdfs
@@ -67,6 +72,33 @@ def test_build_cdfs_matches_oracle(ctx, K):
         # the fp64 rounding of 1 - F on the oracle side)
         err = np.abs(g - ref)
         assert np.all(err <= 2.0 ** -24 * ref + 1e-15), (i, np.max(err / np.maximum(ref, 1e-300)))
+
+
+@pytest.mark.parametrize("K", [1, 5, 64, 1000, 4096])
+def test_build_cdfs_support(ctx, K):
+    say(f"build_cdfs support K={K}")
+    r = np.random.default_rng(100 + K)
+    rows = 24
+    counts = np.zeros((rows, K), np.uint32)
+    for i in range(rows):
+        lo = int(r.integers(0, K))
+        hi = int(r.integers(lo, K))
+        counts[i, lo:hi + 1] = r.integers(0, 9, size=hi - lo + 1)
+        counts[i, lo] = counts[i, hi] = 3
+    counts[0] = 0
+    counts[0, K - 1] = 1                                 # only the last bin
+    counts[1] = 0
+    counts[1, 0] = 1                                     # only the first bin
+    d = torch.from_numpy(counts.view(np.int32)).to(ctx.device)
+    sup = torch.full((rows, 2), -7, dtype=torch.int32, device=ctx.device)
+    ccdf = ctx.build_cdfs(d, support=sup).cpu().numpy()
+    ctx.sync()
+    sup = sup.cpu().numpy()
+    for i in range(rows):
+        nz = np.nonzero(counts[i])[0]
+        assert sup[i, 0] == nz[0] and sup[i, 1] == nz[-1], i
+        # the entries the scorer may skip hold exactly 1 and 0
+        assert np.all(ccdf[i, :nz[0]] == 1.0) and np.all(ccdf[i, nz[-1]:] == 0.0), i
 
 
 def test_build_cdfs_empty_histogram_is_a_data_error(ctx):
@@ -108,6 +140,16 @@ def test_random_cases(ctx, case):
     ora = oracle.score_workload(wl)
     err = parity.compare(wl, got, ora)
     say("  max errors", err)
+
+
+@pytest.mark.parametrize("case", [RANDOM_CASES[i] for i in (0, 5, 6, 8, 13, 14)],
+                         ids=lambda c: f"seed{c['seed']}")
+def test_support_trimming_changes_no_bits(ctx, case):
+    say("trim on/off", case)
+    wl = W.random_case(**case)
+    _, on = run_gpu(wl, ctx, trim=True)
+    _, off = run_gpu(wl, ctx, trim=False)
+    assert_same_bits(on, off)
 
 
 @pytest.mark.parametrize("seed", [20, 21, 22])
@@ -163,6 +205,14 @@ def test_config5_full_launch_sampled_models(ctx, cfg5):
     for q in range(wl.n_models):
         E = got["expected_finish"][sc.h_cand_off[q]:sc.h_cand_off[q + 1]]
         assert np.all(E >= -1e-6) and np.all(E <= 64 + 1e-6)
+
+
+def test_config5_trimmed_and_full_reads_agree(ctx, cfg5):
+    wl = cfg5.subset(list(range(0, 128, 16)))
+    say("config 5, 8 models, trim on/off")
+    _, on = run_gpu(wl, ctx, trim=True)
+    _, off = run_gpu(wl, ctx, trim=False)
+    assert_same_bits(on, off)
 
 
 def test_config5_relaxed_slo_sampled(ctx):
