@@ -60,6 +60,43 @@ def algorithmic_bytes(wl, mode=0):
                 distinct_rows=rows, n_cands=n_c, n_probs=n_p)
 
 
+def support_table_bytes(wl, mode=0):
+    """Table bytes of the same distinct rows counting only each row's
+    support (first to last bin holding mass): the entries outside it are
+    known to be exactly 1 or 0 once the table is built."""
+    nz = wl.counts > 0
+    K = wl.n_bins
+    lo = np.argmax(nz, axis=-1)
+    hi = K - 1 - np.argmax(nz[..., ::-1], axis=-1)
+    width = hi - lo + 1
+    total = 0
+    for q in range(wl.n_models):
+        a, b = int(wl.queue_off[q]), int(wl.queue_off[q + 1])
+        N = b - a
+        cls = wl.cls[a:b]
+        for bi, s in enumerate(wl.batch_sizes):
+            cap = N if mode else min(int(s), N)
+            total += int(width[q, bi, np.unique(cls[:cap])].sum())
+    return total * 4
+
+
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "score_kernel_cfg5_traffic.txt")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2209_00159_amd", "csrc", "orloj.hip")
+
+
+def measured_traffic():
+    """HBM bytes per score launch from the committed rocprofv3 counter
+    summary, or None when it is missing or was taken on another version of
+    the kernel source."""
+    from paper_2209_00159_amd import profsum
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    d = profsum.read_summary(TRAFFIC_SUMMARY)
+    if d.get("source_sha256") != profsum.source_sha(KERNEL_SOURCE):
+        return None
+    return float(d["traffic_bytes_per_launch"])
+
+
 def valid_candidates(wl):
     return sum(min(int(s), wl.queue_len(q)) for q in range(wl.n_models) for s in wl.batch_sizes)
 
@@ -162,10 +199,18 @@ def main():
           f"{score_ms:.4f} ms", file=sys.stderr, flush=True)
 
     achieved = ab["total"] / (score_ms * 1e-3) / 1e9
+    traffic = measured_traffic()
+    sup_bytes = ab["total"] - ab["table"] + support_table_bytes(wl)
     roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
-                frac=round(achieved / HBM_PEAK_GBS, 4), traffic=None,
+                frac=round(achieved / HBM_PEAK_GBS, 4),
+                traffic=None if traffic is None else round(traffic),
+                traffic_unit="bytes/launch",
                 kernel="score_kernel", kernel_ms=round(score_ms, 5),
-                algorithmic_bytes=ab["total"])
+                algorithmic_bytes=ab["total"],
+                support_only_bytes=sup_bytes,
+                support_only_frac=round(sup_bytes / (score_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4))
+    if traffic is not None:
+        roof["traffic_gbs"] = round(traffic / (score_ms * 1e-3) / 1e9, 1)
     line = dict(
         metric=METRIC, value=evals / (ms_per_step * 1e-3), unit="evals/s", n_gpus=1,
         steps=args.steps, warmup=args.warmup, ms_per_step=round(ms_per_step, 5),

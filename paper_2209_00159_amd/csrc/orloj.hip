@@ -236,6 +236,7 @@ struct ScoreArgs {
     float* EL;
     float* S;
     const int32_t* sup;        // [M][nbs][C][2] first / last bin with mass, or NULL
+    const float* fill;         // [2][16] zeros, ones (the context's stand-in rows)
     int* err;
     double b;
     int M, C, K, nbs, rect, maxcap;
@@ -245,11 +246,10 @@ struct ScoreArgs {
 // Stand-in rows for lane chunks that lie wholly outside a row's support:
 // there every entry of 1 - F is exactly 0 (past the last bin with mass) or
 // exactly 1 (before the first), so the update G <- G - G (1 - F) gives the
-// same bits whether it reads the table or these constants.  They stay in
-// cache, so trimmed chunks cost no HBM traffic.
-__constant__ __align__(64) float kFill[2][16] = {
-    {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f},
-    {1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f}};
+// same bits whether it reads the table or these constants.  They live in a
+// small buffer of the context (kFillFloats floats: 16 zeros, then 16 ones),
+// stay in cache, and keep every row load a plain global load.
+constexpr int kFillFloats = 32;
 
 // Per-member lookup plan, built once per workgroup in LDS (it depends on
 // the deadline only, not on the step).
@@ -581,7 +581,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         const float* src = tab_qb + (size_t)c * (size_t)K + c0;
         int lim = K - 1 - c0;
         if (ones || zeros) {
-            src = kFill[ones ? 1 : 0];
+            src = a.fill + (ones ? 16 : 0);
             lim = CPL - 1;
         }
         load_chunk<CPL, EXACT>(v, src, lim);
@@ -875,7 +875,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const SelectArgs a) {
 struct orloj_ctx {
     int device;
     hipStream_t stream;
-    int* d_err;
+    int* d_err;      // device status word (data error bits)
+    float* d_fill;   // kFillFloats stand-in table entries: 16 zeros, 16 ones
     char msg[512];
 };
 
@@ -1007,17 +1008,23 @@ int orloj_create(orloj_ctx** out, int32_t hip_device, void* hip_stream) {
     ctx->device = hip_device;
     ctx->stream = (hipStream_t)hip_stream;
     ctx->d_err = nullptr;
+    ctx->d_fill = nullptr;
     ctx->msg[0] = 0;
     int n = 0;
     if (hipGetDeviceCount(&n) != hipSuccess || hip_device < 0 || hip_device >= n) {
         delete ctx;
         return ORLOJ_E_INVALID;
     }
+    float fill[kFillFloats];
+    for (int i = 0; i < kFillFloats; ++i) fill[i] = i < kFillFloats / 2 ? 0.0f : 1.0f;
     hipError_t e = hipSetDevice(hip_device);
     if (e == hipSuccess) e = hipMalloc((void**)&ctx->d_err, sizeof(int));
     if (e == hipSuccess) e = hipMemset(ctx->d_err, 0, sizeof(int));
+    if (e == hipSuccess) e = hipMalloc((void**)&ctx->d_fill, sizeof fill);
+    if (e == hipSuccess) e = hipMemcpy(ctx->d_fill, fill, sizeof fill, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         if (ctx->d_err) (void)hipFree(ctx->d_err);
+        if (ctx->d_fill) (void)hipFree(ctx->d_fill);
         delete ctx;
         return e == hipErrorOutOfMemory ? ORLOJ_E_NOMEM : ORLOJ_E_HIP;
     }
@@ -1030,6 +1037,7 @@ void orloj_destroy(orloj_ctx* ctx) {
     (void)hipSetDevice(ctx->device);
     (void)hipStreamSynchronize(ctx->stream);
     if (ctx->d_err) (void)hipFree(ctx->d_err);
+    if (ctx->d_fill) (void)hipFree(ctx->d_fill);
     delete ctx;
 }
 
@@ -1163,6 +1171,7 @@ int orloj_score_candidates(orloj_ctx* ctx, const orloj_grid* grid, const float* 
     ScoreArgs a;
     a.tab = d_ccdf;
     a.sup = d_support;
+    a.fill = ctx->d_fill;
     a.queue_off = queues->d_queue_off;
     a.cls = queues->d_class;
     a.deadline = queues->d_deadline_ms;
