@@ -454,7 +454,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     const int K = a.K;
     const int NP = (K + PW - 1) / PW;
 
-    const float d = (float)exp(-bw);                  // discount per bin
+    const double d64 = exp(-bw);                      // discount per bin
     const float log2d = (float)(-bw * 1.4426950408889634);
     const float gamma = (float)(-expm1(-bw) / bw);   // (1 - d) / (b w)
     const float omd = (float)(-expm1(-bw));          // 1 - d
@@ -645,17 +645,16 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             if (!skip) {
 #pragma unroll
                 for (int qq = 0; qq < Q::NQ; ++qq) {
-                    float zz = 0.0f;
+                    double zz = 0.0;
 #pragma unroll
                     for (int r = 0; r < Q::QW; ++r) {
                         const int j = qq * Q::QW + r;
                         const float t = (EXACT || pbase + j < K) ? buf[i][j] : 0.0f;
                         Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
                         gs[r] = qq == 0 ? Gacc[j] : gs[r] + Gacc[j];
-                        const float g = (float)Gacc[j];
-                        zz = r == 0 ? g : fmaf(zz, d, g);
+                        zz = r == 0 ? Gacc[j] : fma(zz, d64, Gacc[j]);
                     }
-                    zqv[qq] = zz;
+                    zqv[qq] = (float)zz;
                 }
             }
             // the slot is refilled only after the update has consumed it, so
