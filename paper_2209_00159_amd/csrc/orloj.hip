@@ -961,9 +961,11 @@ hipError_t launch_score_v(const ScoreArgs& a, unsigned grid, hipStream_t st) {
 }
 
 // Bins per lane chunk: panels of 64 chunks of CPL bins, at most kMaxChunk
-// bins per lane (larger rows take more panels).  A panel pass re-reads the
-// slice of each member's row once per member; narrow panels keep those
-// slices in L2 between the re-reads of a class.
+// bins per lane (larger rows take more panels).  Wider panels spread each
+// step's cross-lane reductions over more bins; narrower ones need fewer
+// registers (more waves per SIMD) and re-read a repeated class's row slice
+// sooner, while it may still sit in L2.  16 bins per lane (144 VGPRs, three
+// waves per SIMD) balances the two on gfx950.
 constexpr int kMaxChunk = 16;
 
 int score_chunk(int K) {

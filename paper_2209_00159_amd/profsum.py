@@ -11,13 +11,15 @@ per launch of one kernel, each scaled by what the same counter reads for a
 plain device copy of known size run in the same process (bench.py
 --calibrate-copy copies N bytes once): scale = N / (counter KiB x 1024).  It
 writes a `key: value` text summary that bench.py reads back while the
-kernel's source is unchanged (the summary records the source's SHA-256).
+kernel's code is unchanged (the summary records a SHA-256 of the source
+with comments and whitespace removed).
 """
 from __future__ import annotations
 
 import argparse
 import csv
 import hashlib
+import re
 import statistics
 import sys
 from collections import defaultdict
@@ -93,8 +95,15 @@ def _kernel_and_copy(path, counter, kernel):
 
 
 def source_sha(path) -> str:
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    """SHA-256 of the source with comments and whitespace removed, so that
+    editing documentation does not invalidate a counter summary while any
+    change to the code does."""
+    with open(path) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    text = re.sub(r"\s+", "", text)
+    return hashlib.sha256(text.encode()).hexdigest()
 
 
 def traffic(fetch_csv, write_csv, kernel, copy_bytes, source, out):
