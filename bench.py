@@ -125,6 +125,25 @@ def cpu_baseline(config_id, max_models, budget_s=15.0):
                 seconds=dt, decisions_per_s=done / dt)
 
 
+def oracle_on_states(wl, recorded, budget_s=10.0):
+    """The oracle on decision states recorded by the scheduling loop, in
+    order, for about budget_s seconds: decisions/s, and how many of its
+    selections equal the GPU's."""
+    import oracle
+    t0 = time.perf_counter()
+    done = same = 0
+    for dec in recorded:
+        sub = wl.subset([dec.model]).with_queues([(dec.cls, dec.deadline_ms)], [dec.now_ms])
+        o = oracle.score_workload(sub)
+        done += 1
+        same += int((int(o["sel_n"][0]), int(o["sel_bs"][0])) == (dec.sel_n, dec.sel_bs))
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return dict(decisions_per_s=done / dt, states=done, same_selection=same, seconds=round(dt, 2),
+                cores=1)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -135,6 +154,9 @@ def main():
                     help="most models the CPU oracle sample may take (it stops after ~15 s)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workers", type=int, default=16)
+    ap.add_argument("--trace-arrivals", type=int, default=20_000,
+                    help="arrivals of the configuration-5 trace replayed by the scheduling "
+                         "loop after the timed steps (0 = skip)")
     ap.add_argument("--no-trim", action="store_true",
                     help="score without the table support (every table entry is read)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -235,9 +257,33 @@ def main():
         torch.cuda.synchronize()
         line["calibration_copy_bytes"] = src.numel() * 4
         del src, dst
+    recorded = []
+    if args.trace_arrivals and args.config == 5:
+        from paper_2209_00159_amd import schedsim
+        print(f"[bench] scheduling loop over {args.trace_arrivals} arrivals", file=sys.stderr,
+              flush=True)
+        loop = schedsim.TraceLoop(wl, schedsim.config5_trace(args.trace_arrivals), ctx=ctx,
+                                  record_every=25, record_limit=400,
+                                  tables=(sc.ccdf, sc.support if not args.no_trim else None))
+        st = loop.run()
+        recorded = st.recorded
+        d = st.as_dict()
+        line["trace"] = dict(
+            arrivals=args.trace_arrivals, simulated_ms=round(d["sim_ms"], 1), ticks=d["ticks"],
+            launches=d["launches"], decisions=d["decisions"], dispatched=d["dispatched"],
+            dropped=d["dropped"], finish_rate=round(d["finish_rate"], 4),
+            decisions_per_s=round(d["decisions_per_s"], 1),
+            decisions_per_device_s=round(d["decisions_per_device_s"], 1),
+            note="decisions_per_s: wall clock of the whole host loop (Python queue handling "
+                 "included); decisions_per_device_s: queue upload + score + select + "
+                 "selection download per tick only")
+        print(f"[bench] loop: {d['decisions']} decisions in {d['wall_s']:.2f} s wall "
+              f"({d['device_s']:.2f} s on device)", file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(args.config, args.cpu_models)
+        if recorded:
+            line["cpu_baseline"]["trace"] = oracle_on_states(wl, recorded, budget_s=10.0)
     print(json.dumps(line), flush=True)
 
 
