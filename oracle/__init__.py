@@ -46,6 +46,11 @@ def _bind(L):
         _U32P, ctypes.c_int64, _I32P, _F64P, ctypes.c_double, ctypes.c_double,
         ctypes.c_int32, _F64P, _F64P, _F64P, _F64P, _F64P, _I32P, _I32P, _F64P]
     L.orloj_oracle_score_model.restype = ctypes.c_int
+    L.orloj_oracle_iterate_model.argtypes = [
+        ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _I32P, ctypes.c_double, _U32P, _F64P,
+        ctypes.c_int64, _I32P, _F64P, ctypes.c_double, ctypes.c_double, _I32P, _F64P, _I32P,
+        _I32P, _I32P]
+    L.orloj_oracle_iterate_model.restype = ctypes.c_int
     return L
 
 
@@ -153,3 +158,46 @@ def score_workload(wl, prefix_mode: int = 0, models: Optional[Sequence[int]] = N
     out["sel_score"] = np.array([p["sel_score"] for p in parts])
     out["per_model"] = parts
     return out
+
+
+def iterate_model(counts, batch_sizes, bin_width_ms, cls, deadline_ms, now_ms, b_expo,
+                  weights=None, L=None) -> dict:
+    """One Algorithm 1 iteration of one model (see orloj_oracle_iterate_model)."""
+    L = L or lib()
+    cnt = np.ascontiguousarray(counts, dtype=np.uint32)
+    B, C, K = cnt.shape
+    bs = np.ascontiguousarray(batch_sizes, dtype=np.int32)
+    cl = np.ascontiguousarray(cls, dtype=np.int32)
+    dl = np.ascontiguousarray(deadline_ms, dtype=np.float64)
+    wt = None if weights is None else np.ascontiguousarray(weights, dtype=np.float64)
+    N = cl.size
+    timed_out = np.zeros(max(N, 1), np.int32)
+    score = np.zeros(max(N, 1))
+    batch = np.full(max(int(bs[-1]), 1), -1, np.int32)
+    cand = np.zeros(1, np.int32)
+    bn = np.zeros(1, np.int32)
+    rc = L.orloj_oracle_iterate_model(
+        C, K, B, _p(bs, _I32P), float(bin_width_ms), _p(cnt, _U32P),
+        _p(wt, _F64P) if wt is not None else None, N, _p(cl, _I32P), _p(dl, _F64P),
+        float(now_ms), float(b_expo), _p(timed_out, _I32P), _p(score, _F64P), _p(cand, _I32P),
+        _p(batch, _I32P), _p(bn, _I32P))
+    if rc:
+        raise OracleError(f"orloj_oracle_iterate_model rc={rc}")
+    return dict(timed_out=timed_out[:N], score=score[:N], cand_bs=int(cand[0]),
+                batch=batch[:int(bn[0])].copy())
+
+
+def iterate_workload(wl, weights=None, models: Optional[Sequence[int]] = None, L=None) -> dict:
+    """Algorithm 1 for every model of a workload (or the listed ones);
+    per-request outputs concatenated in model order."""
+    models = list(range(wl.n_models)) if models is None else list(models)
+    parts = []
+    for q in models:
+        m = wl.model(q)
+        parts.append(iterate_model(m["counts"], wl.batch_sizes, m["bin_width_ms"], m["cls"],
+                                   m["deadline_ms"], m["now_ms"], wl.b_expo,
+                                   None if weights is None else weights[q], L))
+    cat = lambda k: (np.concatenate([p[k] for p in parts]) if parts else np.zeros(0))
+    return dict(timed_out=cat("timed_out").astype(np.int32), score=cat("score"),
+                cand_bs=np.array([p["cand_bs"] for p in parts], np.int32),
+                batch=[p["batch"] for p in parts], per_model=parts)

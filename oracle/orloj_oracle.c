@@ -256,3 +256,176 @@ int orloj_oracle_score_model(int32_t n_classes, int32_t n_bins, int32_t n_bs,
     free(F); free(G); free(mass);
     return ORACLE_OK;
 }
+
+/*
+ * One scheduler iteration (§3.2 Algorithm 1) for one model, with the paper's
+ * own per-request priority (§4.1 Eq. (1)-(2), §4.2, §4.3).
+ *
+ * Readings taken:
+ *   - EstimateBatchLatency of the drop phase is read as "could the request
+ *     finish by its deadline run alone at batch size s": r stays in Q_s iff
+ *     F_{c_r,s}(tau_r) > 0.  A request in no Q_s is timed out.
+ *   - The candidate batch size takes the batch sizes ordered by
+ *     (D_{Q_s}, s) descending, D_{Q_s} the earliest deadline in Q_s, and
+ *     picks the first one whose Q_s holds at least s requests (an empty Q_s
+ *     never qualifies).
+ *   - The batch a request joins is unknown when its priority is computed
+ *     (§4.3), so its batch latency at batch size s is the max of its own
+ *     latency and s - 1 others drawn independently from the model's class
+ *     mix F_mix,s = sum_c pi_c F_{c,s} (pi uniform unless weights are given):
+ *     CDF F_{c_r,s} F_mix,s^(s-1) (§4.2.1: the max of k identical variables
+ *     has CDF F^k).  E[L] in the priority is the model-wide expected batch
+ *     latency, of F_mix,s^s (§4.3: all of the model's distributions).
+ *   - PopBatch returns the s requests of Q_s with the largest priority at
+ *     batch size s; equal priorities go to the earlier queue position.
+ *
+ * counts is [n_bs][n_classes][n_bins]; weights (n_classes, may be NULL) are
+ * the class mix; the queue is sorted by deadline.  Outputs:
+ *   timed_out[N]   1 when the request is in no Q_s
+ *   score[N]       priority at the candidate batch size for requests in
+ *                  Q_cand, else 0
+ *   *cand_bs       the candidate batch size (0: no batch)
+ *   batch[cand_bs] queue indices of the popped batch, highest priority first
+ *   *batch_n       cand_bs, or 0
+ */
+int orloj_oracle_iterate_model(int32_t n_classes, int32_t n_bins, int32_t n_bs,
+                               const int32_t *batch_sizes, double bin_width_ms,
+                               const uint32_t *counts, const double *weights,
+                               int64_t n_queue, const int32_t *cls, const double *deadline_ms,
+                               double now_ms, double b_expo, int32_t *timed_out,
+                               double *score, int32_t *cand_bs, int32_t *batch,
+                               int32_t *batch_n)
+{
+    const int32_t C = n_classes, K = n_bins;
+    const double w = bin_width_ms, b = b_expo;
+    if (C < 1 || K < 1 || n_bs < 1 || !batch_sizes || !counts || n_queue < 0 ||
+        !(w > 0.0) || !(b > 0.0) || !cand_bs || !batch_n)
+        return ORACLE_E_INVALID;
+    if (n_queue > 0 && (!cls || !deadline_ms || !timed_out || !score))
+        return ORACLE_E_INVALID;
+    for (int32_t i = 0; i < n_bs; ++i)
+        if (batch_sizes[i] < 1 || (i > 0 && batch_sizes[i] <= batch_sizes[i - 1]))
+            return ORACLE_E_INVALID;
+    for (int64_t i = 0; i < n_queue; ++i) {
+        if (cls[i] < 0 || cls[i] >= C || isnan(deadline_ms[i]))
+            return ORACLE_E_DATA;
+        if (i > 0 && deadline_ms[i] < deadline_ms[i - 1])
+            return ORACLE_E_DATA;
+    }
+    double wsum = 0.0;
+    if (weights) {
+        for (int32_t c = 0; c < C; ++c) {
+            if (!(weights[c] >= 0.0))
+                return ORACLE_E_INVALID;
+            wsum += weights[c];
+        }
+        if (!(wsum > 0.0))
+            return ORACLE_E_INVALID;
+    }
+
+    size_t row = (size_t)K + 1;
+    double *F = (double *)malloc(sizeof(double) * row * (size_t)n_bs * (size_t)C);
+    double *mix = (double *)malloc(sizeof(double) * row);
+    double *G = (double *)malloc(sizeof(double) * row);
+    double *dG = (double *)malloc(sizeof(double) * (size_t)K);
+    int64_t *in_q = (int64_t *)malloc(sizeof(int64_t) * (size_t)n_bs);
+    int64_t *first = (int64_t *)malloc(sizeof(int64_t) * (size_t)n_bs);
+    int64_t *order = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n_queue > 0 ? n_queue : 1));
+    if (!F || !mix || !G || !dG || !in_q || !first || !order) {
+        free(F); free(mix); free(G); free(dG); free(in_q); free(first); free(order);
+        return ORACLE_E_NOMEM;
+    }
+    int rc = ORACLE_OK;
+    for (int32_t bi = 0; bi < n_bs && rc == ORACLE_OK; ++bi)
+        for (int32_t c = 0; c < C; ++c) {
+            size_t t = (size_t)bi * (size_t)C + (size_t)c;
+            if (orloj_oracle_cdf(K, counts + t * (size_t)K, F + t * row)) {
+                rc = ORACLE_E_DATA;
+                break;
+            }
+        }
+
+    /* Drop phase: Q_s membership, |Q_s| and the earliest deadline in Q_s. */
+    for (int32_t bi = 0; bi < n_bs && rc == ORACLE_OK; ++bi) {
+        in_q[bi] = 0;
+        first[bi] = -1;
+    }
+    for (int64_t r = 0; r < n_queue && rc == ORACLE_OK; ++r) {
+        double tau = deadline_ms[r] - now_ms;
+        int any = 0;
+        for (int32_t bi = 0; bi < n_bs; ++bi) {
+            const double *Fr = F + ((size_t)bi * (size_t)C + (size_t)cls[r]) * row;
+            if (finish_probability(Fr, K, w, tau) > 0.0) {
+                any = 1;
+                if (in_q[bi]++ == 0)
+                    first[bi] = r;
+            }
+        }
+        timed_out[r] = any ? 0 : 1;
+        score[r] = 0.0;
+    }
+
+    /* Candidate batch size: (D_{Q_s}, s) descending, first with |Q_s| >= s. */
+    int32_t cand = -1;
+    for (int32_t bi = 0; bi < n_bs && rc == ORACLE_OK; ++bi) {
+        if (in_q[bi] < batch_sizes[bi])
+            continue;
+        if (cand < 0) {
+            cand = bi;
+            continue;
+        }
+        double d_new = deadline_ms[first[bi]], d_old = deadline_ms[first[cand]];
+        if (d_new > d_old || (d_new == d_old && batch_sizes[bi] > batch_sizes[cand]))
+            cand = bi;
+    }
+    *cand_bs = 0;
+    *batch_n = 0;
+    if (rc == ORACLE_OK && cand >= 0) {
+        const int32_t s = batch_sizes[cand];
+        /* The class mix at batch size s and the model-wide E[L] of mix^s. */
+        for (int32_t k = 0; k <= K; ++k) {
+            double acc = 0.0;
+            for (int32_t c = 0; c < C; ++c) {
+                double pc = weights ? weights[c] / wsum : 1.0 / (double)C;
+                acc += pc * F[((size_t)cand * (size_t)C + (size_t)c) * row + (size_t)k];
+            }
+            mix[k] = acc;
+        }
+        double el_model = 0.0;
+        for (int32_t k = 0; k < K; ++k)
+            el_model += 1.0 - 0.5 * (pow(mix[k], s) + pow(mix[k + 1], s));
+        el_model *= w;
+        /* Priority of every request in Q_s, from its own batch law. */
+        int64_t nq = 0;
+        for (int64_t r = 0; r < n_queue; ++r) {
+            double tau = deadline_ms[r] - now_ms;
+            const double *Fr = F + ((size_t)cand * (size_t)C + (size_t)cls[r]) * row;
+            if (!(finish_probability(Fr, K, w, tau) > 0.0))
+                continue;
+            for (int32_t k = 0; k <= K; ++k)
+                G[k] = Fr[k] * pow(mix[k], s - 1);
+            for (int32_t k = 0; k < K; ++k)
+                dG[k] = G[k + 1] - G[k];
+            score[r] = priority_times_latency(dG, K, w, tau, b) / el_model;
+            order[nq++] = r;
+        }
+        /* PopBatch: the s best by priority, ties to the earlier position
+         * (a stable selection pass, plainly O(s * |Q_s|)). */
+        for (int32_t j = 0; j < s; ++j) {
+            int64_t best = j;
+            for (int64_t i = j + 1; i < nq; ++i) {
+                double si = score[order[i]], sb = score[order[best]];
+                if (si > sb || (si == sb && order[i] < order[best]))
+                    best = i;
+            }
+            int64_t tmp = order[j];
+            order[j] = order[best];
+            order[best] = tmp;
+            batch[j] = (int32_t)order[j];
+        }
+        *cand_bs = s;
+        *batch_n = s;
+    }
+    free(F); free(mix); free(G); free(dG); free(in_q); free(first); free(order);
+    return rc;
+}

@@ -508,6 +508,157 @@ def pin_toy_example(L):
     assert np.all(pri[taus <= 9.0] == 0.0)                 # then 0
 
 
+# ---------------------------------------------------------------- Algorithm 1 iteration
+def iterate(L, counts_bcK, batch_sizes, cls, taus, w, b=1e-4, now=500.0, weights=None):
+    dl = now + np.asarray(taus, np.float64)
+    out = oracle.iterate_model(counts_bcK, batch_sizes, w, np.asarray(cls, np.int32), dl, now, b,
+                               weights=weights, L=L)
+    out["tau"] = dl - now
+    return out
+
+
+def pin_iterate_one_class(L):
+    """With a single class the law of a request's batch at batch size s is
+    that of s identical members, F^s: its priority must equal the
+    candidate-scoring priority of a member of the s-member batch of that
+    class (a product of s CDFs there, a power of the mix here), for every
+    request in Q_s, and the model-wide E[L] must be that batch's E[L_B]."""
+    r = rng(61)
+    K = 40
+    row = r.integers(0, 30, size=K)
+    row[:3] = 0
+    row[-1] += 1
+    w, b = 2.0, 0.01
+    for s in (1, 3, 6):
+        N = s + 3
+        taus = np.sort(r.uniform(8.0, 90.0, size=N))
+        it = iterate(L, row[None, None, :], [s], np.zeros(N), taus, w, b)
+        assert it["cand_bs"] == s
+        sc = run_model(L, row[None], np.zeros(s), taus[:s], w, b, batch_sizes=[s])
+        E = sc["expected_latency_ms"][s - 1]
+        for m in range(1, s + 1):
+            pr = sc["priority"][slot(s, m)]
+            assert abs(it["score"][m - 1] - pr) <= 1e-12 + 1e-10 * abs(pr), (s, m, it["score"][m - 1], pr)
+        # E[L] enters as the normaliser: score * E[L_B] is the bare Eq. (2) sum
+        for m in range(1, s + 1):
+            assert abs(it["score"][m - 1] * E - sc["priority"][slot(s, m)] * E) <= 1e-10
+
+
+def pin_iterate_point_mix(L):
+    """A class mix concentrated on one class m0 makes the batch of a request
+    of class c at batch size s the batch {c, m0 x (s-1)}: its priority must
+    equal the candidate-scoring priority of that request as the first member
+    of the prefix [c, m0, ..., m0], divided by the mix's own E[L] instead of
+    that batch's."""
+    r = rng(62)
+    K, C = 30, 3
+    rows = r.integers(0, 20, size=(C, K))
+    rows[rows.sum(axis=1) == 0, -1] = 1
+    w, b, s, m0 = 1.5, 0.02, 4, 2
+    weights = np.zeros(C)
+    weights[m0] = 1.0
+    checked = 0
+    for c in range(C):
+        taus = np.array([25.0, 26.0, 27.0, 28.0, 29.0])
+        cls = [c, m0, m0, m0, m0]
+        it = iterate(L, rows[None], [s], cls, taus, w, b, weights=weights)
+        if it["cand_bs"] != s or it["score"][0] == 0.0:
+            continue
+        sc = run_model(L, rows, cls[:s], [taus[0]] * s, w, b, batch_sizes=[s])
+        E_batch = sc["expected_latency_ms"][s - 1]
+        pr_times_E = sc["priority"][slot(s, 1)] * E_batch
+        mixonly = run_model(L, rows, [m0] * s, [taus[0]] * s, w, b, batch_sizes=[s])
+        E_mix = mixonly["expected_latency_ms"][s - 1]
+        got = it["score"][0]
+        assert abs(got - pr_times_E / E_mix) <= 1e-12 + 1e-9 * abs(got), (c, got, pr_times_E / E_mix)
+        checked += 1
+    assert checked >= 2
+
+
+def pin_iterate_monte_carlo_mix(L):
+    """Monte Carlo of the mix law: a request of class c plus s-1 members
+    whose classes are drawn from the weights; the Eq. (1) event under that
+    latency, divided by the model-wide E[L] (Monte Carlo of s mix members),
+    must match the oracle's priority within 4 sigma."""
+    r = rng(63)
+    K, C, s = 16, 3, 3
+    rows = r.integers(0, 12, size=(C, K))
+    rows[rows.sum(axis=1) == 0, -1] = 1
+    weights = np.array([0.5, 0.3, 0.2])
+    w, b = 1.0, 0.05
+    taus = np.array([9.0, 11.5, 14.0])
+    cls = np.array([1, 0, 2])
+    it = iterate(L, rows[None], [s], cls, taus, w, b, weights=weights)
+    assert it["cand_bs"] == s
+    S = 600_000
+
+    def draw(c, size):
+        p = rows[c] / rows[c].sum()
+        return (r.choice(K, size=size, p=p) + r.random(size)) * w
+
+    def draw_mix(size):
+        cc = r.choice(C, size=size, p=weights)
+        out = np.empty(size)
+        for c in range(C):
+            sel = cc == c
+            out[sel] = draw(c, int(sel.sum()))
+        return out
+
+    model_lat = np.max(np.stack([draw_mix(S) for _ in range(s)]), axis=0)
+    E_mix = model_lat.mean()
+    for i, (c, tau) in enumerate(zip(cls, taus)):
+        lat = draw(c, S)
+        for _ in range(s - 1):
+            lat = np.maximum(lat, draw_mix(S))
+        delay = r.exponential(1.0 / b, size=S)
+        ev = ((lat <= tau) & (tau < lat + delay)).mean()
+        got = it["score"][i] * E_mix
+        sig = math.sqrt(max(ev * (1 - ev), 1e-12) / S) + abs(got) * float(model_lat.std()) / math.sqrt(S) / E_mix
+        assert abs(ev - got) <= 4 * sig + 1e-9, (i, ev, got, sig)
+
+
+def pin_iterate_feasibility_and_popbatch(L):
+    """The drop phase against the counts themselves (a request can finish
+    by tau at batch size s iff tau lies past the left edge of the first bin
+    holding mass of its class's histogram), the candidate rule's defining
+    property, and PopBatch by brute force over all subsets of Q_cand."""
+    import itertools
+    r = rng(64)
+    for trial in range(40):
+        K, C = 12, 3
+        bsz = sorted(set(int(x) for x in r.integers(1, 5, size=3)))
+        B = len(bsz)
+        counts = r.integers(0, 6, size=(B, C, K))
+        counts[..., : int(r.integers(0, 6))] = 0
+        counts[counts.sum(axis=-1) == 0, -1] = 1
+        N = int(r.integers(0, 8))
+        w, b = 1.0, 0.05
+        taus = np.sort(r.uniform(-2.0, 14.0, size=N))
+        cls = r.integers(0, C, size=N)
+        it = iterate(L, counts, bsz, cls, taus, w, b)
+        first = np.argmax(counts > 0, axis=-1)                 # [B, C]
+        feas = np.array([[taus[i] > first[j, cls[i]] * w for j in range(B)] for i in range(N)],
+                        dtype=bool).reshape(N, B)
+        assert np.array_equal(it["timed_out"], (~feas.any(axis=1)).astype(np.int32)), trial
+        sizes = feas.sum(axis=0)
+        ok = [j for j in range(B) if sizes[j] >= bsz[j]]
+        if not ok:
+            assert it["cand_bs"] == 0 and it["batch"].size == 0
+            continue
+        key = lambda j: (taus[np.argmax(feas[:, j])], bsz[j])
+        jbest = max(ok, key=key)
+        assert it["cand_bs"] == bsz[jbest], trial
+        q = [i for i in range(N) if feas[i, jbest]]
+        sc = it["score"]
+        assert all(sc[i] == 0.0 for i in range(N) if i not in q)
+        best = max(sum(sc[list(c)]) for c in itertools.combinations(q, bsz[jbest]))
+        assert abs(sum(sc[it["batch"]]) - best) <= 1e-12 * max(1.0, best)
+        assert set(it["batch"]).issubset(q) and len(set(it["batch"])) == bsz[jbest]
+        assert all(sc[it["batch"][i]] >= sc[it["batch"][i + 1]] for i in range(len(it["batch"]) - 1))
+
+
 PINS = [pin_enumeration, pin_iid_power, pin_point_mass, pin_quadrature_medium, pin_b_to_zero,
         pin_monte_carlo_max, pin_monte_carlo_priority, pin_ozbey_eq8, pin_invariants,
-        pin_continuity, pin_edge_cases, pin_selection, pin_rect_mode, pin_toy_example]
+        pin_continuity, pin_edge_cases, pin_selection, pin_rect_mode, pin_toy_example,
+        pin_iterate_one_class, pin_iterate_point_mix, pin_iterate_monte_carlo_mix,
+        pin_iterate_feasibility_and_popbatch]

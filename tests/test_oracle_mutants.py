@@ -55,6 +55,23 @@ MUTANTS = {
     "select_nonpositive": ("if (have_best && best > 0.0) {", "if (have_best) {"),
     # step 8: over-long prefixes allowed
     "select_rect_mask": ("if (n <= batch_sizes[bi]) {", "if (1) {"),
+    # Algorithm 1: the request's batch holds s mix members besides it
+    "iter_mix_power": ("G[k] = Fr[k] * pow(mix[k], s - 1);", "G[k] = Fr[k] * pow(mix[k], s);"),
+    # Algorithm 1: model-wide E[L] of s - 1 mix members
+    "iter_el_power": ("pow(mix[k], s) + pow(mix[k + 1], s)",
+                      "pow(mix[k], s - 1) + pow(mix[k + 1], s - 1)"),
+    # Algorithm 1: the class mix ignores the weights
+    "iter_weights_ignored": ("double pc = weights ? weights[c] / wsum : 1.0 / (double)C;",
+                             "double pc = 1.0 / (double)C;"),
+    # Algorithm 1: a request is kept at every batch size
+    "iter_drop_never": ("if (finish_probability(Fr, K, w, tau) > 0.0) {",
+                        "if (finish_probability(Fr, K, w, tau) >= 0.0) {"),
+    # Algorithm 1: candidate order ascending in D_{Q_s}
+    "iter_cand_order": ("if (d_new > d_old || (d_new == d_old && batch_sizes[bi] > batch_sizes[cand]))",
+                        "if (d_new < d_old || (d_new == d_old && batch_sizes[bi] > batch_sizes[cand]))"),
+    # Algorithm 1: PopBatch takes the lowest priorities
+    "iter_pop_lowest": ("if (si > sb || (si == sb && order[i] < order[best]))",
+                        "if (si < sb || (si == sb && order[i] < order[best]))"),
 }
 
 
