@@ -11,6 +11,9 @@
  *                           batch CDF, E[L_B], finish probabilities,
  *                           expected finish count, priority score
  *   orloj_select_batch      highest-scoring candidate per model
+ *   orloj_build_model_laws  model-wide batch laws for the scheduler iteration
+ *   orloj_iterate           one Algorithm 1 iteration per model (drop phase,
+ *                           candidate batch size, PopBatch by priority)
  *
  * Conventions.  Pointers named d_* are device (HBM) pointers owned by the
  * caller; h_* pointers and the structs are host memory read during the call
@@ -184,6 +187,60 @@ int orloj_score_candidates(orloj_ctx *ctx, const orloj_grid *grid, const float *
 int orloj_select_batch(orloj_ctx *ctx, const orloj_grid *grid, const orloj_queues *queues,
                        int32_t prefix_mode, const int64_t *d_cand_off, const float *d_score,
                        int32_t *d_sel_n, int32_t *d_sel_bs, float *d_sel_score);
+
+/*
+ * The scheduler iteration of §3.2 Algorithm 1 with the paper's own
+ * per-request priority (§4.1 Eq. (1)-(2), §4.2, §4.3), data-parallel over
+ * every model's queue.  Two calls:
+ *
+ * orloj_build_model_laws (off the scheduling path; rebuild when the
+ * histograms, the class mix or b_expo change).  When a request's priority
+ * is computed, the batch it will run in is not yet known (§4.3), so its
+ * batch latency at batch size s is taken as the max of its own latency and
+ * s - 1 others drawn independently from the model's class mix
+ *   F_mix,s = sum_c pi_c F_{c,s}   (pi = d_class_weights[q][c] normalised;
+ *                                    NULL = uniform over the classes),
+ * and the expected batch latency in the priority is the model-wide one of
+ * F_mix,s^s (§4.2.1: the max of k identical variables has CDF F^k).  For
+ * every model q, batch-size index b and class c, at the right edge of bin k:
+ *   d_law[q][b][c][k]  = F_{c,b}(x_{k+1}) * F_mix,b(x_{k+1})^(s_b - 1)
+ *   d_disc[q][b][c][k] = sum_{i<=k} d_law[q][b][c][i] * d^(k-i),
+ *                        d = exp(-b_expo_per_ms * w_q)
+ *   d_model_el[q][b]   = E[L] of F_mix,b^(s_b), Eq. (5)       (ms)
+ * d_ccdf is orloj_build_cdfs' [M][n_bs][C][K] table; d_law and d_disc have
+ * its shape (float32), d_model_el is [M][n_bs] float32.  Negative, infinite
+ * or all-zero weights of a model are a data error (orloj_sync).
+ *
+ * orloj_iterate: one iteration for every model in one launch.  For model q
+ * at time now_q, with tau_r = D_r - now_q:
+ *   drop phase   r is kept at batch size s iff it could finish by its
+ *                deadline run alone at s: F_{c_r,s}(tau_r) > 0, i.e. tau_r is
+ *                past the left edge of the first bin with mass (read from
+ *                d_support, orloj_build_cdfs' support of the same table).
+ *                A request kept at no batch size is timed out.
+ *   candidate    batch sizes in (D_{Q_s}, s) descending order, D_{Q_s} the
+ *                earliest deadline kept at s; the first whose kept set holds
+ *                at least s requests (none: no batch).
+ *   PopBatch     the s kept requests with the largest priority at the
+ *                candidate size; equal priorities go to the earlier queue
+ *                position.
+ * Outputs: d_timed_out[N] int32 (1 = timed out), d_score[N] float32 (the
+ * priority at the candidate size for requests kept there, else 0),
+ * d_cand_bs[M] int32 (0 = no batch), d_batch[M][s_max] int32 (positions in
+ * the model's queue, highest priority first, then -1), s_max the largest
+ * batch size.  b_expo_per_ms must be the value the laws were built with.
+ * ORLOJ_E_UNSUPPORTED for a queue longer than 4096 requests or a batch size
+ * above 1024.  Queue data errors are reported by orloj_sync as for
+ * orloj_score_candidates.
+ */
+int orloj_build_model_laws(orloj_ctx *ctx, const orloj_grid *grid, const float *d_ccdf,
+                           const double *d_class_weights, double b_expo_per_ms,
+                           float *d_law, float *d_disc, float *d_model_el);
+
+int orloj_iterate(orloj_ctx *ctx, const orloj_grid *grid, const int32_t *d_support,
+                  const float *d_law, const float *d_disc, const float *d_model_el,
+                  const orloj_queues *queues, double b_expo_per_ms, int32_t *d_timed_out,
+                  float *d_score, int32_t *d_cand_bs, int32_t *d_batch);
 
 #ifdef __cplusplus
 }

@@ -40,6 +40,7 @@ constexpr int kErrDeadlineNaN = 4;
 constexpr int kErrUnsorted = 8;
 constexpr int kErrNowNaN = 16;
 constexpr int kErrWidth = 32;
+constexpr int kErrWeights = 64;
 
 // ---------------------------------------------------------------------------
 // wave64 helpers
@@ -871,6 +872,334 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const SelectArgs a) {
 // ===========================================================================
 // C ABI
 // ===========================================================================
+namespace {
+
+// ---------------------------------------------------------------------------
+// Scheduler iteration (§3.2 Algorithm 1) with the paper's own priority.
+//
+// laws_kernel: one workgroup per (model, batch size).  Thread t owns the VPT
+// consecutive bins [t*VPT, t*VPT + VPT).  It forms the model's class mix
+// F_mix = sum_c pi_c F_c in fp64, then for each class the CDF of a
+// request's batch latency, F_c F_mix^(s-1) (the request plus s-1 members
+// drawn from the mix; §4.2.1: the max of k identical variables has CDF
+// F^k), and its discounted prefix Z(k) = sum_{i<=k} G(x_{i+1}) d^(k-i),
+// d = e^{-b w}: an in-thread fp64 prefix, a weighted DPP scan across the
+// wave and a weighted combination across the four waves.  Block 0 of each
+// model also writes the model-wide E[L] of F_mix^s (§4.3).
+// ---------------------------------------------------------------------------
+struct LawArgs {
+    const float* tab;          // [M][nbs][C][K] 1 - F(x_{k+1})
+    const double* weights;     // [M][C] class mix, or NULL (uniform)
+    const double* width;       // [M]
+    float* law;                // [M][nbs][C][K]
+    float* disc;               // [M][nbs][C][K]
+    float* model_el;           // [M][nbs]
+    int* err;
+    double b;
+    int M, C, K, nbs;
+    int bs[ORLOJ_MAX_BATCH_SIZES];
+};
+
+template <int VPT>
+__global__ __launch_bounds__(kThreads) void laws_kernel(const LawArgs a) {
+    __shared__ float s_wave[kWaves];
+    __shared__ double s_el[kWaves];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int q = (int)(blockIdx.x / (unsigned)a.nbs);
+    const int bi = (int)(blockIdx.x % (unsigned)a.nbs);
+    const int K = a.K, C = a.C;
+    const int s = a.bs[bi];
+    const double w = a.width[q];
+    const double d = exp(-a.b * w);
+    const int base = tid * VPT;
+    const size_t row0 = ((size_t)q * (size_t)a.nbs + (size_t)bi) * (size_t)C;
+
+    // class mix and its powers at this thread's bins (padding bins: F = 1)
+    double mix[VPT];
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) mix[j] = 0.0;
+    double wsum = 0.0;
+    bool wbad = false;
+    for (int c = 0; c < C; ++c) {
+        const double wc = a.weights ? a.weights[(size_t)q * C + c] : 1.0;
+        wbad |= !(wc >= 0.0) || isinf(wc);
+        wsum += wc;
+    }
+    if (wbad || !(wsum > 0.0)) {
+        if (tid == 0) atomicOr(a.err, kErrWeights);
+        wsum = 1.0;
+    }
+    for (int c = 0; c < C; ++c) {
+        const double pc = (a.weights ? a.weights[(size_t)q * C + c] : 1.0) / wsum;
+        const float* t = a.tab + (row0 + (size_t)c) * (size_t)K;
+#pragma unroll
+        for (int j = 0; j < VPT; ++j) {
+            const int k = base + j;
+            const double F = k < K ? 1.0 - (double)t[k] : 1.0;
+            mix[j] = fma(pc, F, mix[j]);
+        }
+    }
+    double pm[VPT];
+    double el = 0.0;
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) {
+        pm[j] = s > 1 ? pow(mix[j], (double)(s - 1)) : 1.0;
+        if (base + j < K) el += 1.0 - pm[j] * mix[j];
+    }
+    // model-wide E[L] = w (1/2 + sum_k (1 - F_mix^s(x_{k+1})))
+    for (int o = 32; o > 0; o >>= 1) el += __shfl_xor(el, o, 64);
+    if (lane == 0) s_el[wv] = el;
+    __syncthreads();
+    if (tid == 0) {
+        double tot = 0.0;
+        for (int i = 0; i < kWaves; ++i) tot += s_el[i];
+        a.model_el[(size_t)q * a.nbs + bi] = (float)(w * (0.5 + tot));
+    }
+
+    // scan constants: a thread chunk spans VPT bins
+    const float log2d = (float)(-a.b * w * 1.4426950408889634);
+    float rp[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) rp[i] = exp2_hw(log2d * (float)(VPT << i));
+    const float w15 = exp2_hw(log2d * (float)(VPT * ((lane & 15) + 1)));
+    const float w31 = exp2_hw(log2d * (float)(VPT * (lane >= 32 ? lane - 31 : 0)));
+    const float d_wave = exp2_hw(log2d * (float)(64 * VPT));
+
+    for (int c = 0; c < C; ++c) {
+        const size_t r = (row0 + (size_t)c) * (size_t)K;
+        const float* t = a.tab + r;
+        double g[VPT];
+        double z = 0.0;
+#pragma unroll
+        for (int j = 0; j < VPT; ++j) {
+            const int k = base + j;
+            const double F = k < K ? 1.0 - (double)t[k] : 1.0;
+            g[j] = F * pm[j];
+            z = fma(z, d, g[j]);
+        }
+        // in-wave weighted scan of the chunk totals, then across the waves
+        const float A = wave_wscan((float)z, rp, w15, w31);
+        if (lane == 63) s_wave[wv] = A;
+        __syncthreads();
+        float carry = 0.0f;   // discounted sum of the earlier waves' bins, at the end of the last one
+#pragma unroll
+        for (int i = 0; i < kWaves; ++i)
+            if (i < wv) carry = fmaf(carry, d_wave, s_wave[i]);
+        __syncthreads();
+        // prefix up to the end of the previous thread chunk
+        const float prev = __shfl_up(A, 1, 64);
+        const float before = (lane > 0 ? prev : 0.0f) + carry * exp2_hw(log2d * (float)(VPT * lane));
+        double zz = (double)before;
+#pragma unroll
+        for (int j = 0; j < VPT; ++j) {
+            const int k = base + j;
+            zz = fma(zz, d, g[j]);
+            if (k < K) {
+                a.law[r + k] = (float)g[j];
+                a.disc[r + k] = (float)zz;
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// iterate_kernel: one workgroup per model.  Requests are strided over the
+// threads (request i on thread i mod 256).  For every batch size the drop
+// phase keeps a request iff its deadline lies past the left edge of its
+// class's first bin with mass at that batch size (then it could finish run
+// alone); counts and the earliest kept request come from wave ballots.
+// Thread 0 picks the candidate batch size ((D_{Q_s}, s) descending, first
+// with |Q_s| >= s).  Requests kept at the candidate size get their
+// priority from the model-law tables (Eq. (2) in the scan form:
+// gamma e^{-b theta w} (G_k - (1-d) Z(k-2)) + h_k psi(theta), over the
+// model-wide E[L]); PopBatch takes the s largest keys (kept flag, priority,
+// earlier position), found by bisection over the 64-bit keys, and orders
+// them by rank.
+// ---------------------------------------------------------------------------
+struct IterArgs {
+    const int32_t* sup;        // [M][nbs][C][2]
+    const float* law;          // [M][nbs][C][K]
+    const float* disc;         // [M][nbs][C][K]
+    const float* model_el;     // [M][nbs]
+    const int64_t* queue_off;
+    const int32_t* cls;
+    const double* deadline;
+    const double* now;
+    const double* width;
+    int32_t* timed_out;        // [N]
+    float* score;              // [N]
+    int32_t* cand_bs;          // [M]
+    int32_t* batch;            // [M][bs_max]
+    int* err;
+    double b;
+    int M, C, K, nbs, bs_max;
+    int bs[ORLOJ_MAX_BATCH_SIZES];
+};
+
+constexpr int kIterMaxBatch = 1024;      // largest batch size PopBatch orders in LDS
+constexpr int kIterMaxQueue = 4096;      // longest queue one workgroup ranks
+
+__global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
+    __shared__ int s_cnt[ORLOJ_MAX_BATCH_SIZES];
+    __shared__ int s_first[ORLOJ_MAX_BATCH_SIZES];
+    __shared__ int s_cand;
+    __shared__ unsigned long long s_part[kWaves];
+    __shared__ unsigned long long s_sel[kIterMaxBatch];
+    __shared__ int s_nsel;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int q = blockIdx.x;
+    const int64_t q0 = a.queue_off[q];
+    const int N = (int)(a.queue_off[q + 1] - q0);
+    const int nbs = a.nbs, C = a.C, K = a.K;
+    const double w = a.width[q];
+    const double nowq = a.now[q];
+    const bool wok = w > 0.0 && w < HUGE_VAL;
+    for (int i = tid; i < nbs; i += kThreads) {
+        s_cnt[i] = 0;
+        s_first[i] = 0x7fffffff;
+    }
+    if (tid == 0) { s_cand = -1; s_nsel = 0; }
+    __syncthreads();
+    const int32_t* sup_q = a.sup + (size_t)q * (size_t)nbs * (size_t)C * 2;
+
+    // drop phase
+    for (int i0 = 0; i0 < N; i0 += kThreads) {
+        const int i = i0 + tid;
+        const bool live = i < N;
+        int c = 0;
+        double tau = 0.0;
+        if (live) {
+            c = a.cls[q0 + i];
+            const double D = a.deadline[q0 + i];
+            int flag = 0;
+            if (c < 0 || c >= C) { flag |= kErrClassRange; c = 0; }
+            if (isnan(D)) flag |= kErrDeadlineNaN;
+            if (i > 0 && D < a.deadline[q0 + i - 1]) flag |= kErrUnsorted;
+            if (i == 0 && isnan(nowq)) flag |= kErrNowNaN;
+            if (i == 0 && !wok) flag |= kErrWidth;
+            if (flag) atomicOr(a.err, flag);
+            tau = D - nowq;
+        }
+        bool any = false;
+        for (int bi = 0; bi < nbs; ++bi) {
+            const int lo = sup_q[((size_t)bi * C + c) * 2];
+            const bool keep = live && wok && tau > (double)lo * w;
+            any |= keep;
+            const unsigned long long m = __ballot(keep);
+            if (lane == 0 && m) {
+                atomicAdd(&s_cnt[bi], __popcll(m));
+                atomicMin(&s_first[bi], i0 + wv * 64 + __ffsll((long long)m) - 1);
+            }
+        }
+        if (live) {
+            a.timed_out[q0 + i] = any ? 0 : 1;
+            a.score[q0 + i] = 0.0f;
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int cand = -1;
+        double dc = 0.0;
+        for (int bi = 0; bi < nbs; ++bi) {
+            if (s_cnt[bi] < a.bs[bi]) continue;
+            const double D = a.deadline[q0 + s_first[bi]];
+            if (cand < 0 || D > dc || (D == dc && a.bs[bi] > a.bs[cand])) {
+                cand = bi;
+                dc = D;
+            }
+        }
+        s_cand = cand;
+        a.cand_bs[q] = cand >= 0 ? a.bs[cand] : 0;
+    }
+    __syncthreads();
+    const int cand = s_cand;
+    int32_t* bq = a.batch + (size_t)q * (size_t)a.bs_max;
+    if (cand < 0) {
+        for (int j = tid; j < a.bs_max; j += kThreads) bq[j] = -1;
+        return;
+    }
+    const int s = a.bs[cand];
+
+    // priorities at the candidate size; keys = kept | priority bits | ~index
+    const double bw = a.b * w;
+    const double gamma = -expm1(-bw) / bw;
+    const double omd = -expm1(-bw);
+    const float el = a.model_el[(size_t)q * nbs + cand];
+    const size_t lrow0 = ((size_t)q * nbs + cand) * (size_t)C;
+    constexpr int kPer = kIterMaxQueue / kThreads;   // keys per thread, in registers
+    unsigned long long key[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) key[j] = 0ull;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int i = j * kThreads + tid;
+        if (i < N) {
+            int c = a.cls[q0 + i];
+            c = (c < 0 || c >= C) ? 0 : c;
+            const double tau = a.deadline[q0 + i] - nowq;
+            const int lo = sup_q[((size_t)cand * C + c) * 2];
+            if (wok && tau > (double)lo * w) {
+                const float* G = a.law + (lrow0 + c) * (size_t)K;
+                const float* Z = a.disc + (lrow0 + c) * (size_t)K;
+                const double u = tau / w;
+                double num;
+                if (u >= (double)K) {
+                    const double cg = gamma * exp(-a.b * (tau - (double)K * w));
+                    const double zk = K >= 2 ? (double)Z[K - 2] : 0.0;
+                    num = cg * (1.0 - omd * zk);
+                } else {
+                    const int k = (int)floor(u);
+                    const double th = u - (double)k;
+                    const double gk = k >= 1 ? (double)G[k - 1] : 0.0;
+                    const double gk1 = (double)G[k];
+                    const double zk = k >= 2 ? (double)Z[k - 2] : 0.0;
+                    const double cg = gamma * exp(-a.b * th * w);
+                    const double psi = -expm1(-a.b * th * w) / bw;
+                    num = cg * (gk - omd * zk) + (gk1 - gk) * psi;
+                }
+                const float p = (float)(num / (double)el);
+                a.score[q0 + i] = p;
+                const float pp = p > 0.0f ? p : 0.0f;
+                key[j] = (1ull << 63) | ((unsigned long long)__float_as_uint(pp) << 32) |
+                         (unsigned long long)(0xffffffffu - (unsigned)i);
+            }
+        }
+    }
+    // the s-th largest key by bisection over [0, 2^64)
+    unsigned long long lo_k = 0ull, hi_k = ~0ull;   // invariant: count(key >= lo_k) >= s
+    for (int it = 0; it < 64 && lo_k < hi_k; ++it) {
+        const unsigned long long mid = lo_k + (hi_k - lo_k) / 2 + 1;
+        int cnt = 0;
+#pragma unroll
+        for (int j = 0; j < kPer; ++j) cnt += key[j] >= mid;
+        for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+        if (lane == 0) s_part[wv] = (unsigned long long)cnt;
+        __syncthreads();
+        unsigned long long tot = 0;
+        for (int i = 0; i < kWaves; ++i) tot += s_part[i];
+        __syncthreads();
+        if (tot >= (unsigned long long)s) lo_k = mid; else hi_k = mid - 1;
+    }
+    // the selected keys, then each one's rank among them
+#pragma unroll
+    for (int j = 0; j < kPer; ++j)
+        if (key[j] >= lo_k && key[j] != 0ull) {
+            const int slot = atomicAdd(&s_nsel, 1);
+            if (slot < kIterMaxBatch) s_sel[slot] = key[j];
+        }
+    __syncthreads();
+    const int nsel = min(s_nsel, min(s, kIterMaxBatch));
+    for (int j = tid; j < nsel; j += kThreads) {
+        const unsigned long long kj = s_sel[j];
+        int rank = 0;
+        for (int i = 0; i < nsel; ++i) rank += s_sel[i] > kj;
+        bq[rank] = (int32_t)(0xffffffffu - (unsigned)(kj & 0xffffffffull));
+    }
+    for (int j = nsel + tid; j < a.bs_max; j += kThreads) bq[j] = -1;
+}
+
+}  // namespace
+
 struct orloj_ctx {
     int device;
     hipStream_t stream;
@@ -1061,13 +1390,14 @@ int orloj_sync(orloj_ctx* ctx) {
     if (flags) {
         e = hipMemset(ctx->d_err, 0, sizeof(int));
         if (e != hipSuccess) return hip_fail(ctx, e, "clearing the device status word");
-        return fail(ctx, ORLOJ_E_DATA, "device data error:%s%s%s%s%s%s",
+        return fail(ctx, ORLOJ_E_DATA, "device data error:%s%s%s%s%s%s%s",
                     (flags & kErrEmptyHistogram) ? " histogram-with-no-samples" : "",
                     (flags & kErrClassRange) ? " class-id-out-of-range" : "",
                     (flags & kErrDeadlineNaN) ? " NaN-deadline" : "",
                     (flags & kErrUnsorted) ? " deadlines-not-sorted" : "",
                     (flags & kErrNowNaN) ? " NaN-now" : "",
-                    (flags & kErrWidth) ? " bin-width-not-positive" : "");
+                    (flags & kErrWidth) ? " bin-width-not-positive" : "",
+                    (flags & kErrWeights) ? " class-weights-invalid" : "");
     }
     return ORLOJ_OK;
 }
@@ -1208,6 +1538,107 @@ int orloj_score_candidates(orloj_ctx* ctx, const orloj_grid* grid, const float* 
         default: e = launch_score<16>(a, g, ctx->stream); break;
     }
     if (e != hipSuccess) return hip_fail(ctx, e, "score_kernel launch");
+    return ORLOJ_OK;
+}
+
+int orloj_build_model_laws(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
+                           const double* d_class_weights, double b_expo_per_ms, float* d_law,
+                           float* d_disc, float* d_model_el) {
+    if (!ctx) return ORLOJ_E_INVALID;
+    int rc = check_grid(ctx, grid);
+    if (rc) return rc;
+    if (!(b_expo_per_ms > 0.0) || !isfinite(b_expo_per_ms))
+        return fail(ctx, ORLOJ_E_INVALID, "b_expo_per_ms must be finite and > 0");
+    if (grid->n_models == 0) return ORLOJ_OK;
+    if (!d_ccdf || !d_law || !d_disc || !d_model_el)
+        return fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
+    const int64_t nblk = (int64_t)grid->n_models * grid->n_bs;
+    if (nblk > 0x7fffffff) return fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (model, batch size) pairs");
+    LawArgs a;
+    a.tab = d_ccdf;
+    a.weights = d_class_weights;
+    a.width = grid->d_bin_width_ms;
+    a.law = d_law;
+    a.disc = d_disc;
+    a.model_el = d_model_el;
+    a.err = ctx->d_err;
+    a.b = b_expo_per_ms;
+    a.M = grid->n_models;
+    a.C = grid->n_classes;
+    a.K = grid->n_bins;
+    a.nbs = grid->n_bs;
+    memset(a.bs, 0, sizeof a.bs);
+    for (int i = 0; i < grid->n_bs; ++i) a.bs[i] = grid->batch_sizes[i];
+    hipError_t e = hipSetDevice(ctx->device);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    const unsigned g = (unsigned)nblk;
+    switch (chunk_per_lane(grid->n_bins)) {
+        case 1: hipLaunchKernelGGL(laws_kernel<1>, dim3(g), dim3(kThreads), 0, ctx->stream, a); break;
+        case 2: hipLaunchKernelGGL(laws_kernel<2>, dim3(g), dim3(kThreads), 0, ctx->stream, a); break;
+        case 4: hipLaunchKernelGGL(laws_kernel<4>, dim3(g), dim3(kThreads), 0, ctx->stream, a); break;
+        case 8: hipLaunchKernelGGL(laws_kernel<8>, dim3(g), dim3(kThreads), 0, ctx->stream, a); break;
+        case 16: hipLaunchKernelGGL(laws_kernel<16>, dim3(g), dim3(kThreads), 0, ctx->stream, a); break;
+        default: hipLaunchKernelGGL(laws_kernel<32>, dim3(g), dim3(kThreads), 0, ctx->stream, a); break;
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(ctx, e, "laws_kernel launch");
+    return ORLOJ_OK;
+}
+
+int orloj_iterate(orloj_ctx* ctx, const orloj_grid* grid, const int32_t* d_support,
+                  const float* d_law, const float* d_disc, const float* d_model_el,
+                  const orloj_queues* queues, double b_expo_per_ms, int32_t* d_timed_out,
+                  float* d_score, int32_t* d_cand_bs, int32_t* d_batch) {
+    if (!ctx) return ORLOJ_E_INVALID;
+    int rc = check_grid(ctx, grid);
+    if (rc) return rc;
+    rc = check_queues(ctx, grid, queues);
+    if (rc) return rc;
+    if (!(b_expo_per_ms > 0.0) || !isfinite(b_expo_per_ms))
+        return fail(ctx, ORLOJ_E_INVALID, "b_expo_per_ms must be finite and > 0");
+    const int M = grid->n_models;
+    if (M == 0) return ORLOJ_OK;
+    const int bs_max = grid->batch_sizes[grid->n_bs - 1];
+    if (bs_max > kIterMaxBatch)
+        return fail(ctx, ORLOJ_E_UNSUPPORTED, "batch size %d > %d", bs_max, kIterMaxBatch);
+    for (int q = 0; q < M; ++q) {
+        const int64_t N = queues->h_queue_off[q + 1] - queues->h_queue_off[q];
+        if (N > kIterMaxQueue)
+            return fail(ctx, ORLOJ_E_UNSUPPORTED, "queue of model %d holds %lld > %d requests", q,
+                        (long long)N, kIterMaxQueue);
+    }
+    if (!d_support || !d_law || !d_disc || !d_model_el || !d_cand_bs || !d_batch)
+        return fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
+    if (queues->h_queue_off[M] > 0 && (!d_timed_out || !d_score))
+        return fail(ctx, ORLOJ_E_INVALID, "NULL per-request output");
+    IterArgs a;
+    a.sup = d_support;
+    a.law = d_law;
+    a.disc = d_disc;
+    a.model_el = d_model_el;
+    a.queue_off = queues->d_queue_off;
+    a.cls = queues->d_class;
+    a.deadline = queues->d_deadline_ms;
+    a.now = queues->d_now_ms;
+    a.width = grid->d_bin_width_ms;
+    a.timed_out = d_timed_out;
+    a.score = d_score;
+    a.cand_bs = d_cand_bs;
+    a.batch = d_batch;
+    a.err = ctx->d_err;
+    a.b = b_expo_per_ms;
+    a.M = M;
+    a.C = grid->n_classes;
+    a.K = grid->n_bins;
+    a.nbs = grid->n_bs;
+    a.bs_max = bs_max;
+    memset(a.bs, 0, sizeof a.bs);
+    for (int i = 0; i < grid->n_bs; ++i) a.bs[i] = grid->batch_sizes[i];
+    hipError_t e = hipSetDevice(ctx->device);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    hipLaunchKernelGGL(iterate_kernel, dim3(M), dim3(kThreads), 0, ctx->stream, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(ctx, e, "iterate_kernel launch");
     return ORLOJ_OK;
 }
 

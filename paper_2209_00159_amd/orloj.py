@@ -52,7 +52,7 @@ _I64P = ctypes.POINTER(ctypes.c_int64)
 
 EXPORTS = ("orloj_create", "orloj_destroy", "orloj_set_stream", "orloj_last_error", "orloj_sync",
            "orloj_build_cdfs", "orloj_output_sizes", "orloj_score_candidates",
-           "orloj_select_batch")
+           "orloj_select_batch", "orloj_build_model_laws", "orloj_iterate")
 
 
 def load(path: Optional[str] = None):
@@ -85,6 +85,11 @@ def load(path: Optional[str] = None):
     L.orloj_score_candidates.restype = ctypes.c_int
     L.orloj_select_batch.argtypes = [_VP, _GP, _QP, ctypes.c_int32, _VP, _VP, _VP, _VP, _VP]
     L.orloj_select_batch.restype = ctypes.c_int
+    L.orloj_build_model_laws.argtypes = [_VP, _GP, _VP, _VP, ctypes.c_double, _VP, _VP, _VP]
+    L.orloj_build_model_laws.restype = ctypes.c_int
+    L.orloj_iterate.argtypes = [_VP, _GP, _VP, _VP, _VP, _VP, _QP, ctypes.c_double, _VP, _VP,
+                                _VP, _VP]
+    L.orloj_iterate.restype = ctypes.c_int
     if default:
         _LIB = L
     return L
@@ -277,3 +282,74 @@ class Scorer:
             score=self.score_out[:self.n_cands].cpu().numpy(),
             sel_n=self.sel_n.cpu().numpy(), sel_bs=self.sel_bs.cpu().numpy(),
             sel_score=self.sel_score.cpu().numpy())
+
+
+class Iterator:
+    """The scheduler iteration (Algorithm 1 with the paper's own priority)
+    over a workload resident in HBM: builds the CDF tables, their support and
+    the model-wide batch laws once, then runs orloj_iterate on the queues."""
+
+    def __init__(self, wl, ctx: Optional[Context] = None, class_weights=None,
+                 counts_device: Optional[torch.Tensor] = None):
+        self.ctx = ctx or Context()
+        self.wl = wl
+        dev = self.ctx.device
+        self.counts = counts_device if counts_device is not None else \
+            torch.from_numpy(np.ascontiguousarray(wl.counts).view(np.int32)).to(dev)
+        shape = self.counts.shape
+        self.ccdf = torch.empty(shape, dtype=torch.float32, device=dev)
+        self.support = torch.empty(shape[:-1] + (2,), dtype=torch.int32, device=dev)
+        self.law = torch.empty(shape, dtype=torch.float32, device=dev)
+        self.disc = torch.empty(shape, dtype=torch.float32, device=dev)
+        self.model_el = torch.empty(shape[:2], dtype=torch.float32, device=dev)
+        self.weights = None if class_weights is None else \
+            torch.from_numpy(np.ascontiguousarray(class_weights, np.float64)).to(dev)
+        self.width = torch.from_numpy(np.ascontiguousarray(wl.bin_width_ms, np.float64)).to(dev)
+        self.grid = make_grid(wl.n_models, wl.n_classes, wl.n_bins, wl.batch_sizes, self.width)
+        self.bs_max = int(wl.batch_sizes[-1])
+        self.cand_bs = torch.zeros(wl.n_models, dtype=torch.int32, device=dev)
+        self.batch = torch.full((wl.n_models, self.bs_max), -1, dtype=torch.int32, device=dev)
+        self.set_queues(wl.queue_off, wl.cls, wl.deadline_ms, wl.now_ms)
+
+    def set_queues(self, queue_off, cls, deadline_ms, now_ms):
+        dev = self.ctx.device
+        self.h_queue_off = np.ascontiguousarray(queue_off, np.int64)
+        self.d_queue_off = torch.from_numpy(self.h_queue_off).to(dev)
+        self.d_class = torch.from_numpy(np.ascontiguousarray(cls, np.int32)).to(dev)
+        self.d_deadline = torch.from_numpy(np.ascontiguousarray(deadline_ms, np.float64)).to(dev)
+        self.d_now = torch.from_numpy(np.ascontiguousarray(now_ms, np.float64)).to(dev)
+        self.queues = make_queues(self.h_queue_off, self.d_queue_off, self.d_class,
+                                  self.d_deadline, self.d_now)
+        n = int(self.h_queue_off[-1])
+        self.timed_out = torch.zeros(max(n, 1), dtype=torch.int32, device=dev)
+        self.score = torch.zeros(max(n, 1), dtype=torch.float32, device=dev)
+
+    def build(self, b_expo: Optional[float] = None):
+        b = self.wl.b_expo if b_expo is None else b_expo
+        self.b = float(b)
+        self.ctx.build_cdfs(self.counts, self.ccdf, self.support)
+        c = self.ctx
+        c._check(c.L.orloj_build_model_laws(
+            c.ctx, ctypes.byref(self.grid), _ptr(self.ccdf), _ptr(self.weights), self.b,
+            _ptr(self.law), _ptr(self.disc), _ptr(self.model_el)))
+
+    def iterate(self):
+        c = self.ctx
+        c._check(c.L.orloj_iterate(
+            c.ctx, ctypes.byref(self.grid), _ptr(self.support), _ptr(self.law), _ptr(self.disc),
+            _ptr(self.model_el), ctypes.byref(self.queues), self.b, _ptr(self.timed_out),
+            _ptr(self.score), _ptr(self.cand_bs), _ptr(self.batch)))
+
+    def run(self, build: bool = True, b_expo: Optional[float] = None) -> dict:
+        if build:
+            self.build(b_expo)
+        self.iterate()
+        self.ctx.sync()
+        return self.fetch()
+
+    def fetch(self) -> dict:
+        torch.cuda.synchronize(self.ctx.device)
+        n = int(self.h_queue_off[-1])
+        return dict(timed_out=self.timed_out[:n].cpu().numpy(), score=self.score[:n].cpu().numpy(),
+                    cand_bs=self.cand_bs.cpu().numpy(), batch=self.batch.cpu().numpy(),
+                    model_el=self.model_el.cpu().numpy())

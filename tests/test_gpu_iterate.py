@@ -1,0 +1,145 @@
+"""The scheduler iteration (Algorithm 1 with the paper's own priority)
+through the C ABI against the oracle: timed-out flags and candidate batch
+sizes bit-exact, priorities within the score bar, and the popped batch a
+valid top-s under the oracle's priorities (ties within the bar aside)."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2209_00159_amd import orloj as O
+from paper_2209_00159_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+TOL_ABS, TOL_REL = 1e-6, 1e-5
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    return O.Context()
+
+
+def check(wl, got, ora):
+    err = 0.0
+    for q in range(wl.n_models):
+        a, b = int(wl.queue_off[q]), int(wl.queue_off[q + 1])
+        o = ora["per_model"][q]
+        assert np.array_equal(got["timed_out"][a:b], o["timed_out"]), q
+        assert int(got["cand_bs"][q]) == o["cand_bs"], (q, got["cand_bs"][q], o["cand_bs"])
+        gs = got["score"][a:b].astype(np.float64)
+        os_ = o["score"]
+        d = np.abs(gs - os_)
+        assert np.all(d <= TOL_ABS + TOL_REL * np.abs(os_)), (q, float(d.max()))
+        err = max(err, float(d.max(initial=0.0)))
+        s = o["cand_bs"]
+        gb = got["batch"][q]
+        if s == 0:
+            assert np.all(gb == -1), q
+            continue
+        assert np.all(gb[s:] == -1) and np.all(gb[:s] >= 0), q
+        sel = gb[:s]
+        assert len(set(sel.tolist())) == s
+        # ordered by the GPU's own priorities, earlier position first on ties
+        g_sel = gs[sel]
+        assert np.all((g_sel[:-1] > g_sel[1:]) | ((g_sel[:-1] == g_sel[1:]) & (sel[:-1] < sel[1:]))), q
+        # a top-s set under the oracle's priorities, up to the bar
+        kept = np.nonzero(os_ > 0)[0] if np.any(os_ > 0) else np.array([], int)
+        thr = np.sort(os_[o["batch"]])[0]
+        tol = TOL_ABS + TOL_REL * abs(thr)
+        assert np.all(os_[sel] >= thr - tol), q
+        rest = np.setdiff1d(np.arange(b - a), sel)
+        in_q = rest[np.isin(rest, kept)]
+        assert np.all(os_[in_q] <= thr + tol), q
+    return err
+
+
+def run(wl, ctx, weights=None, b_expo=None):
+    it = O.Iterator(wl, ctx, class_weights=weights)
+    got = it.run(b_expo=b_expo)
+    ora = oracle.iterate_workload(wl if b_expo is None else _with_b(wl, b_expo), weights=weights)
+    return got, ora
+
+
+def _with_b(wl, b):
+    import dataclasses
+    return dataclasses.replace(wl, b_expo=b)
+
+
+CASES = [
+    dict(seed=0),
+    dict(seed=1, n_models=3, queue_lens=[0, 7, 13], batch_sizes=(1, 4, 16)),
+    dict(seed=2, n_bins=1, batch_sizes=(1, 2)),
+    dict(seed=3, n_bins=2, n_classes=1),
+    dict(seed=4, n_bins=255, batch_sizes=(2, 3, 5, 7, 11, 13)),
+    dict(seed=5, n_bins=257, queue_lens=[40, 1], batch_sizes=(1, 8, 32, 64)),
+    dict(seed=6, n_bins=1023, n_classes=7, queue_lens=[65, 64], batch_sizes=(1, 63, 64, 65)),
+    dict(seed=7, n_models=1, n_bins=4096, n_classes=5, queue_lens=[300], batch_sizes=(16, 64)),
+    dict(seed=9, n_models=5, queue_lens=[0, 0, 0, 0, 0]),
+    dict(seed=10, n_models=1, n_bins=100, queue_lens=[4096], batch_sizes=(128, 256, 1024)),
+    dict(seed=11, n_bins=64, tau_range=(-50.0, -1.0)),
+    dict(seed=12, n_bins=64, tau_range=(500.0, 900.0)),
+    dict(seed=13, n_bins=300, sparsity=0.9, total=3),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: f"seed{c['seed']}")
+def test_iterate_random_cases(ctx, case):
+    say("iterate", case)
+    wl = W.random_case(**case)
+    got, ora = run(wl, ctx)
+    say("  max |d score|", check(wl, got, ora))
+
+
+@pytest.mark.parametrize("seed", [20, 21])
+def test_iterate_class_weights(ctx, seed):
+    wl = W.random_case(seed, n_models=3, queue_lens=[30, 12, 50], n_classes=5, n_bins=200,
+                       batch_sizes=(1, 2, 4, 8, 16))
+    r = np.random.default_rng(seed)
+    weights = r.random((3, 5))
+    weights[1, 2:] = 0.0
+    got, ora = run(wl, ctx, weights=weights)
+    check(wl, got, ora)
+
+
+@pytest.mark.parametrize("b", [1e-6, 1e-2, 1e-1])
+def test_iterate_delay_rate(ctx, b):
+    wl = W.random_case(30, n_models=2, queue_lens=[40, 25], batch_sizes=(1, 2, 4, 8, 16, 32),
+                       n_bins=512, tau_range=(0.0, 700.0))
+    got, ora = run(wl, ctx, b_expo=b)
+    check(wl, got, ora)
+
+
+@pytest.mark.parametrize("cid,scale", [(1, 1.0), (1, 4.0), (2, 1.0), (2, 3.0), (3, 1.0), (4, 1.0),
+                                       (4, 3.0)])
+def test_iterate_configs(ctx, cid, scale):
+    say(f"iterate config {cid} slo x{scale}")
+    wl = W.make(cid, workers=8, slo_scale=scale)
+    got, ora = run(wl, ctx)
+    say("  candidates", np.unique(got["cand_bs"]), "max |d score|", check(wl, got, ora))
+
+
+def test_iterate_bad_weights_are_a_data_error(ctx):
+    wl = W.random_case(40, n_models=2, queue_lens=[6, 3], n_classes=3)
+    weights = np.ones((2, 3))
+    weights[1] = 0.0
+    it = O.Iterator(wl, ctx, class_weights=weights)
+    it.build()
+    with pytest.raises(O.OrlojError) as ei:
+        ctx.sync()
+    assert ei.value.code == O.ORLOJ_E_DATA
+
+
+def test_iterate_queue_limit_is_unsupported(ctx):
+    wl = W.random_case(41, n_models=1, queue_lens=[4097], batch_sizes=(1, 8))
+    it = O.Iterator(wl, ctx)
+    it.build()
+    with pytest.raises(O.OrlojError) as ei:
+        it.iterate()
+    assert ei.value.code == O.ORLOJ_E_UNSUPPORTED
