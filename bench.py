@@ -157,6 +157,8 @@ def main():
     ap.add_argument("--trace-arrivals", type=int, default=20_000,
                     help="arrivals of the configuration-5 trace replayed by the scheduling "
                          "loop after the timed steps (0 = skip)")
+    ap.add_argument("--no-iterate", action="store_true",
+                    help="skip timing the Algorithm 1 iteration (orloj_iterate) on the same state")
     ap.add_argument("--no-trim", action="store_true",
                     help="score without the table support (every table entry is read)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -257,6 +259,41 @@ def main():
         torch.cuda.synchronize()
         line["calibration_copy_bytes"] = src.numel() * 4
         del src, dst
+    if not args.no_iterate:
+        it = O.Iterator(wl, ctx, counts_device=sc.counts)
+        torch.cuda.synchronize()
+        l0, l1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        it.build()
+        ctx.sync()
+        l0.record()
+        it.build()
+        l1.record()
+        ctx.sync()
+        laws_ms = l0.elapsed_time(l1)
+        for _ in range(args.warmup):
+            it.iterate()
+        ctx.sync()
+        iev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        for e0, e1 in iev:
+            e0.record()
+            it.iterate()
+            e1.record()
+        ctx.sync()
+        it_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in iev]))
+        res = it.fetch()
+        n_batches = int((res["cand_bs"] > 0).sum())
+        line["iterate"] = dict(
+            what="orloj_iterate: one Algorithm 1 iteration (drop phase, candidate batch size, "
+                 "priority of every kept request, PopBatch) for every model, one launch",
+            ms_per_iteration=round(it_ms, 5), models_with_batch=n_batches,
+            decisions_per_s=round(n_batches / (it_ms * 1e-3), 1),
+            requests=int(wl.queue_off[-1]),
+            build_tables_ms=round(laws_ms, 4),
+            build_tables_note="orloj_build_cdfs + orloj_build_model_laws, off the scheduling path")
+        print(f"[bench] iterate: {it_ms:.4f} ms per iteration, tables {laws_ms:.2f} ms",
+              file=sys.stderr, flush=True)
+        del it
     recorded = []
     if args.trace_arrivals and args.config == 5:
         from paper_2209_00159_amd import schedsim
