@@ -21,6 +21,7 @@ _LIB = None
 _I32P = ctypes.POINTER(ctypes.c_int32)
 _U32P = ctypes.POINTER(ctypes.c_uint32)
 _F64P = ctypes.POINTER(ctypes.c_double)
+_I64P = ctypes.POINTER(ctypes.c_int64)
 
 
 def lib(path: Optional[str] = None):
@@ -43,13 +44,17 @@ def _bind(L):
     L.orloj_oracle_batch_cdf.restype = ctypes.c_int
     L.orloj_oracle_score_model.argtypes = [
         ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _I32P, ctypes.c_double,
-        _U32P, ctypes.c_int64, _I32P, _F64P, ctypes.c_double, ctypes.c_double,
+        _U32P, ctypes.c_int64, _I32P, _F64P, _F64P, ctypes.c_double, ctypes.c_double,
         ctypes.c_int32, _F64P, _F64P, _F64P, _F64P, _F64P, _I32P, _I32P, _F64P]
     L.orloj_oracle_score_model.restype = ctypes.c_int
     L.orloj_oracle_iterate_model.argtypes = [
         ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _I32P, ctypes.c_double, _U32P, _F64P,
-        ctypes.c_int64, _I32P, _F64P, ctypes.c_double, ctypes.c_double, _I32P, _F64P, _I32P,
-        _I32P, _I32P]
+        ctypes.c_int64, _I32P, _F64P, _F64P, _I64P, _F64P, _F64P, ctypes.c_double,
+        ctypes.c_double, _I32P, _F64P, _I32P, _I32P, _I32P]
+    L.orloj_oracle_accumulate.argtypes = [
+        ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _F64P, ctypes.c_int64,
+        _I32P, _I32P, _I32P, _F64P, _U32P, _I64P]
+    L.orloj_oracle_accumulate.restype = ctypes.c_int
     L.orloj_oracle_iterate_model.restype = ctypes.c_int
     return L
 
@@ -104,8 +109,12 @@ def output_sizes(queue_off, batch_sizes, prefix_mode: int = 0):
     return cand_off, prob_off
 
 
+def _opt64(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.float64)
+
+
 def score_model(counts, batch_sizes, bin_width_ms, cls, deadline_ms, now_ms, b_expo,
-                prefix_mode: int = 0, want_priority: bool = False, L=None) -> dict:
+                prefix_mode: int = 0, want_priority: bool = False, L=None, cost=None) -> dict:
     """All candidates of one model (see orloj_oracle_score_model)."""
     L = L or lib()
     cnt = np.ascontiguousarray(counts, dtype=np.uint32)
@@ -124,9 +133,11 @@ def score_model(counts, batch_sizes, bin_width_ms, cls, deadline_ms, now_ms, b_e
     sn = np.zeros(1, np.int32)
     sb = np.zeros(1, np.int32)
     ss = np.zeros(1)
+    co = _opt64(cost)
     rc = L.orloj_oracle_score_model(
         C, K, B, _p(bs, _I32P), float(bin_width_ms), _p(cnt, _U32P), cl.size,
-        _p(cl, _I32P), _p(dl, _F64P), float(now_ms), float(b_expo), int(prefix_mode),
+        _p(cl, _I32P), _p(dl, _F64P), _p(co, _F64P) if co is not None else None,
+        float(now_ms), float(b_expo), int(prefix_mode),
         _p(P, _F64P), _p(pr, _F64P) if pr is not None else None, _p(E, _F64P),
         _p(EL, _F64P), _p(S, _F64P), _p(sn, _I32P), _p(sb, _I32P), _p(ss, _F64P))
     if rc:
@@ -161,7 +172,8 @@ def score_workload(wl, prefix_mode: int = 0, models: Optional[Sequence[int]] = N
 
 
 def iterate_model(counts, batch_sizes, bin_width_ms, cls, deadline_ms, now_ms, b_expo,
-                  weights=None, L=None) -> dict:
+                  weights=None, L=None, cost=None, steps=None) -> dict:
+    """steps = (step_off [N+1], step_deadline_ms [S], step_cost [S]) or None."""
     """One Algorithm 1 iteration of one model (see orloj_oracle_iterate_model)."""
     L = L or lib()
     cnt = np.ascontiguousarray(counts, dtype=np.uint32)
@@ -176,9 +188,18 @@ def iterate_model(counts, batch_sizes, bin_width_ms, cls, deadline_ms, now_ms, b
     batch = np.full(max(int(bs[-1]), 1), -1, np.int32)
     cand = np.zeros(1, np.int32)
     bn = np.zeros(1, np.int32)
+    co = _opt64(cost)
+    if steps is not None:
+        so = np.ascontiguousarray(steps[0], dtype=np.int64)
+        sd = np.ascontiguousarray(steps[1], dtype=np.float64)
+        sc = np.ascontiguousarray(steps[2], dtype=np.float64)
     rc = L.orloj_oracle_iterate_model(
         C, K, B, _p(bs, _I32P), float(bin_width_ms), _p(cnt, _U32P),
         _p(wt, _F64P) if wt is not None else None, N, _p(cl, _I32P), _p(dl, _F64P),
+        _p(co, _F64P) if co is not None else None,
+        _p(so, _I64P) if steps is not None else None,
+        _p(sd, _F64P) if steps is not None else None,
+        _p(sc, _F64P) if steps is not None else None,
         float(now_ms), float(b_expo), _p(timed_out, _I32P), _p(score, _F64P), _p(cand, _I32P),
         _p(batch, _I32P), _p(bn, _I32P))
     if rc:
@@ -201,3 +222,24 @@ def iterate_workload(wl, weights=None, models: Optional[Sequence[int]] = None, L
     return dict(timed_out=cat("timed_out").astype(np.int32), score=cat("score"),
                 cand_bs=np.array([p["cand_bs"] for p in parts], np.int32),
                 batch=[p["batch"] for p in parts], per_model=parts)
+
+
+def accumulate(counts, bin_width_ms, model, bs_index, cls, latency_ms, L=None) -> int:
+    """Add the samples to counts ([M][B][C][K] uint32, in place); returns the
+    number of rejected samples (see orloj_oracle_accumulate)."""
+    L = L or lib()
+    if not (isinstance(counts, np.ndarray) and counts.dtype == np.uint32 and
+            counts.flags.c_contiguous):
+        raise TypeError("counts must be a C-contiguous uint32 array")
+    M, B, C, K = counts.shape
+    w = np.ascontiguousarray(bin_width_ms, dtype=np.float64)
+    mo = np.ascontiguousarray(model, dtype=np.int32)
+    bi = np.ascontiguousarray(bs_index, dtype=np.int32)
+    cl = np.ascontiguousarray(cls, dtype=np.int32)
+    la = np.ascontiguousarray(latency_ms, dtype=np.float64)
+    rej = np.zeros(1, np.int64)
+    rc = L.orloj_oracle_accumulate(M, B, C, K, _p(w, _F64P), la.size, _p(mo, _I32P), _p(bi, _I32P),
+                                   _p(cl, _I32P), _p(la, _F64P), _p(counts, _U32P), _p(rej, _I64P))
+    if rc:
+        raise OracleError(f"orloj_oracle_accumulate rc={rc}")
+    return int(rej[0])

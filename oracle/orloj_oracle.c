@@ -46,7 +46,8 @@
  *     a deadline at or beyond K*w finishes with probability 1, one at or
  *     before now with probability 0;
  *   - inside a bin the batch CDF is linear (uniform mass per bin);
- *   - the cost of a miss is c = 1;
+ *   - the cost of a miss is c = 1 unless per-request costs are given (the
+ *     score then sums c_m p_m; finish probabilities are unweighted);
  *   - selection: the largest score; exact ties go to the larger prefix,
  *     then the smaller batch size; no batch when the best score is <= 0.
  */
@@ -150,8 +151,9 @@ static double priority_times_latency(const double *mass, int32_t n_bins, double 
 int orloj_oracle_score_model(int32_t n_classes, int32_t n_bins, int32_t n_bs,
                              const int32_t *batch_sizes, double bin_width_ms,
                              const uint32_t *counts, int64_t n_queue, const int32_t *cls,
-                             const double *deadline_ms, double now_ms, double b_expo,
-                             int32_t prefix_mode, double *finish_prob, double *priority,
+                             const double *deadline_ms, const double *cost, double now_ms,
+                             double b_expo, int32_t prefix_mode, double *finish_prob,
+                             double *priority,
                              double *expected_finish, double *expected_latency_ms,
                              double *score, int32_t *sel_n, int32_t *sel_bs,
                              double *sel_score)
@@ -171,6 +173,8 @@ int orloj_oracle_score_model(int32_t n_classes, int32_t n_bins, int32_t n_bs,
         if (cls[i] < 0 || cls[i] >= C || isnan(deadline_ms[i]))
             return ORACLE_E_DATA;
         if (i > 0 && deadline_ms[i] < deadline_ms[i - 1])
+            return ORACLE_E_DATA;
+        if (cost && !(cost[i] >= 0.0 && cost[i] < INFINITY))
             return ORACLE_E_DATA;
     }
 
@@ -226,7 +230,7 @@ int orloj_oracle_score_model(int32_t n_classes, int32_t n_bins, int32_t n_bs,
                     priority[slot] = p;
                 ++slot;
                 e_count += P;                                        /* step 6 */
-                s += p;
+                s += (cost ? cost[m - 1] : 1.0) * p;                 /* miss cost c */
             }
             expected_finish[cand] = e_count;
             expected_latency_ms[cand] = el;
@@ -278,6 +282,16 @@ int orloj_oracle_score_model(int32_t n_classes, int32_t n_bins, int32_t n_bs,
  *     latency, of F_mix,s^s (§4.3: all of the model's distributions).
  *   - PopBatch returns the s requests of Q_s with the largest priority at
  *     batch size s; equal priorities go to the earlier queue position.
+ *   - Costs (§4.1: the cost c of a miss; App. B: piecewise-step costs).  A
+ *     request's cost function is c_r (default 1) times either one step at
+ *     its deadline, or, with step_off given, the steps
+ *     (step_deadline_ms[j], step_cost[j]) for j in [step_off[r],
+ *     step_off[r+1]): deadlines increasing, cumulative costs non-decreasing.
+ *     App. B: such a function is the sum of single steps at d_j with costs
+ *     c_j - c_{j-1}, so its priority is the matching sum of single-step
+ *     priorities.  The drop phase uses the request's last step deadline (a
+ *     request still has cost to save until then); the queue order and
+ *     D_{Q_s} use deadline_ms.
  *
  * counts is [n_bs][n_classes][n_bins]; weights (n_classes, may be NULL) are
  * the class mix; the queue is sorted by deadline.  Outputs:
@@ -292,6 +306,8 @@ int orloj_oracle_iterate_model(int32_t n_classes, int32_t n_bins, int32_t n_bs,
                                const int32_t *batch_sizes, double bin_width_ms,
                                const uint32_t *counts, const double *weights,
                                int64_t n_queue, const int32_t *cls, const double *deadline_ms,
+                               const double *cost, const int64_t *step_off,
+                               const double *step_deadline_ms, const double *step_cost,
                                double now_ms, double b_expo, int32_t *timed_out,
                                double *score, int32_t *cand_bs, int32_t *batch,
                                int32_t *batch_n)
@@ -311,7 +327,22 @@ int orloj_oracle_iterate_model(int32_t n_classes, int32_t n_bins, int32_t n_bs,
             return ORACLE_E_DATA;
         if (i > 0 && deadline_ms[i] < deadline_ms[i - 1])
             return ORACLE_E_DATA;
+        if (cost && !(cost[i] >= 0.0 && cost[i] < INFINITY))
+            return ORACLE_E_DATA;
+        if (step_off) {
+            if (step_off[i + 1] <= step_off[i] || (i == 0 && step_off[0] != 0))
+                return ORACLE_E_DATA;
+            for (int64_t j = step_off[i]; j < step_off[i + 1]; ++j) {
+                if (isnan(step_deadline_ms[j]) || !(step_cost[j] >= 0.0 && step_cost[j] < INFINITY))
+                    return ORACLE_E_DATA;
+                if (j > step_off[i] && (step_deadline_ms[j] <= step_deadline_ms[j - 1] ||
+                                        step_cost[j] < step_cost[j - 1]))
+                    return ORACLE_E_DATA;
+            }
+        }
     }
+    if (step_off && (!step_deadline_ms || !step_cost))
+        return ORACLE_E_INVALID;
     double wsum = 0.0;
     if (weights) {
         for (int32_t c = 0; c < C; ++c) {
@@ -351,7 +382,8 @@ int orloj_oracle_iterate_model(int32_t n_classes, int32_t n_bins, int32_t n_bs,
         first[bi] = -1;
     }
     for (int64_t r = 0; r < n_queue && rc == ORACLE_OK; ++r) {
-        double tau = deadline_ms[r] - now_ms;
+        double last = step_off ? step_deadline_ms[step_off[r + 1] - 1] : deadline_ms[r];
+        double tau = last - now_ms;
         int any = 0;
         for (int32_t bi = 0; bi < n_bs; ++bi) {
             const double *Fr = F + ((size_t)bi * (size_t)C + (size_t)cls[r]) * row;
@@ -398,15 +430,26 @@ int orloj_oracle_iterate_model(int32_t n_classes, int32_t n_bins, int32_t n_bs,
         /* Priority of every request in Q_s, from its own batch law. */
         int64_t nq = 0;
         for (int64_t r = 0; r < n_queue; ++r) {
-            double tau = deadline_ms[r] - now_ms;
+            double last = step_off ? step_deadline_ms[step_off[r + 1] - 1] : deadline_ms[r];
             const double *Fr = F + ((size_t)cand * (size_t)C + (size_t)cls[r]) * row;
-            if (!(finish_probability(Fr, K, w, tau) > 0.0))
+            if (!(finish_probability(Fr, K, w, last - now_ms) > 0.0))
                 continue;
             for (int32_t k = 0; k <= K; ++k)
                 G[k] = Fr[k] * pow(mix[k], s - 1);
             for (int32_t k = 0; k < K; ++k)
                 dG[k] = G[k + 1] - G[k];
-            score[r] = priority_times_latency(dG, K, w, tau, b) / el_model;
+            double cr = cost ? cost[r] : 1.0, pr = 0.0;
+            if (step_off) {
+                double below = 0.0;             /* App. B: one single step per cost increment */
+                for (int64_t j = step_off[r]; j < step_off[r + 1]; ++j) {
+                    double tau_j = step_deadline_ms[j] - now_ms;
+                    pr += (step_cost[j] - below) * priority_times_latency(dG, K, w, tau_j, b);
+                    below = step_cost[j];
+                }
+            } else {
+                pr = priority_times_latency(dG, K, w, deadline_ms[r] - now_ms, b);
+            }
+            score[r] = cr * pr / el_model;
             order[nq++] = r;
         }
         /* PopBatch: the s best by priority, ties to the earlier position
@@ -428,4 +471,43 @@ int orloj_oracle_iterate_model(int32_t n_classes, int32_t n_bins, int32_t n_bs,
     }
     free(F); free(mix); free(G); free(dG); free(in_q); free(first); free(order);
     return rc;
+}
+
+/*
+ * Profiler feedback (§3.2 "Long-Term Feedback Loop"): execution times of
+ * sampled finished requests, measured alone, are accumulated into the
+ * histograms the scheduler reads.  counts is [M][n_bs][C][K] (updated in
+ * place); sample i adds one count to model model[i], batch-size index
+ * bs_index[i], class cls[i], bin floor(latency_ms[i] / w_q), a latency at
+ * or beyond the grid counting in the last bin (the grid's convention).
+ * Samples with an index out of range or a latency that is negative or not
+ * finite are skipped and counted in *n_rejected.  Resetting the profiling
+ * memory at the end of a window is the caller zeroing counts.
+ */
+int orloj_oracle_accumulate(int32_t n_models, int32_t n_bs, int32_t n_classes, int32_t n_bins,
+                            const double *bin_width_ms, int64_t n_samples, const int32_t *model,
+                            const int32_t *bs_index, const int32_t *cls,
+                            const double *latency_ms, uint32_t *counts, int64_t *n_rejected)
+{
+    if (n_models < 0 || n_bs < 1 || n_classes < 1 || n_bins < 1 || n_samples < 0 || !n_rejected)
+        return ORACLE_E_INVALID;
+    if (n_samples > 0 && (!bin_width_ms || !model || !bs_index || !cls || !latency_ms || !counts))
+        return ORACLE_E_INVALID;
+    int64_t rejected = 0;
+    for (int64_t i = 0; i < n_samples; ++i) {
+        int32_t q = model[i], b = bs_index[i], c = cls[i];
+        double lat = latency_ms[i];
+        if (q < 0 || q >= n_models || b < 0 || b >= n_bs || c < 0 || c >= n_classes ||
+            !(lat >= 0.0 && lat < INFINITY) || !(bin_width_ms[q] > 0.0)) {
+            ++rejected;
+            continue;
+        }
+        double u = floor(lat / bin_width_ms[q]);
+        int32_t k = u >= (double)(n_bins - 1) ? n_bins - 1 : (int32_t)u;
+        size_t at = (((size_t)q * (size_t)n_bs + (size_t)b) * (size_t)n_classes + (size_t)c) *
+                    (size_t)n_bins + (size_t)k;
+        counts[at] += 1u;
+    }
+    *n_rejected = rejected;
+    return ORACLE_OK;
 }

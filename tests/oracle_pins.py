@@ -657,8 +657,128 @@ def pin_iterate_feasibility_and_popbatch(L):
         assert all(sc[it["batch"][i]] >= sc[it["batch"][i + 1]] for i in range(len(it["batch"]) - 1))
 
 
+# ---------------------------------------------------------------- costs and profiler feedback
+def pin_cost_weights(L):
+    """Per-request miss costs (§4.1's c): unit costs change nothing; scaling
+    every cost by lam scales every score by lam and leaves the selection; a
+    member with cost 0 adds nothing; and a Monte Carlo of Eq. (1) with the
+    cost, c P(L <= tau < L + delay) summed over the batch, matches the score
+    times E[L_B]."""
+    r = rng(71)
+    K, C, n = 20, 3, 4
+    rows = r.integers(0, 25, size=(C, K))
+    rows[rows.sum(axis=1) == 0, -1] = 1
+    cls = r.integers(0, C, size=n)
+    w, b = 1.5, 0.08
+    taus = np.sort(r.uniform(5.0, 35.0, size=n))
+    dl = 1000.0 + taus
+    counts = rows[None].repeat(1, axis=0)
+    base = oracle.score_model(counts, [n], w, cls, dl, 1000.0, b, want_priority=True, L=L)
+    unit = oracle.score_model(counts, [n], w, cls, dl, 1000.0, b, L=L, cost=np.ones(n))
+    assert np.array_equal(base["score"], unit["score"])
+    cost = r.uniform(0.2, 3.0, size=n)
+    wgt = oracle.score_model(counts, [n], w, cls, dl, 1000.0, b, L=L, cost=cost)
+    sc2 = oracle.score_model(counts, [n], w, cls, dl, 1000.0, b, L=L, cost=2.5 * cost)
+    assert np.allclose(sc2["score"], 2.5 * wgt["score"], rtol=1e-13, atol=0)
+    assert (sc2["sel_n"], sc2["sel_bs"]) == (wgt["sel_n"], wgt["sel_bs"])
+    zero = cost.copy()
+    zero[1] = 0.0
+    z = oracle.score_model(counts, [n], w, cls, dl, 1000.0, b, L=L, cost=zero)
+    assert z["score"][0] == wgt["score"][0]                         # prefix 1 does not hold member 2
+    # Monte Carlo of the weighted event for the full batch
+    G = exact_cdf_product(rows[cls])
+    mass = np.array([float(G[k + 1] - G[k]) for k in range(K)])
+    S = 1_000_000
+    lat = (r.choice(K, size=S, p=mass / mass.sum()) + r.random(S)) * w
+    delay = r.exponential(1.0 / b, size=S)
+    ev = sum(cost[m] * ((lat <= taus[m]) & (taus[m] < lat + delay)).mean() for m in range(n))
+    got = wgt["score"][n - 1] * wgt["expected_latency_ms"][n - 1]
+    sig = math.sqrt(sum(cost ** 2) * 0.25 / S)
+    assert abs(ev - got) <= 4 * sig, (ev, got, sig)
+
+
+def pin_step_costs(L):
+    """App. B: a piecewise-step cost function is the sum of single steps.
+    A request whose cost rises by c1 at d1 and to c2 at d2 must score
+    c1 p(d1) + (c2 - c1) p(d2), p(d) the score of a single-step request of
+    the same class with deadline d in the same queue; and a Monte Carlo of
+    the cost function itself, E[cost(L + delay) - cost(L)] over the batch
+    law F^s, must match that score times E[L]."""
+    r = rng(72)
+    K = 30
+    row = r.integers(0, 20, size=K)
+    row[:2] = 0
+    row[-1] += 1
+    w, b, s = 1.0, 0.04, 2
+    now = 100.0
+    d1, d2, c1, c2 = now + 12.0, now + 19.0, 0.7, 1.9
+    # queue: the step request (deadline d1) and single-step twins at d1, d2
+    cls = np.zeros(3, np.int32)
+    dl = np.array([d1, d1, d2])
+    steps = (np.array([0, 2, 3, 4]), np.array([d1, d2, d1, d2]), np.array([c1, c2, 1.0, 1.0]))
+    it = oracle.iterate_model(row[None, None, :], [s], w, cls, dl, now, b, L=L, steps=steps)
+    assert it["cand_bs"] == s
+    p1, p2 = it["score"][1], it["score"][2]
+    assert p1 > 0 and p2 > 0
+    assert abs(it["score"][0] - (c1 * p1 + (c2 - c1) * p2)) <= 1e-12 * it["score"][0]
+    # Monte Carlo of the step cost function under the batch law F^s
+    F = np.concatenate([[0.0], np.cumsum(row) / row.sum()])
+    G = F ** s
+    mass = np.diff(G)
+    S = 1_000_000
+    lat = (r.choice(K, size=S, p=mass / mass.sum()) + r.random(S)) * w
+    delay = r.exponential(1.0 / b, size=S)
+
+    def cost(fin):
+        return np.where(fin <= d1 - now, 0.0, np.where(fin <= d2 - now, c1, c2))
+    saved = cost(lat + delay) - cost(lat)
+    E = w * (0.5 + np.sum(1.0 - G[1:]))
+    got = it["score"][0] * E
+    sig = float(saved.std()) / math.sqrt(S)
+    assert abs(saved.mean() - got) <= 4 * sig + 1e-9, (saved.mean(), got, sig)
+    # the drop phase looks at the last step: past d1 but before d2 a step
+    # request is still kept, a single-step one is not
+    later = oracle.iterate_model(row[None, None, :], [1], w, np.zeros(2, np.int32),
+                                 np.array([d1, d1]), d1 + 1.0, b, L=L,
+                                 steps=(np.array([0, 2, 3]), np.array([d1, d2, d1]),
+                                        np.array([c1, c2, 1.0])))
+    assert list(later["timed_out"]) == [0, 1]
+
+
+def pin_accumulate(L):
+    """Profiler feedback against numpy.histogram per (model, batch size,
+    class) group, on latencies away from bin edges, with out-of-range,
+    negative and non-finite samples rejected and beyond-grid ones in the
+    last bin."""
+    r = rng(73)
+    M, B, C, K = 3, 2, 4, 16
+    widths = np.array([0.5, 1.25, 2.0])
+    counts = r.integers(0, 5, size=(M, B, C, K)).astype(np.uint32)
+    before = counts.copy()
+    n = 5000
+    mo = r.integers(0, M, size=n)
+    bi = r.integers(0, B, size=n)
+    cl = r.integers(0, C, size=n)
+    lat = (r.integers(0, K + 6, size=n) + r.uniform(0.01, 0.99, size=n)) * widths[mo]
+    bad = r.random(n) < 0.05
+    lat[bad & (r.random(n) < 0.5)] = -1.0
+    lat[bad & (lat >= 0)] = np.nan
+    mo[r.random(n) < 0.01] = M
+    cl[r.random(n) < 0.01] = -1
+    rej = oracle.accumulate(counts, widths, mo, bi, cl, lat, L=L)
+    ok = (mo >= 0) & (mo < M) & (cl >= 0) & (cl < C) & np.isfinite(lat) & (lat >= 0)
+    assert rej == int((~ok).sum())
+    for q in range(M):
+        edges = np.concatenate([np.arange(K) * widths[q], [np.inf]])
+        for b_ in range(B):
+            for c in range(C):
+                sel = ok & (mo == q) & (bi == b_) & (cl == c)
+                h, _ = np.histogram(lat[sel], bins=edges)
+                assert np.array_equal(counts[q, b_, c].astype(np.int64) - before[q, b_, c], h), (q, b_, c)
+
+
 PINS = [pin_enumeration, pin_iid_power, pin_point_mass, pin_quadrature_medium, pin_b_to_zero,
         pin_monte_carlo_max, pin_monte_carlo_priority, pin_ozbey_eq8, pin_invariants,
         pin_continuity, pin_edge_cases, pin_selection, pin_rect_mode, pin_toy_example,
         pin_iterate_one_class, pin_iterate_point_mix, pin_iterate_monte_carlo_mix,
-        pin_iterate_feasibility_and_popbatch]
+        pin_iterate_feasibility_and_popbatch, pin_cost_weights, pin_step_costs, pin_accumulate]

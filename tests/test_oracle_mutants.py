@@ -69,6 +69,19 @@ MUTANTS = {
     # Algorithm 1: candidate order ascending in D_{Q_s}
     "iter_cand_order": ("if (d_new > d_old || (d_new == d_old && batch_sizes[bi] > batch_sizes[cand]))",
                         "if (d_new < d_old || (d_new == d_old && batch_sizes[bi] > batch_sizes[cand]))"),
+    # miss costs ignored in the score
+    "cost_ignored": ("s += (cost ? cost[m - 1] : 1.0) * p;", "s += p;"),
+    # App. B: cumulative costs used as increments
+    "steps_cumulative": ("pr += (step_cost[j] - below) * priority_times_latency(dG, K, w, tau_j, b);",
+                         "pr += step_cost[j] * priority_times_latency(dG, K, w, tau_j, b);"),
+    # App. B: the drop phase looks at the first step
+    "steps_drop_first": ("double last = step_off ? step_deadline_ms[step_off[r + 1] - 1] : deadline_ms[r];\n        double tau = last - now_ms;",
+                         "double last = deadline_ms[r];\n        double tau = last - now_ms;"),
+    # profiler: beyond-grid samples dropped instead of counted in the last bin
+    "accumulate_clip": ("int32_t k = u >= (double)(n_bins - 1) ? n_bins - 1 : (int32_t)u;",
+                        "if (u >= (double)n_bins) { ++rejected; continue; }\n        int32_t k = (int32_t)u;"),
+    # profiler: bin by rounding instead of flooring
+    "accumulate_round": ("double u = floor(lat / bin_width_ms[q]);", "double u = floor(lat / bin_width_ms[q] + 0.5);"),
     # Algorithm 1: PopBatch takes the lowest priorities
     "iter_pop_lowest": ("if (si > sb || (si == sb && order[i] < order[best]))",
                         "if (si < sb || (si == sb && order[i] < order[best]))"),
