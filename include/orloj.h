@@ -14,6 +14,7 @@
  *   orloj_build_model_laws  model-wide batch laws for the scheduler iteration
  *   orloj_iterate           one Algorithm 1 iteration per model (drop phase,
  *                           candidate batch size, PopBatch by priority)
+ *   orloj_accumulate        profiler feedback into the histograms
  *
  * Conventions.  Pointers named d_* are device (HBM) pointers owned by the
  * caller; h_* pointers and the structs are host memory read during the call
@@ -106,6 +107,11 @@ typedef struct orloj_queues {
     const int32_t *d_class;         /* device [N], class id in [0, C) */
     const double *d_deadline_ms;    /* device [N] absolute deadlines */
     const double *d_now_ms;         /* device [M] current time per model */
+    const double *d_cost;           /* device [N] miss cost c of each request (§4.1), finite,
+                                       >= 0; NULL = 1 for every request.  It weights the
+                                       request's priority; finish probabilities are not
+                                       weighted.  A negative or non-finite cost is a data
+                                       error (the request then counts with cost 0). */
 } orloj_queues;
 
 /*
@@ -233,14 +239,51 @@ int orloj_select_batch(orloj_ctx *ctx, const orloj_grid *grid, const orloj_queue
  * above 1024.  Queue data errors are reported by orloj_sync as for
  * orloj_score_candidates.
  */
+/*
+ * Piecewise-step cost functions (App. B) for orloj_iterate: request r's cost
+ * rises to d_step_cost[j] when it finishes after d_step_deadline_ms[j], for
+ * j in [d_step_off[r], d_step_off[r+1]) (r indexes the whole queue array,
+ * all models back to back; deadlines increasing, costs non-decreasing and
+ * >= 0, at least one step per request).  Such a function is the sum of
+ * single steps at each d_j with cost d_step_cost[j] - d_step_cost[j-1], so
+ * the request's priority is the matching sum of single-step priorities,
+ * times its d_cost.  The drop phase uses the last step's deadline (the
+ * request still has cost to save until then); queue order and D_{Q_s} use
+ * d_deadline_ms.  Malformed steps are a data error (the request then scores
+ * 0).  h_step_off is the host copy of the offsets (validated on the host).
+ */
+typedef struct orloj_steps {
+    const int64_t *h_step_off;      /* host [N+1] */
+    const int64_t *d_step_off;      /* device copy */
+    const double *d_step_deadline_ms;
+    const double *d_step_cost;
+} orloj_steps;
+
 int orloj_build_model_laws(orloj_ctx *ctx, const orloj_grid *grid, const float *d_ccdf,
                            const double *d_class_weights, double b_expo_per_ms,
                            float *d_law, float *d_disc, float *d_model_el);
 
 int orloj_iterate(orloj_ctx *ctx, const orloj_grid *grid, const int32_t *d_support,
                   const float *d_law, const float *d_disc, const float *d_model_el,
-                  const orloj_queues *queues, double b_expo_per_ms, int32_t *d_timed_out,
-                  float *d_score, int32_t *d_cand_bs, int32_t *d_batch);
+                  const orloj_queues *queues, const orloj_steps *steps,
+                  double b_expo_per_ms, int32_t *d_timed_out, float *d_score,
+                  int32_t *d_cand_bs, int32_t *d_batch);
+
+/*
+ * Profiler feedback (§3.2 "Long-Term Feedback Loop"): add n_samples solo
+ * execution times of sampled finished requests to the histograms.  Sample i
+ * adds one count to d_counts[d_model[i]][d_bs_index[i]][d_class[i]][k],
+ * k = floor(d_latency_ms[i] / w_q), a latency at or beyond the grid counting
+ * in the last bin.  Samples with an index out of range or a negative or
+ * non-finite latency are skipped and counted in *d_n_rejected (device,
+ * optional, added to).  Atomic updates: concurrent calls on the same counts
+ * add up.  A profiling window is reset by zeroing d_counts; the CDF tables
+ * are rebuilt from the counts with orloj_build_cdfs.
+ */
+int orloj_accumulate(orloj_ctx *ctx, const orloj_grid *grid, int64_t n_samples,
+                     const int32_t *d_model, const int32_t *d_bs_index, const int32_t *d_class,
+                     const double *d_latency_ms, uint32_t *d_counts,
+                     unsigned long long *d_n_rejected);
 
 #ifdef __cplusplus
 }

@@ -159,7 +159,7 @@ def score_workload(wl, prefix_mode: int = 0, models: Optional[Sequence[int]] = N
         m = wl.model(q)
         parts.append(score_model(m["counts"], wl.batch_sizes, m["bin_width_ms"], m["cls"],
                                  m["deadline_ms"], m["now_ms"], wl.b_expo, prefix_mode,
-                                 want_priority, L))
+                                 want_priority, L, cost=m["cost"]))
     cat = lambda k: (np.concatenate([p[k] for p in parts]) if parts else np.zeros(0))
     out = {k: cat(k) for k in ("finish_prob", "expected_finish", "expected_latency_ms", "score")}
     if want_priority:
@@ -208,16 +208,25 @@ def iterate_model(counts, batch_sizes, bin_width_ms, cls, deadline_ms, now_ms, b
                 batch=batch[:int(bn[0])].copy())
 
 
-def iterate_workload(wl, weights=None, models: Optional[Sequence[int]] = None, L=None) -> dict:
+def iterate_workload(wl, weights=None, models: Optional[Sequence[int]] = None, L=None,
+                     steps=None) -> dict:
     """Algorithm 1 for every model of a workload (or the listed ones);
-    per-request outputs concatenated in model order."""
+    per-request outputs concatenated in model order.  steps = (step_off over
+    the whole queue array, step_deadline_ms, step_cost) or None."""
     models = list(range(wl.n_models)) if models is None else list(models)
     parts = []
     for q in models:
         m = wl.model(q)
+        st = None
+        if steps is not None:
+            a, b = int(wl.queue_off[q]), int(wl.queue_off[q + 1])
+            off = np.asarray(steps[0], np.int64)
+            lo, hi = int(off[a]), int(off[b])
+            st = (off[a:b + 1] - lo, np.asarray(steps[1])[lo:hi], np.asarray(steps[2])[lo:hi])
         parts.append(iterate_model(m["counts"], wl.batch_sizes, m["bin_width_ms"], m["cls"],
                                    m["deadline_ms"], m["now_ms"], wl.b_expo,
-                                   None if weights is None else weights[q], L))
+                                   None if weights is None else weights[q], L, cost=m["cost"],
+                                   steps=st))
     cat = lambda k: (np.concatenate([p[k] for p in parts]) if parts else np.zeros(0))
     return dict(timed_out=cat("timed_out").astype(np.int32), score=cat("score"),
                 cand_bs=np.array([p["cand_bs"] for p in parts], np.int32),

@@ -41,6 +41,7 @@ constexpr int kErrUnsorted = 8;
 constexpr int kErrNowNaN = 16;
 constexpr int kErrWidth = 32;
 constexpr int kErrWeights = 64;
+constexpr int kErrCost = 128;
 
 // ---------------------------------------------------------------------------
 // wave64 helpers
@@ -237,6 +238,7 @@ struct ScoreArgs {
     float* EL;
     float* S;
     const int32_t* sup;        // [M][nbs][C][2] first / last bin with mass, or NULL
+    const double* cost;        // [N] miss cost per request, or NULL (1)
     const float* fill;         // [2][16] zeros, ones (the context's stand-in rows)
     int* err;
     double b;
@@ -294,6 +296,7 @@ struct Member {
     float theta;    // position inside bin k
     float cg;       // gamma exp(-b theta w), or gamma exp(-b (tau - K w))
     float psi;      // (1 - exp(-b theta w)) / (b w)
+    float cost;     // the request's miss cost (weights its priority)
 };
 
 template <int CPL>
@@ -470,9 +473,12 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         if (m > 0 && D < a.deadline[q0 + m - 1]) flag |= kErrUnsorted;
         if (m == 0 && isnan(nowq)) flag |= kErrNowNaN;
         if (m == 0 && !wok) flag |= kErrWidth;
+        double cm = a.cost ? a.cost[q0 + m] : 1.0;
+        if (!(cm >= 0.0 && cm < HUGE_VAL)) { flag |= kErrCost; cm = 0.0; }
         if (flag) atomicOr(a.err, flag);
         Member mb;
         mb.cls = c;
+        mb.cost = (float)cm;
         int hp = 0, ig0 = kNone, ig1 = kNone, ig4 = kNone, izq = kNone, la = kNone;
         mb.cW = mb.cG = mb.cA = mb.fq = 0.0f;
         mb.wq[0] = mb.wq[1] = mb.wq[2] = mb.wq[3] = 0.0f;
@@ -738,7 +744,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                             const float Zv = fmaf(mb.cW, Win, fmaf(mb.cG, glin, fmaf(mb.cA, mb.la >= 0 ? al0 : 0.0f, zin)));
                             const float h = gk1 - gk;
                             const float P = fmaf(mb.theta, h, gk);
-                            const float num = fmaf(mb.cg, fmaf(-omd, Zv, gk), h * mb.psi);
+                            const float num = mb.cost * fmaf(mb.cg, fmaf(-omd, Zv, gk), h * mb.psi);
                             a.P[prob + (int64_t)n * nn / 2 + m] = P;
                             pP += (double)P;
                             pN += num;
@@ -1026,6 +1032,10 @@ struct IterArgs {
     const double* deadline;
     const double* now;
     const double* width;
+    const double* cost;        // [N] or NULL (1)
+    const int64_t* step_off;   // [N+1] or NULL (one step at the deadline)
+    const double* step_dl;     // [S]
+    const double* step_cost;   // [S] cumulative costs
     int32_t* timed_out;        // [N]
     float* score;              // [N]
     int32_t* cand_bs;          // [M]
@@ -1071,6 +1081,8 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
         if (live) {
             c = a.cls[q0 + i];
             const double D = a.deadline[q0 + i];
+            // the drop phase looks at the last step of a step cost function
+            const double Dlast = a.step_off ? a.step_dl[a.step_off[q0 + i + 1] - 1] : D;
             int flag = 0;
             if (c < 0 || c >= C) { flag |= kErrClassRange; c = 0; }
             if (isnan(D)) flag |= kErrDeadlineNaN;
@@ -1078,7 +1090,7 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
             if (i == 0 && isnan(nowq)) flag |= kErrNowNaN;
             if (i == 0 && !wok) flag |= kErrWidth;
             if (flag) atomicOr(a.err, flag);
-            tau = D - nowq;
+            tau = Dlast - nowq;
         }
         bool any = false;
         for (int bi = 0; bi < nbs; ++bi) {
@@ -1136,18 +1148,21 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
         if (i < N) {
             int c = a.cls[q0 + i];
             c = (c < 0 || c >= C) ? 0 : c;
-            const double tau = a.deadline[q0 + i] - nowq;
+            const double D = a.deadline[q0 + i];
+            const double Dlast = a.step_off ? a.step_dl[a.step_off[q0 + i + 1] - 1] : D;
             const int lo = sup_q[((size_t)cand * C + c) * 2];
-            if (wok && tau > (double)lo * w) {
+            if (wok && Dlast - nowq > (double)lo * w) {
                 const float* G = a.law + (lrow0 + c) * (size_t)K;
                 const float* Z = a.disc + (lrow0 + c) * (size_t)K;
-                const double u = tau / w;
-                double num;
-                if (u >= (double)K) {
-                    const double cg = gamma * exp(-a.b * (tau - (double)K * w));
-                    const double zk = K >= 2 ? (double)Z[K - 2] : 0.0;
-                    num = cg * (1.0 - omd * zk);
-                } else {
+                // Eq. (2) x E[L] for one deadline, in the scan form
+                auto num_at = [&](double tau) -> double {
+                    if (!(tau > 0.0)) return 0.0;
+                    const double u = tau / w;
+                    if (u >= (double)K) {
+                        const double cg = gamma * exp(-a.b * (tau - (double)K * w));
+                        const double zk = K >= 2 ? (double)Z[K - 2] : 0.0;
+                        return cg * (1.0 - omd * zk);
+                    }
                     const int k = (int)floor(u);
                     const double th = u - (double)k;
                     const double gk = k >= 1 ? (double)G[k - 1] : 0.0;
@@ -1155,8 +1170,31 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
                     const double zk = k >= 2 ? (double)Z[k - 2] : 0.0;
                     const double cg = gamma * exp(-a.b * th * w);
                     const double psi = -expm1(-a.b * th * w) / bw;
-                    num = cg * (gk - omd * zk) + (gk1 - gk) * psi;
+                    return cg * (gk - omd * zk) + (gk1 - gk) * psi;
+                };
+                double cr = a.cost ? a.cost[q0 + i] : 1.0;
+                int flag = 0;
+                if (!(cr >= 0.0 && cr < HUGE_VAL)) { flag = kErrCost; cr = 0.0; }
+                double num = 0.0;
+                if (a.step_off) {
+                    // App. B: one single step per cost increment
+                    double below = 0.0, dprev = -HUGE_VAL;
+                    for (int64_t st = a.step_off[q0 + i]; st < a.step_off[q0 + i + 1]; ++st) {
+                        const double dj = a.step_dl[st], cj = a.step_cost[st];
+                        if (!(cj >= below && cj < HUGE_VAL) || !(dj > dprev)) {
+                            flag = kErrCost;
+                            num = 0.0;
+                            break;
+                        }
+                        num += (cj - below) * num_at(dj - nowq);
+                        below = cj;
+                        dprev = dj;
+                    }
+                } else {
+                    num = num_at(D - nowq);
                 }
+                if (flag) atomicOr(a.err, flag);
+                num *= cr;
                 const float p = (float)(num / (double)el);
                 a.score[q0 + i] = p;
                 const float pp = p > 0.0f ? p : 0.0f;
@@ -1196,6 +1234,46 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
         bq[rank] = (int32_t)(0xffffffffu - (unsigned)(kj & 0xffffffffull));
     }
     for (int j = nsel + tid; j < a.bs_max; j += kThreads) bq[j] = -1;
+}
+
+// ---------------------------------------------------------------------------
+// accumulate_kernel: profiler feedback.  One thread per sample (grid-stride):
+// validate, bin by floor(latency / w) with the last bin catching the tail,
+// and add one count with a device-scope atomic.
+// ---------------------------------------------------------------------------
+struct AccArgs {
+    const int32_t* model;
+    const int32_t* bs_index;
+    const int32_t* cls;
+    const double* latency;
+    const double* width;
+    uint32_t* counts;
+    unsigned long long* n_rejected;
+    int64_t n;
+    int M, nbs, C, K;
+};
+
+__global__ __launch_bounds__(kThreads) void accumulate_kernel(const AccArgs a) {
+    unsigned long long rejected = 0;
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < a.n;
+         i += (int64_t)gridDim.x * kThreads) {
+        const int q = a.model[i], b = a.bs_index[i], c = a.cls[i];
+        const double lat = a.latency[i];
+        if (q < 0 || q >= a.M || b < 0 || b >= a.nbs || c < 0 || c >= a.C ||
+            !(lat >= 0.0 && lat < HUGE_VAL)) {
+            ++rejected;
+            continue;
+        }
+        const double w = a.width[q];
+        if (!(w > 0.0)) {
+            ++rejected;
+            continue;
+        }
+        const double u = floor(lat / w);
+        const int k = u >= (double)(a.K - 1) ? a.K - 1 : (int)u;
+        atomicAdd(a.counts + (((size_t)q * a.nbs + b) * a.C + c) * (size_t)a.K + k, 1u);
+    }
+    if (a.n_rejected && rejected) atomicAdd(a.n_rejected, rejected);
 }
 
 }  // namespace
@@ -1390,14 +1468,15 @@ int orloj_sync(orloj_ctx* ctx) {
     if (flags) {
         e = hipMemset(ctx->d_err, 0, sizeof(int));
         if (e != hipSuccess) return hip_fail(ctx, e, "clearing the device status word");
-        return fail(ctx, ORLOJ_E_DATA, "device data error:%s%s%s%s%s%s%s",
+        return fail(ctx, ORLOJ_E_DATA, "device data error:%s%s%s%s%s%s%s%s",
                     (flags & kErrEmptyHistogram) ? " histogram-with-no-samples" : "",
                     (flags & kErrClassRange) ? " class-id-out-of-range" : "",
                     (flags & kErrDeadlineNaN) ? " NaN-deadline" : "",
                     (flags & kErrUnsorted) ? " deadlines-not-sorted" : "",
                     (flags & kErrNowNaN) ? " NaN-now" : "",
                     (flags & kErrWidth) ? " bin-width-not-positive" : "",
-                    (flags & kErrWeights) ? " class-weights-invalid" : "");
+                    (flags & kErrWeights) ? " class-weights-invalid" : "",
+                    (flags & kErrCost) ? " cost-or-steps-invalid" : "");
     }
     return ORLOJ_OK;
 }
@@ -1502,6 +1581,7 @@ int orloj_score_candidates(orloj_ctx* ctx, const orloj_grid* grid, const float* 
     ScoreArgs a;
     a.tab = d_ccdf;
     a.sup = d_support;
+    a.cost = queues->d_cost;
     a.fill = ctx->d_fill;
     a.queue_off = queues->d_queue_off;
     a.cls = queues->d_class;
@@ -1587,8 +1667,8 @@ int orloj_build_model_laws(orloj_ctx* ctx, const orloj_grid* grid, const float* 
 
 int orloj_iterate(orloj_ctx* ctx, const orloj_grid* grid, const int32_t* d_support,
                   const float* d_law, const float* d_disc, const float* d_model_el,
-                  const orloj_queues* queues, double b_expo_per_ms, int32_t* d_timed_out,
-                  float* d_score, int32_t* d_cand_bs, int32_t* d_batch) {
+                  const orloj_queues* queues, const orloj_steps* steps, double b_expo_per_ms,
+                  int32_t* d_timed_out, float* d_score, int32_t* d_cand_bs, int32_t* d_batch) {
     if (!ctx) return ORLOJ_E_INVALID;
     int rc = check_grid(ctx, grid);
     if (rc) return rc;
@@ -1611,6 +1691,15 @@ int orloj_iterate(orloj_ctx* ctx, const orloj_grid* grid, const int32_t* d_suppo
         return fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
     if (queues->h_queue_off[M] > 0 && (!d_timed_out || !d_score))
         return fail(ctx, ORLOJ_E_INVALID, "NULL per-request output");
+    if (steps) {
+        const int64_t* so = steps->h_step_off;
+        if (!so || !steps->d_step_off || !steps->d_step_deadline_ms || !steps->d_step_cost)
+            return fail(ctx, ORLOJ_E_INVALID, "incomplete orloj_steps");
+        if (so[0] != 0) return fail(ctx, ORLOJ_E_INVALID, "h_step_off[0] != 0");
+        for (int64_t r = 0; r < queues->h_queue_off[M]; ++r)
+            if (so[r + 1] <= so[r])
+                return fail(ctx, ORLOJ_E_INVALID, "request %lld has no cost step", (long long)r);
+    }
     IterArgs a;
     a.sup = d_support;
     a.law = d_law;
@@ -1621,6 +1710,10 @@ int orloj_iterate(orloj_ctx* ctx, const orloj_grid* grid, const int32_t* d_suppo
     a.deadline = queues->d_deadline_ms;
     a.now = queues->d_now_ms;
     a.width = grid->d_bin_width_ms;
+    a.cost = queues->d_cost;
+    a.step_off = steps ? steps->d_step_off : nullptr;
+    a.step_dl = steps ? steps->d_step_deadline_ms : nullptr;
+    a.step_cost = steps ? steps->d_step_cost : nullptr;
     a.timed_out = d_timed_out;
     a.score = d_score;
     a.cand_bs = d_cand_bs;
@@ -1639,6 +1732,40 @@ int orloj_iterate(orloj_ctx* ctx, const orloj_grid* grid, const int32_t* d_suppo
     hipLaunchKernelGGL(iterate_kernel, dim3(M), dim3(kThreads), 0, ctx->stream, a);
     e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(ctx, e, "iterate_kernel launch");
+    return ORLOJ_OK;
+}
+
+int orloj_accumulate(orloj_ctx* ctx, const orloj_grid* grid, int64_t n_samples,
+                     const int32_t* d_model, const int32_t* d_bs_index, const int32_t* d_class,
+                     const double* d_latency_ms, uint32_t* d_counts,
+                     unsigned long long* d_n_rejected) {
+    if (!ctx) return ORLOJ_E_INVALID;
+    int rc = check_grid(ctx, grid);
+    if (rc) return rc;
+    if (n_samples < 0) return fail(ctx, ORLOJ_E_INVALID, "n_samples < 0");
+    if (n_samples == 0) return ORLOJ_OK;
+    if (!d_model || !d_bs_index || !d_class || !d_latency_ms || !d_counts || !grid->d_bin_width_ms)
+        return fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
+    AccArgs a;
+    a.model = d_model;
+    a.bs_index = d_bs_index;
+    a.cls = d_class;
+    a.latency = d_latency_ms;
+    a.width = grid->d_bin_width_ms;
+    a.counts = d_counts;
+    a.n_rejected = d_n_rejected;
+    a.n = n_samples;
+    a.M = grid->n_models;
+    a.nbs = grid->n_bs;
+    a.C = grid->n_classes;
+    a.K = grid->n_bins;
+    hipError_t e = hipSetDevice(ctx->device);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    const int64_t want = (n_samples + kThreads - 1) / kThreads;
+    const unsigned g = (unsigned)(want < 4096 ? want : 4096);
+    hipLaunchKernelGGL(accumulate_kernel, dim3(g), dim3(kThreads), 0, ctx->stream, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(ctx, e, "accumulate_kernel launch");
     return ORLOJ_OK;
 }
 

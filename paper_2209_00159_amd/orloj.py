@@ -41,18 +41,25 @@ class Grid(ctypes.Structure):
 class Queues(ctypes.Structure):
     _fields_ = [("h_queue_off", ctypes.POINTER(ctypes.c_int64)),
                 ("d_queue_off", ctypes.c_void_p), ("d_class", ctypes.c_void_p),
-                ("d_deadline_ms", ctypes.c_void_p), ("d_now_ms", ctypes.c_void_p)]
+                ("d_deadline_ms", ctypes.c_void_p), ("d_now_ms", ctypes.c_void_p),
+                ("d_cost", ctypes.c_void_p)]
+
+
+class Steps(ctypes.Structure):
+    _fields_ = [("h_step_off", ctypes.POINTER(ctypes.c_int64)), ("d_step_off", ctypes.c_void_p),
+                ("d_step_deadline_ms", ctypes.c_void_p), ("d_step_cost", ctypes.c_void_p)]
 
 
 _LIB = None
 _VP = ctypes.c_void_p
 _GP = ctypes.POINTER(Grid)
 _QP = ctypes.POINTER(Queues)
+_SP = ctypes.POINTER(Steps)
 _I64P = ctypes.POINTER(ctypes.c_int64)
 
 EXPORTS = ("orloj_create", "orloj_destroy", "orloj_set_stream", "orloj_last_error", "orloj_sync",
            "orloj_build_cdfs", "orloj_output_sizes", "orloj_score_candidates",
-           "orloj_select_batch", "orloj_build_model_laws", "orloj_iterate")
+           "orloj_select_batch", "orloj_build_model_laws", "orloj_iterate", "orloj_accumulate")
 
 
 def load(path: Optional[str] = None):
@@ -87,9 +94,11 @@ def load(path: Optional[str] = None):
     L.orloj_select_batch.restype = ctypes.c_int
     L.orloj_build_model_laws.argtypes = [_VP, _GP, _VP, _VP, ctypes.c_double, _VP, _VP, _VP]
     L.orloj_build_model_laws.restype = ctypes.c_int
-    L.orloj_iterate.argtypes = [_VP, _GP, _VP, _VP, _VP, _VP, _QP, ctypes.c_double, _VP, _VP,
-                                _VP, _VP]
+    L.orloj_iterate.argtypes = [_VP, _GP, _VP, _VP, _VP, _VP, _QP, _SP, ctypes.c_double, _VP,
+                                _VP, _VP, _VP]
     L.orloj_iterate.restype = ctypes.c_int
+    L.orloj_accumulate.argtypes = [_VP, _GP, ctypes.c_int64, _VP, _VP, _VP, _VP, _VP, _VP]
+    L.orloj_accumulate.restype = ctypes.c_int
     if default:
         _LIB = L
     return L
@@ -175,10 +184,11 @@ def make_grid(n_models, n_classes, n_bins, batch_sizes: np.ndarray,
     return g
 
 
-def make_queues(h_queue_off: np.ndarray, d_queue_off, d_class, d_deadline_ms, d_now_ms):
+def make_queues(h_queue_off: np.ndarray, d_queue_off, d_class, d_deadline_ms, d_now_ms,
+                d_cost=None):
     ho = np.ascontiguousarray(h_queue_off, dtype=np.int64)
     qs = Queues(ho.ctypes.data_as(_I64P), _ptr(d_queue_off), _ptr(d_class), _ptr(d_deadline_ms),
-                _ptr(d_now_ms))
+                _ptr(d_now_ms), _ptr(d_cost))
     qs._keep = ho
     return qs
 
@@ -226,15 +236,17 @@ class Scorer:
         self.sel_bs = torch.zeros(M, dtype=torch.int32, device=dev)
         self.sel_score = torch.zeros(M, dtype=torch.float32, device=dev)
 
-    def set_queues(self, queue_off, cls, deadline_ms, now_ms):
+    def set_queues(self, queue_off, cls, deadline_ms, now_ms, cost=None):
         dev = self.ctx.device
         self.h_queue_off = np.ascontiguousarray(queue_off, np.int64)
         self.d_queue_off = torch.from_numpy(self.h_queue_off).to(dev)
         self.d_class = torch.from_numpy(np.ascontiguousarray(cls, np.int32)).to(dev)
         self.d_deadline = torch.from_numpy(np.ascontiguousarray(deadline_ms, np.float64)).to(dev)
         self.d_now = torch.from_numpy(np.ascontiguousarray(now_ms, np.float64)).to(dev)
+        c = getattr(self.wl, "cost", None) if cost is None else cost
+        self.d_cost = None if c is None else torch.from_numpy(np.ascontiguousarray(c, np.float64)).to(dev)
         self.queues = make_queues(self.h_queue_off, self.d_queue_off, self.d_class,
-                                  self.d_deadline, self.d_now)
+                                  self.d_deadline, self.d_now, self.d_cost)
         self.n_cands, self.n_probs, self.h_cand_off, self.h_prob_off = output_sizes(
             self.grid, self.queues, self.mode)
         self.d_cand_off = torch.from_numpy(self.h_cand_off).to(dev)
@@ -311,15 +323,27 @@ class Iterator:
         self.batch = torch.full((wl.n_models, self.bs_max), -1, dtype=torch.int32, device=dev)
         self.set_queues(wl.queue_off, wl.cls, wl.deadline_ms, wl.now_ms)
 
-    def set_queues(self, queue_off, cls, deadline_ms, now_ms):
+    def set_queues(self, queue_off, cls, deadline_ms, now_ms, cost=None, steps=None):
+        """steps = (step_off [N+1] over the whole queue array, step_deadline_ms,
+        step_cost) for piecewise-step cost functions, or None."""
         dev = self.ctx.device
         self.h_queue_off = np.ascontiguousarray(queue_off, np.int64)
         self.d_queue_off = torch.from_numpy(self.h_queue_off).to(dev)
         self.d_class = torch.from_numpy(np.ascontiguousarray(cls, np.int32)).to(dev)
         self.d_deadline = torch.from_numpy(np.ascontiguousarray(deadline_ms, np.float64)).to(dev)
         self.d_now = torch.from_numpy(np.ascontiguousarray(now_ms, np.float64)).to(dev)
+        c = getattr(self.wl, "cost", None) if cost is None else cost
+        self.d_cost = None if c is None else torch.from_numpy(np.ascontiguousarray(c, np.float64)).to(dev)
         self.queues = make_queues(self.h_queue_off, self.d_queue_off, self.d_class,
-                                  self.d_deadline, self.d_now)
+                                  self.d_deadline, self.d_now, self.d_cost)
+        self.steps = None
+        if steps is not None:
+            self.h_step_off = np.ascontiguousarray(steps[0], np.int64)
+            self.d_step_off = torch.from_numpy(self.h_step_off).to(dev)
+            self.d_step_dl = torch.from_numpy(np.ascontiguousarray(steps[1], np.float64)).to(dev)
+            self.d_step_cost = torch.from_numpy(np.ascontiguousarray(steps[2], np.float64)).to(dev)
+            self.steps = Steps(self.h_step_off.ctypes.data_as(_I64P), _ptr(self.d_step_off),
+                               _ptr(self.d_step_dl), _ptr(self.d_step_cost))
         n = int(self.h_queue_off[-1])
         self.timed_out = torch.zeros(max(n, 1), dtype=torch.int32, device=dev)
         self.score = torch.zeros(max(n, 1), dtype=torch.float32, device=dev)
@@ -337,7 +361,9 @@ class Iterator:
         c = self.ctx
         c._check(c.L.orloj_iterate(
             c.ctx, ctypes.byref(self.grid), _ptr(self.support), _ptr(self.law), _ptr(self.disc),
-            _ptr(self.model_el), ctypes.byref(self.queues), self.b, _ptr(self.timed_out),
+            _ptr(self.model_el), ctypes.byref(self.queues),
+            ctypes.byref(self.steps) if self.steps is not None else None, self.b,
+            _ptr(self.timed_out),
             _ptr(self.score), _ptr(self.cand_bs), _ptr(self.batch)))
 
     def run(self, build: bool = True, b_expo: Optional[float] = None) -> dict:
@@ -353,3 +379,23 @@ class Iterator:
         return dict(timed_out=self.timed_out[:n].cpu().numpy(), score=self.score[:n].cpu().numpy(),
                     cand_bs=self.cand_bs.cpu().numpy(), batch=self.batch.cpu().numpy(),
                     model_el=self.model_el.cpu().numpy())
+
+
+def accumulate(ctx: Context, grid: Grid, counts: torch.Tensor, model, bs_index, cls,
+               latency_ms) -> int:
+    """Profiler feedback: add the samples (device tensors: int32 model,
+    batch-size index, class; float64 latency) to counts (int32/uint32
+    [M][B][C][K] on the device).  Returns the number of rejected samples
+    (this synchronises)."""
+    _need_cuda(counts, "counts", (torch.int32, torch.uint32), ctx.device)
+    for t, name, dt in ((model, "model", torch.int32), (bs_index, "bs_index", torch.int32),
+                        (cls, "cls", torch.int32), (latency_ms, "latency_ms", torch.float64)):
+        _need_cuda(t, name, (dt,), ctx.device)
+    n = int(latency_ms.numel())
+    if not (model.numel() == bs_index.numel() == cls.numel() == n):
+        raise ValueError("sample arrays differ in length")
+    rej = torch.zeros(1, dtype=torch.int64, device=ctx.device)
+    ctx._check(ctx.L.orloj_accumulate(ctx.ctx, ctypes.byref(grid), n, _ptr(model), _ptr(bs_index),
+                                      _ptr(cls), _ptr(latency_ms), _ptr(counts), _ptr(rej)))
+    ctx.sync()
+    return int(rej.item())

@@ -142,6 +142,7 @@ class Workload:
     now_ms: np.ndarray             # float64 [M]
     b_expo: float = DEFAULT_B_EXPO
     description: str = ""
+    cost: Optional[np.ndarray] = None  # float64 [N_total] miss cost per request (None: 1)
 
     @property
     def n_bs(self) -> int:
@@ -154,17 +155,20 @@ class Workload:
         a, b = int(self.queue_off[q]), int(self.queue_off[q + 1])
         return dict(counts=self.counts[q], cls=self.cls[a:b],
                     deadline_ms=self.deadline_ms[a:b], now_ms=float(self.now_ms[q]),
-                    bin_width_ms=float(self.bin_width_ms[q]))
+                    bin_width_ms=float(self.bin_width_ms[q]),
+                    cost=None if self.cost is None else self.cost[a:b])
 
     def subset(self, models: Sequence[int]) -> "Workload":
         """A workload made of the listed models only (same grid shapes)."""
         models = list(models)
         offs = [0]
-        cls, dl = [], []
+        cls, dl, co = [], [], []
         for q in models:
             a, b = int(self.queue_off[q]), int(self.queue_off[q + 1])
             cls.append(self.cls[a:b])
             dl.append(self.deadline_ms[a:b])
+            if self.cost is not None:
+                co.append(self.cost[a:b])
             offs.append(offs[-1] + (b - a))
         return Workload(
             name=f"{self.name}[{len(models)} models]", config_id=self.config_id,
@@ -176,7 +180,8 @@ class Workload:
             cls=np.concatenate(cls).astype(np.int32) if cls else np.zeros(0, np.int32),
             deadline_ms=np.concatenate(dl) if dl else np.zeros(0),
             now_ms=self.now_ms[models].copy(), b_expo=self.b_expo,
-            description=self.description)
+            description=self.description,
+            cost=(np.concatenate(co) if co else np.zeros(0)) if self.cost is not None else None)
 
     def with_queues(self, queues: List[tuple], now_ms: np.ndarray) -> "Workload":
         """Same histograms, new queues: ``queues[q] = (cls, deadline_ms)``."""
@@ -188,7 +193,8 @@ class Workload:
         dl = np.concatenate([np.asarray(d, np.float64) for _, d in queues]) \
             if queues else np.zeros(0)
         return dataclasses.replace(self, queue_off=offs, cls=cls.astype(np.int32),
-                                   deadline_ms=dl, now_ms=np.asarray(now_ms, np.float64))
+                                   deadline_ms=dl, now_ms=np.asarray(now_ms, np.float64),
+                                   cost=None)
 
 
 def _sorted_queue(cls: np.ndarray, deadline: np.ndarray):

@@ -143,3 +143,78 @@ def test_iterate_queue_limit_is_unsupported(ctx):
     with pytest.raises(O.OrlojError) as ei:
         it.iterate()
     assert ei.value.code == O.ORLOJ_E_UNSUPPORTED
+
+
+# ---------------------------------------------------------------- costs, step costs, profiler
+def random_steps(wl, seed, max_steps=3):
+    r = np.random.default_rng(seed)
+    n = wl.cls.size
+    k = r.integers(1, max_steps + 1, size=n)
+    off = np.concatenate([[0], np.cumsum(k)]).astype(np.int64)
+    dl, co = [], []
+    for i in range(n):
+        d = wl.deadline_ms[i] + np.concatenate([[0.0], np.cumsum(r.uniform(1.0, 40.0, size=k[i] - 1))])
+        c = np.cumsum(r.uniform(0.1, 2.0, size=k[i]))
+        dl.append(d)
+        co.append(c)
+    return off, np.concatenate(dl), np.concatenate(co)
+
+
+@pytest.mark.parametrize("seed", [50, 51, 52])
+def test_iterate_costs_and_steps(ctx, seed):
+    import dataclasses
+    wl = W.random_case(seed, n_models=3, queue_lens=[25, 9, 40], n_classes=4, n_bins=300,
+                       batch_sizes=(1, 2, 4, 8), tau_range=(-5.0, 200.0))
+    r = np.random.default_rng(seed)
+    wl = dataclasses.replace(wl, cost=r.uniform(0.0, 3.0, size=wl.cls.size))
+    steps = random_steps(wl, seed)
+    it = O.Iterator(wl, ctx)
+    it.set_queues(wl.queue_off, wl.cls, wl.deadline_ms, wl.now_ms, steps=steps)
+    got = it.run()
+    ora = oracle.iterate_workload(wl, steps=steps)
+    check(wl, got, ora)
+
+
+def test_iterate_bad_steps_are_a_data_error(ctx):
+    wl = W.random_case(53, n_models=1, queue_lens=[4], tau_range=(10.0, 40.0))
+    off = np.array([0, 1, 3, 4, 5], np.int64)
+    dl = np.array([wl.deadline_ms[0], wl.deadline_ms[1], wl.deadline_ms[1] - 1.0,
+                   wl.deadline_ms[2], wl.deadline_ms[3]])
+    co = np.array([1.0, 1.0, 2.0, 1.0, 1.0])
+    it = O.Iterator(wl, ctx)
+    it.set_queues(wl.queue_off, wl.cls, wl.deadline_ms, wl.now_ms, steps=(off, dl, co))
+    it.build()
+    it.iterate()
+    with pytest.raises(O.OrlojError) as ei:
+        ctx.sync()
+    assert ei.value.code == O.ORLOJ_E_DATA
+
+
+@pytest.mark.parametrize("n", [0, 1, 1000, 200_000])
+def test_accumulate_matches_oracle(ctx, n):
+    import torch
+    r = np.random.default_rng(60 + n)
+    M, B, C, K = 3, 4, 5, 257
+    widths = np.array([0.5, 1.25, 2.0])
+    counts = r.integers(0, 9, size=(M, B, C, K)).astype(np.uint32)
+    mo = r.integers(0, M, size=n).astype(np.int32)
+    bi = r.integers(0, B, size=n).astype(np.int32)
+    cl = r.integers(0, C, size=n).astype(np.int32)
+    lat = r.uniform(0.0, 1.2 * K, size=n) * widths[np.clip(mo, 0, M - 1)]
+    bad = r.random(n)
+    lat[bad < 0.01] = -3.0
+    lat[(bad >= 0.01) & (bad < 0.02)] = np.nan
+    lat[(bad >= 0.02) & (bad < 0.03)] = np.inf
+    mo[(bad >= 0.03) & (bad < 0.035)] = M
+    cl[(bad >= 0.035) & (bad < 0.04)] = -1
+    ref = counts.copy()
+    rej_ref = oracle.accumulate(ref, widths, mo, bi, cl, lat)
+    dev = ctx.device
+    d_counts = torch.from_numpy(counts.view(np.int32)).to(dev)
+    d_w = torch.from_numpy(widths).to(dev)
+    grid = O.make_grid(M, C, K, np.arange(1, B + 1), d_w)
+    rej = O.accumulate(ctx, grid, d_counts, torch.from_numpy(mo).to(dev), torch.from_numpy(bi).to(dev),
+                       torch.from_numpy(cl).to(dev), torch.from_numpy(lat).to(dev))
+    got = d_counts.cpu().numpy().view(np.uint32)
+    assert rej == rej_ref
+    assert np.array_equal(got, ref)

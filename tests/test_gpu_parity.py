@@ -263,3 +263,31 @@ def test_native_library_is_loaded(ctx):
     with open("/proc/self/maps") as f:
         maps = f.read()
     assert os.path.basename(O.LIB_PATH) in maps
+
+
+# ---------------------------------------------------------------- miss costs
+@pytest.mark.parametrize("case", [RANDOM_CASES[i] for i in (0, 1, 5, 7, 14)],
+                         ids=lambda c: f"seed{c['seed']}")
+def test_cost_weighted_scores(ctx, case):
+    import dataclasses
+    say("costs", case)
+    wl = W.random_case(**case)
+    r = np.random.default_rng(100 + case["seed"])
+    wl = dataclasses.replace(wl, cost=r.uniform(0.0, 4.0, size=wl.cls.size))
+    sc, got = run_gpu(wl, ctx)
+    parity.compare(wl, got, oracle.score_workload(wl))
+    _, untrimmed = run_gpu(wl, ctx, trim=False)
+    assert_same_bits(got, untrimmed)
+
+
+def test_negative_cost_is_a_data_error(ctx):
+    import dataclasses
+    wl = W.random_case(43, n_models=1, queue_lens=[5])
+    cost = np.ones(5)
+    cost[2] = -1.0
+    sc = O.Scorer(dataclasses.replace(wl, cost=cost), ctx)
+    sc.build()
+    sc.score()
+    with pytest.raises(O.OrlojError) as ei:
+        ctx.sync()
+    assert ei.value.code == O.ORLOJ_E_DATA
