@@ -55,6 +55,11 @@ def _bind(L):
         ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _F64P, ctypes.c_int64,
         _I32P, _I32P, _I32P, _F64P, _U32P, _I64P]
     L.orloj_oracle_accumulate.restype = ctypes.c_int
+    L.orloj_oracle_score_model_affine.argtypes = [
+        ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _I32P, ctypes.c_double, _U32P,
+        ctypes.c_double, ctypes.c_double, ctypes.c_int64, _I32P, _F64P, _F64P, ctypes.c_double,
+        ctypes.c_double, ctypes.c_int32, _F64P, _F64P, _F64P, _F64P, _F64P, _I32P, _I32P, _F64P]
+    L.orloj_oracle_score_model_affine.restype = ctypes.c_int
     L.orloj_oracle_iterate_model.restype = ctypes.c_int
     return L
 
@@ -252,3 +257,60 @@ def accumulate(counts, bin_width_ms, model, bs_index, cls, latency_ms, L=None) -
     if rc:
         raise OracleError(f"orloj_oracle_accumulate rc={rc}")
     return int(rej[0])
+
+
+def score_model_affine(counts_ck, batch_sizes, bin_width_ms, c0_ms, c1, cls, deadline_ms, now_ms,
+                       b_expo, prefix_mode: int = 0, want_priority: bool = False, L=None,
+                       cost=None) -> dict:
+    """All candidates of one model in the affine batch-latency mode (see
+    orloj_oracle_score_model_affine); counts_ck is [C][K]."""
+    L = L or lib()
+    cnt = np.ascontiguousarray(counts_ck, dtype=np.uint32)
+    C, K = cnt.shape
+    bs = np.ascontiguousarray(batch_sizes, dtype=np.int32)
+    cl = np.ascontiguousarray(cls, dtype=np.int32)
+    dl = np.ascontiguousarray(deadline_ms, dtype=np.float64)
+    caps = ncap(bs, cl.size, prefix_mode)
+    n_cand = int(caps.sum())
+    n_prob = int((caps * (caps + 1) // 2).sum())
+    P = np.empty(n_prob)
+    pr = np.empty(n_prob) if want_priority else None
+    E = np.empty(n_cand)
+    EL = np.empty(n_cand)
+    S = np.empty(n_cand)
+    sn = np.zeros(1, np.int32)
+    sb = np.zeros(1, np.int32)
+    ss = np.zeros(1)
+    co = _opt64(cost)
+    rc = L.orloj_oracle_score_model_affine(
+        C, K, bs.size, _p(bs, _I32P), float(bin_width_ms), _p(cnt, _U32P), float(c0_ms), float(c1),
+        cl.size, _p(cl, _I32P), _p(dl, _F64P), _p(co, _F64P) if co is not None else None,
+        float(now_ms), float(b_expo), int(prefix_mode), _p(P, _F64P),
+        _p(pr, _F64P) if pr is not None else None, _p(E, _F64P), _p(EL, _F64P), _p(S, _F64P),
+        _p(sn, _I32P), _p(sb, _I32P), _p(ss, _F64P))
+    if rc:
+        raise OracleError(f"orloj_oracle_score_model_affine rc={rc}")
+    out = dict(finish_prob=P, expected_finish=E, expected_latency_ms=EL, score=S,
+               sel_n=int(sn[0]), sel_bs=int(sb[0]), sel_score=float(ss[0]))
+    if pr is not None:
+        out["priority"] = pr
+    return out
+
+
+def score_workload_affine(wl, c0_ms, c1, prefix_mode: int = 0, models=None, L=None) -> dict:
+    """Affine mode over a workload whose counts are [M][C][K] (batch-size
+    independent); outputs concatenated in model order."""
+    models = list(range(wl.n_models)) if models is None else list(models)
+    parts = []
+    for q in models:
+        m = wl.model(q)
+        parts.append(score_model_affine(m["counts"], wl.batch_sizes, m["bin_width_ms"], c0_ms[q],
+                                        c1[q], m["cls"], m["deadline_ms"], m["now_ms"], wl.b_expo,
+                                        prefix_mode, L=L, cost=m["cost"]))
+    cat = lambda k: (np.concatenate([p[k] for p in parts]) if parts else np.zeros(0))
+    out = {k: cat(k) for k in ("finish_prob", "expected_finish", "expected_latency_ms", "score")}
+    out["sel_n"] = np.array([p["sel_n"] for p in parts], np.int32)
+    out["sel_bs"] = np.array([p["sel_bs"] for p in parts], np.int32)
+    out["sel_score"] = np.array([p["sel_score"] for p in parts])
+    out["per_model"] = parts
+    return out

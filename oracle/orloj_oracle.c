@@ -49,7 +49,13 @@
  *   - the cost of a miss is c = 1 unless per-request costs are given (the
  *     score then sums c_m p_m; finish probabilities are unweighted);
  *   - selection: the largest score; exact ties go to the larger prefix,
- *     then the smaller batch size; no batch when the best score is <= 0.
+ *     then the smaller batch size; no batch when the best score is <= 0;
+ *   - affine mode (Eq. (3)): one histogram per class of the solo latency;
+ *     a batch of size k whose slowest member takes l runs c0 + c1 k l, so
+ *     its CDF at time t is the members' product at (t - c0) / (c1 k) and
+ *     its histogram has the bins of that product stretched by c1 k and
+ *     shifted by c0 (Eq. (9), read with the Jacobian 1 / (c1 k) that the
+ *     printed form leaves out).
  */
 #include <math.h>
 #include <stdint.h>
@@ -139,6 +145,40 @@ static double priority_times_latency(const double *mass, int32_t n_bins, double 
     return acc;
 }
 
+/* Step 8 bookkeeping: the best candidate so far among prefixes no longer
+ * than their batch size, and the final no-batch rule. */
+typedef struct {
+    int have;
+    double score;
+    int64_t n;
+    int32_t bs;
+} best_so_far;
+
+static void best_consider(best_so_far *bt, int64_t n, int32_t bs, double s)
+{
+    if (n <= bs) {
+        if (!bt->have || s > bt->score || (s == bt->score && n > bt->n)) {
+            bt->have = 1;
+            bt->score = s;
+            bt->n = n;
+            bt->bs = bs;
+        }
+    }
+}
+
+static void best_write(const best_so_far *bt, int32_t *sel_n, int32_t *sel_bs, double *sel_score)
+{
+    if (bt->have && bt->score > 0.0) {
+        *sel_n = (int32_t)bt->n;
+        *sel_bs = bt->bs;
+        *sel_score = bt->score;
+    } else {
+        *sel_n = 0;
+        *sel_bs = 0;
+        *sel_score = 0.0;
+    }
+}
+
 /*
  * All candidates of one model.  counts is [n_bs][n_classes][n_bins]; the
  * queue (cls, deadline_ms) is sorted by deadline.  Outputs, in candidate
@@ -197,10 +237,7 @@ int orloj_oracle_score_model(int32_t n_classes, int32_t n_bins, int32_t n_bs,
         }
 
     int64_t cand = 0, slot = 0;
-    int have_best = 0;
-    double best = 0.0;
-    int64_t best_n = 0;
-    int32_t best_bs = 0;
+    best_so_far best = {0, 0.0, 0, 0};
     for (int32_t bi = 0; bi < n_bs; ++bi) {
         int64_t cap = prefix_mode ? n_queue
                                   : (n_queue < batch_sizes[bi] ? n_queue : batch_sizes[bi]);
@@ -237,26 +274,10 @@ int orloj_oracle_score_model(int32_t n_classes, int32_t n_bins, int32_t n_bs,
             score[cand] = s;
             ++cand;
 
-            /* Step 8. */
-            if (n <= batch_sizes[bi]) {
-                if (!have_best || s > best || (s == best && n > best_n)) {
-                    have_best = 1;
-                    best = s;
-                    best_n = n;
-                    best_bs = batch_sizes[bi];
-                }
-            }
+            best_consider(&best, n, batch_sizes[bi], s);             /* step 8 */
         }
     }
-    if (have_best && best > 0.0) {
-        *sel_n = (int32_t)best_n;
-        *sel_bs = best_bs;
-        *sel_score = best;
-    } else {
-        *sel_n = 0;
-        *sel_bs = 0;
-        *sel_score = 0.0;
-    }
+    best_write(&best, sel_n, sel_bs, sel_score);
     free(F); free(G); free(mass);
     return ORACLE_OK;
 }
@@ -509,5 +530,109 @@ int orloj_oracle_accumulate(int32_t n_models, int32_t n_bs, int32_t n_classes, i
         counts[at] += 1u;
     }
     *n_rejected = rejected;
+    return ORACLE_OK;
+}
+
+/*
+ * Affine batch-latency mode (§4.2.1 Eq. (3), (5); §4.2.2 Eq. (9)): a batch
+ * of batch size s whose slowest member takes l runs for c0 + c1 s l, with
+ * model constants c0 (ms) and c1, and one histogram per class of the
+ * latency of a request run alone (counts is [n_classes][n_bins], no
+ * batch-size dimension).  For candidate (n, s):
+ *   X = max of the members' solo latencies, CDF G on the base grid as in
+ *       step 3 (the product of the members' CDFs);
+ *   L_B = c0 + c1 s X, so its histogram has the bins of X mapped to
+ *       [c0 + c1 s i w, c0 + c1 s (i+1) w) with the same masses;
+ *   E[L_B] = c0 + c1 s E[X]                                     (Eq. (5));
+ *   P_m = P(L_B <= tau_m), and the priority is Eq. (2) on L_B's histogram:
+ *       both are the base-grid routines with the bin width c1 s w and the
+ *       time left tau_m - c0.
+ * Outputs, candidate order and selection are those of
+ * orloj_oracle_score_model.
+ */
+int orloj_oracle_score_model_affine(int32_t n_classes, int32_t n_bins, int32_t n_bs,
+                                    const int32_t *batch_sizes, double bin_width_ms,
+                                    const uint32_t *counts, double c0_ms, double c1,
+                                    int64_t n_queue, const int32_t *cls,
+                                    const double *deadline_ms, const double *cost,
+                                    double now_ms, double b_expo, int32_t prefix_mode,
+                                    double *finish_prob, double *priority,
+                                    double *expected_finish, double *expected_latency_ms,
+                                    double *score, int32_t *sel_n, int32_t *sel_bs,
+                                    double *sel_score)
+{
+    const int32_t C = n_classes, K = n_bins;
+    const double w = bin_width_ms, b = b_expo;
+    if (C < 1 || K < 1 || n_bs < 1 || !batch_sizes || !counts || n_queue < 0 ||
+        !(w > 0.0) || !(b > 0.0) || !(c0_ms >= 0.0 && c0_ms < INFINITY) ||
+        !(c1 > 0.0 && c1 < INFINITY) || (prefix_mode != 0 && prefix_mode != 1) ||
+        !sel_n || !sel_bs || !sel_score)
+        return ORACLE_E_INVALID;
+    if (n_queue > 0 && (!cls || !deadline_ms))
+        return ORACLE_E_INVALID;
+    for (int32_t i = 0; i < n_bs; ++i)
+        if (batch_sizes[i] < 1 || (i > 0 && batch_sizes[i] <= batch_sizes[i - 1]))
+            return ORACLE_E_INVALID;
+    for (int64_t i = 0; i < n_queue; ++i) {
+        if (cls[i] < 0 || cls[i] >= C || isnan(deadline_ms[i]))
+            return ORACLE_E_DATA;
+        if (i > 0 && deadline_ms[i] < deadline_ms[i - 1])
+            return ORACLE_E_DATA;
+        if (cost && !(cost[i] >= 0.0 && cost[i] < INFINITY))
+            return ORACLE_E_DATA;
+    }
+    size_t row = (size_t)K + 1;
+    double *F = (double *)malloc(sizeof(double) * row * (size_t)C);
+    double *G = (double *)malloc(sizeof(double) * row);
+    double *hist = (double *)malloc(sizeof(double) * (size_t)K);
+    if (!F || !G || !hist) {
+        free(F); free(G); free(hist);
+        return ORACLE_E_NOMEM;
+    }
+    for (int32_t c = 0; c < C; ++c)
+        if (orloj_oracle_cdf(K, counts + (size_t)c * (size_t)K, F + (size_t)c * row)) {
+            free(F); free(G); free(hist);
+            return ORACLE_E_DATA;
+        }
+    int64_t cand = 0, slot = 0;
+    best_so_far best = {0, 0.0, 0, 0};
+    for (int32_t bi = 0; bi < n_bs; ++bi) {
+        const double ws = c1 * (double)batch_sizes[bi] * w;     /* bin width of L_B */
+        int64_t cap = prefix_mode ? n_queue
+                                  : (n_queue < batch_sizes[bi] ? n_queue : batch_sizes[bi]);
+        for (int32_t k = 0; k <= K; ++k)
+            G[k] = 1.0;
+        for (int64_t n = 1; n <= cap; ++n) {
+            const double *Fn = F + (size_t)cls[n - 1] * row;
+            for (int32_t k = 0; k <= K; ++k)
+                G[k] = G[k] * Fn[k];
+            double ex = 0.0;                                    /* E[X], Eq. (5) */
+            for (int32_t k = 0; k < K; ++k)
+                ex += 1.0 - 0.5 * (G[k] + G[k + 1]);
+            ex *= w;
+            const double el = c0_ms + c1 * (double)batch_sizes[bi] * ex;
+            for (int32_t k = 0; k < K; ++k)
+                hist[k] = G[k + 1] - G[k];
+            double e_count = 0.0, sc = 0.0;
+            for (int64_t m = 1; m <= n; ++m) {
+                double tau = deadline_ms[m - 1] - now_ms;
+                double P = tau > 0.0 ? finish_probability(G, K, ws, tau - c0_ms) : 0.0;
+                double p = tau > 0.0 ? priority_times_latency(hist, K, ws, tau - c0_ms, b) / el : 0.0;
+                finish_prob[slot] = P;
+                if (priority)
+                    priority[slot] = p;
+                ++slot;
+                e_count += P;
+                sc += (cost ? cost[m - 1] : 1.0) * p;
+            }
+            expected_finish[cand] = e_count;
+            expected_latency_ms[cand] = el;
+            score[cand] = sc;
+            ++cand;
+            best_consider(&best, n, batch_sizes[bi], sc);
+        }
+    }
+    best_write(&best, sel_n, sel_bs, sel_score);
+    free(F); free(G); free(hist);
     return ORACLE_OK;
 }

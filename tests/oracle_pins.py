@@ -777,8 +777,125 @@ def pin_accumulate(L):
                 assert np.array_equal(counts[q, b_, c].astype(np.int64) - before[q, b_, c], h), (q, b_, c)
 
 
+# ------------------------------------------------------------- affine mode
+def _affine(L, rows, bs, w, c0, c1, cls, taus, b=0.05, now=1000.0, cost=None):
+    return oracle.score_model_affine(rows, bs, w, c0, c1, cls, now + np.asarray(taus, np.float64),
+                                     now, b, want_priority=True, L=L, cost=cost)
+
+
+def pin_affine_reduces(L):
+    """Eq. (3) with c0 = 0 and c1 k = 1 is the tabulated mode on the same
+    table, bit for bit (the setting of the toy example in §4.2.2); and for
+    a single member at batch size s with c0 = 0, c1 = 1, L_B = s l has the
+    table of l stretched s times: each bin split into s equal sub-bins of
+    the base width (a brute-force restatement of Eq. (9) for one member)."""
+    r = rng(81)
+    K, C, n = 24, 3, 5
+    rows = r.integers(0, 30, size=(C, K))
+    rows[rows.sum(axis=1) == 0, -1] = 1
+    cls = r.integers(0, C, size=n)
+    taus = np.sort(r.uniform(0.5, 40.0, size=n))
+    w = 1.25
+    for bs, c1 in (([1], 1.0), ([2], 0.5), ([4], 0.25)):
+        aff = _affine(L, rows, bs, w, 0.0, c1, cls, taus)
+        tab = run_model(L, rows, cls, taus, w, b=0.05, batch_sizes=bs)
+        for k in ("finish_prob", "priority", "expected_finish", "expected_latency_ms", "score"):
+            assert np.array_equal(aff[k], tab[k]), (bs, k)
+        assert (aff["sel_n"], aff["sel_bs"]) == (tab["sel_n"], tab["sel_bs"])
+    bs = [1, 2, 3]
+    aff = _affine(L, rows, bs, w, 0.0, 1.0, cls, taus)
+    Kf = K * bs[-1]
+    per = np.zeros((len(bs), C, Kf), np.int64)
+    for bi, s in enumerate(bs):
+        per[bi, :, :s * K] = np.repeat(rows, s, axis=1)     # sub-bin j of bin j // s
+    tab = run_model(L, None, cls, taus, w, b=0.05, batch_sizes=bs, per_bs_rows=per)
+    ai = ti = 0
+    for s in bs:                                             # n = 1 of every batch size
+        for k in ("expected_latency_ms", "score"):
+            assert math.isclose(aff[k][ai], tab[k][ai], rel_tol=1e-12, abs_tol=1e-15), (s, k)
+        assert math.isclose(aff["finish_prob"][ti], tab["finish_prob"][ti], rel_tol=1e-12,
+                            abs_tol=1e-15), s
+        ai += s
+        ti += s * (s + 1) // 2
+
+
+def pin_affine_shift(L):
+    """Eq. (3)'s overhead c0 delays the whole batch: raising c0 and every
+    deadline by the same amount leaves each finish probability and each
+    E[L_B] p_m (the priority before its 1/E[L_B] factor) unchanged and adds
+    the amount to E[L_B] (Eq. (5)); a request whose time left is positive
+    but at most c0 cannot finish and has priority 0."""
+    r = rng(82)
+    K, C, n = 30, 4, 6
+    rows = r.integers(0, 20, size=(C, K))
+    rows[rows.sum(axis=1) == 0, -1] = 1
+    cls = r.integers(0, C, size=n)
+    taus = np.sort(r.uniform(1.0, 60.0, size=n))
+    bs, w, c1 = [1, 3, 6], 0.9, 0.4
+    a = _affine(L, rows, bs, w, 0.0, c1, cls, taus)
+    sh = 7.3
+    z = _affine(L, rows, bs, w, sh, c1, cls, taus + sh)
+    assert np.allclose(z["finish_prob"], a["finish_prob"], rtol=1e-12, atol=1e-14)
+    assert np.allclose(z["expected_latency_ms"], a["expected_latency_ms"] + sh, rtol=1e-12, atol=0)
+    assert np.allclose(z["score"] * z["expected_latency_ms"], a["score"] * a["expected_latency_ms"],
+                       rtol=1e-10, atol=1e-14)
+    early = _affine(L, rows, [2], w, 5.0, c1, cls[:2], [2.0, 5.0])
+    assert np.array_equal(early["finish_prob"], np.zeros(3))
+    assert np.array_equal(early["priority"], np.zeros(3))
+
+
+def pin_affine_nodes(L):
+    """At a time left tau = c0 + c1 s w i (a node of the L_B grid) the
+    finish probability of a batch of any size is the exact product of its
+    members' CDFs at bin edge i (max of independent latencies, §4.2.2, with
+    Eq. (3)); beyond the grid it is 1."""
+    r = rng(83)
+    K, C = 16, 3
+    rows = r.integers(0, 12, size=(C, K))
+    rows[rows.sum(axis=1) == 0, 0] = 1
+    w, c0, c1, bs = 2.0, 3.5, 0.75, [4]
+    cls = r.integers(0, C, size=4)
+    edges = np.sort(r.integers(1, K, size=3))
+    taus = [c0 + c1 * 4 * w * float(i) for i in edges] + [c0 + c1 * 4 * w * (K + 2.5)]
+    out = _affine(L, rows, bs, w, c0, c1, cls, taus)
+    for nn in range(1, 5):
+        G = exact_cdf_product(rows[cls[:nn]])
+        for m in range(1, nn + 1):
+            want = 1.0 if m == 4 else float(G[int(edges[m - 1])])
+            got = out["finish_prob"][slot(nn, m)]
+            assert math.isclose(got, want, rel_tol=1e-12, abs_tol=1e-15), (nn, m, got, want)
+
+
+def pin_affine_monte_carlo(L):
+    """Eq. (1) by simulation with L_B = c0 + c1 s max_i l_i (Eq. (3)): draw
+    each member's latency from its histogram (uniform inside a bin), an
+    anticipated delay ~ Exp(b), and count the members that finish in time
+    but not after the delay; its mean matches the score times E[L_B].  The
+    sample mean of L_B matches E[L_B] within the half-bin spread of the
+    uniform-in-bin model."""
+    r = rng(84)
+    K, C, n = 20, 3, 3
+    rows = r.integers(0, 25, size=(C, K))
+    rows[rows.sum(axis=1) == 0, -1] = 1
+    cls = r.integers(0, C, size=n)
+    w, c0, c1, s, b = 1.0, 4.0, 0.3, 5, 0.06
+    taus = np.sort(r.uniform(8.0, 30.0, size=n))
+    out = _affine(L, rows, [s], w, c0, c1, cls, taus, b=b)
+    G = exact_cdf_product(rows[cls])
+    mass = np.array([float(G[k + 1] - G[k]) for k in range(K)])
+    S = 1_000_000
+    lat = c0 + c1 * s * (r.choice(K, size=S, p=mass / mass.sum()) + r.random(S)) * w
+    delay = r.exponential(1.0 / b, size=S)
+    ev = sum(((lat <= taus[m]) & (taus[m] < lat + delay)).mean() for m in range(n))
+    got = out["score"][n - 1] * out["expected_latency_ms"][n - 1]
+    sig = math.sqrt(n * 0.25 / S)
+    assert abs(ev - got) <= 4 * sig, (ev, got, sig)
+    assert abs(lat.mean() - out["expected_latency_ms"][n - 1]) <= 4 * lat.std() / math.sqrt(S)
+
+
 PINS = [pin_enumeration, pin_iid_power, pin_point_mass, pin_quadrature_medium, pin_b_to_zero,
         pin_monte_carlo_max, pin_monte_carlo_priority, pin_ozbey_eq8, pin_invariants,
         pin_continuity, pin_edge_cases, pin_selection, pin_rect_mode, pin_toy_example,
         pin_iterate_one_class, pin_iterate_point_mix, pin_iterate_monte_carlo_mix,
-        pin_iterate_feasibility_and_popbatch, pin_cost_weights, pin_step_costs, pin_accumulate]
+        pin_iterate_feasibility_and_popbatch, pin_cost_weights, pin_step_costs, pin_accumulate,
+        pin_affine_reduces, pin_affine_shift, pin_affine_nodes, pin_affine_monte_carlo]

@@ -50,11 +50,11 @@ MUTANTS = {
     "priority_not_normalised": ("priority_times_latency(mass, K, w, tau, b) / el;",
                                 "priority_times_latency(mass, K, w, tau, b);"),
     # step 8: exact ties to the larger batch size
-    "select_tie_bs": ("(s == best && n > best_n)", "(s == best && n >= best_n)"),
+    "select_tie_bs": ("(s == bt->score && n > bt->n)", "(s == bt->score && n >= bt->n)"),
     # step 8: no-batch rule dropped
-    "select_nonpositive": ("if (have_best && best > 0.0) {", "if (have_best) {"),
+    "select_nonpositive": ("if (bt->have && bt->score > 0.0) {", "if (bt->have) {"),
     # step 8: over-long prefixes allowed
-    "select_rect_mask": ("if (n <= batch_sizes[bi]) {", "if (1) {"),
+    "select_rect_mask": ("if (n <= bs) {", "if (1) {"),
     # Algorithm 1: the request's batch holds s mix members besides it
     "iter_mix_power": ("G[k] = Fr[k] * pow(mix[k], s - 1);", "G[k] = Fr[k] * pow(mix[k], s);"),
     # Algorithm 1: model-wide E[L] of s - 1 mix members
@@ -77,6 +77,20 @@ MUTANTS = {
     # App. B: the drop phase looks at the first step
     "steps_drop_first": ("double last = step_off ? step_deadline_ms[step_off[r + 1] - 1] : deadline_ms[r];\n        double tau = last - now_ms;",
                          "double last = deadline_ms[r];\n        double tau = last - now_ms;"),
+    # Eq. (3): the overhead c0 ignored in the finish probability
+    "affine_p_no_c0": ("finish_probability(G, K, ws, tau - c0_ms)", "finish_probability(G, K, ws, tau)"),
+    # Eq. (3): the priority measured from the batch start, not after c0
+    "affine_priority_no_c0": ("priority_times_latency(hist, K, ws, tau - c0_ms, b)",
+                              "priority_times_latency(hist, K, ws, tau, b)"),
+    # Eq. (9): the L_B grid not stretched by the batch size
+    "affine_width_no_k": ("const double ws = c1 * (double)batch_sizes[bi] * w;",
+                          "const double ws = c1 * w;"),
+    # Eq. (5): c0 dropped from E[L_B]
+    "affine_el_no_c0": ("const double el = c0_ms + c1 * (double)batch_sizes[bi] * ex;",
+                        "const double el = c1 * (double)batch_sizes[bi] * ex;"),
+    # Eq. (5): E[L_B] without the factor k
+    "affine_el_no_k": ("const double el = c0_ms + c1 * (double)batch_sizes[bi] * ex;",
+                       "const double el = c0_ms + c1 * ex;"),
     # profiler: beyond-grid samples dropped instead of counted in the last bin
     "accumulate_clip": ("int32_t k = u >= (double)(n_bins - 1) ? n_bins - 1 : (int32_t)u;",
                         "if (u >= (double)n_bins) { ++rejected; continue; }\n        int32_t k = (int32_t)u;"),
