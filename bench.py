@@ -30,6 +30,8 @@ sys.path.insert(0, ROOT)
 METRIC = ("candidate-batch × histogram-bin evaluations/sec; "
           "scheduling decisions/sec")
 HBM_PEAK_GBS = 8000.0
+# fp64 vector peak: 256 CUs x 64 fp64 FMA lanes per clock x 2 flops x 2.4 GHz
+FP64_VECTOR_PEAK_TFLOPS = 256 * 64 * 2 * 2.4e9 / 1e12
 
 
 def algorithmic_bytes(wl, mode=0):
@@ -97,6 +99,22 @@ def measured_traffic():
     return float(d["traffic_bytes_per_launch"])
 
 
+def affine_algorithmic_flops(wl):
+    """Floating-point operations one affine-mode score launch must do at
+    least: per (model, prefix n, bin) the product update and the E[X] sum
+    (shared by every batch size), per (model, batch size, prefix, bin) the
+    discounted-prefix step at that batch size's rate (one multiply-add)."""
+    K = wl.n_bins
+    per_n = 0
+    per_cand = 0
+    for q in range(wl.n_models):
+        N = wl.queue_len(q)
+        caps = [min(int(s), N) for s in wl.batch_sizes]
+        per_n += max(caps, default=0)
+        per_cand += sum(caps)
+    return 2 * K * per_n + 2 * K * per_cand
+
+
 def valid_candidates(wl):
     return sum(min(int(s), wl.queue_len(q)) for q in range(wl.n_models) for s in wl.batch_sizes)
 
@@ -144,6 +162,49 @@ def oracle_on_states(wl, recorded, budget_s=10.0):
                 cores=1)
 
 
+def bench_affine(wl, ctx, args, torch, O, W):
+    """Time orloj_score_candidates_affine (+ select) on the same queues with
+    one solo-latency table per class and the batch law c0 + c1 s l."""
+    aw = W.affine(wl)
+    sc = O.Scorer(aw, ctx, trim=not args.no_trim)
+    sc.build()
+    ctx.sync()
+    for _ in range(args.warmup):
+        sc.score()
+        sc.select()
+    ctx.sync()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for e0, e1 in evs:
+        e0.record()
+        sc.score()
+        e1.record()
+        sc.select()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ctx.sync()
+    kms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in evs]))
+    ms = wall * 1e3 / args.steps
+    evals = valid_candidates(aw) * aw.n_bins
+    flops = affine_algorithmic_flops(aw)
+    achieved = flops / (kms * 1e-3) / 1e12
+    print(f"[bench] affine: {ms:.4f} ms/step, score kernel {kms:.4f} ms", file=sys.stderr,
+          flush=True)
+    del sc
+    return dict(
+        what="orloj_score_candidates_affine + orloj_select_batch: batch latency c0 + c1 s l "
+             "(one solo-latency table per class), same queues, grid and batch sizes",
+        workload=aw.name, c1=float(aw.c1[0]), ms_per_step=round(ms, 5),
+        evals_per_s=evals / (ms * 1e-3), decisions_per_s=aw.n_models / (ms * 1e-3),
+        table_bytes=int(aw.counts.size * 4),
+        roofline=dict(bound="alu", achieved=round(achieved, 2), peak=round(FP64_VECTOR_PEAK_TFLOPS, 1),
+                      unit="TFLOP/s", frac=round(achieved / FP64_VECTOR_PEAK_TFLOPS, 4),
+                      traffic=None, kernel="score_kernel (affine)", kernel_ms=round(kms, 5),
+                      algorithmic_flops=flops))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -161,6 +222,8 @@ def main():
                     help="skip timing the Algorithm 1 iteration (orloj_iterate) on the same state")
     ap.add_argument("--no-trim", action="store_true",
                     help="score without the table support (every table entry is read)")
+    ap.add_argument("--no-affine", action="store_true",
+                    help="skip timing the affine batch-latency mode on the same state")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after timing, copy a 1 GiB buffer once (a plain copy kernel of "
                          "known size, for scaling HBM traffic counters)")
@@ -259,6 +322,8 @@ def main():
         torch.cuda.synchronize()
         line["calibration_copy_bytes"] = src.numel() * 4
         del src, dst
+    if not args.no_affine:
+        line["affine"] = bench_affine(wl, ctx, args, torch, O, W)
     if not args.no_iterate:
         it = O.Iterator(wl, ctx, counts_device=sc.counts)
         torch.cuda.synchronize()

@@ -10,6 +10,8 @@
  *   orloj_score_candidates  every prefix candidate at every batch size:
  *                           batch CDF, E[L_B], finish probabilities,
  *                           expected finish count, priority score
+ *   orloj_score_candidates_affine  the same with the affine batch-latency
+ *                           law c0 + c1 s l of §4.2.1 (one table per class)
  *   orloj_select_batch      highest-scoring candidate per model
  *   orloj_build_model_laws  model-wide batch laws for the scheduler iteration
  *   orloj_iterate           one Algorithm 1 iteration per model (drop phase,
@@ -181,6 +183,34 @@ int orloj_score_candidates(orloj_ctx *ctx, const orloj_grid *grid, const float *
                            const int64_t *d_prob_off, float *d_finish_prob,
                            double *d_expected_finish, float *d_expected_latency_ms,
                            float *d_score);
+
+/*
+ * Affine batch-latency mode (§4.2.1 Eq. (3) and (5), §4.2.2 Eq. (9)): a
+ * batch of size s whose slowest member takes l runs for c0 + c1 s l, with
+ * per-model constants c0 = d_c0_ms[q] (ms, finite, >= 0) and
+ * c1 = d_c1[q] (finite, > 0), so one latency histogram per class, of a
+ * request run alone, serves every batch size.  d_ccdf is orloj_build_cdfs'
+ * table of those histograms, [M][C][K] (no batch-size dimension), and
+ * d_support (optional) its support, [M][C][2].  For candidate (q, b, n):
+ *   G(x_k)  = prod_i F_{c_i}(x_k) on the base grid (the members' max X);
+ *   L_B     = c0 + c1 s_b X: its histogram holds G's bin masses on bins
+ *             [c0 + c1 s_b k w, c0 + c1 s_b (k+1) w), linear inside a bin
+ *             (Eq. (9) with the Jacobian 1 / (c1 s_b));
+ *   E[L_B]  = c0 + c1 s_b E[X]                                  (Eq. (5));
+ *   P_m, p_m as in orloj_score_candidates on that histogram: the time left
+ *             tau_m - c0 on bins c1 s_b w wide.
+ * Outputs, their layout and every other argument are those of
+ * orloj_score_candidates; orloj_select_batch applies unchanged.  A
+ * negative or non-finite c0, or a c1 that is not finite and > 0, is a data
+ * error (orloj_sync); that model's requests then score as dead.
+ */
+int orloj_score_candidates_affine(orloj_ctx *ctx, const orloj_grid *grid, const float *d_ccdf,
+                                  const int32_t *d_support, const double *d_c0_ms,
+                                  const double *d_c1, const orloj_queues *queues,
+                                  double b_expo_per_ms, int32_t prefix_mode,
+                                  const int64_t *d_cand_off, const int64_t *d_prob_off,
+                                  float *d_finish_prob, double *d_expected_finish,
+                                  float *d_expected_latency_ms, float *d_score);
 
 /*
  * Pick one batch per model (the scheduler pops the top batch, §3.2

@@ -42,6 +42,7 @@ constexpr int kErrNowNaN = 16;
 constexpr int kErrWidth = 32;
 constexpr int kErrWeights = 64;
 constexpr int kErrCost = 128;
+constexpr int kErrAffine = 256;
 
 // ---------------------------------------------------------------------------
 // wave64 helpers
@@ -239,6 +240,8 @@ struct ScoreArgs {
     float* S;
     const int32_t* sup;        // [M][nbs][C][2] first / last bin with mass, or NULL
     const double* cost;        // [N] miss cost per request, or NULL (1)
+    const double* c0;          // affine mode: [M] fixed batch overhead (ms); else NULL
+    const double* c1;          // affine mode: [M] per-member slope; NULL = tabulated mode
     const float* fill;         // [2][16] zeros, ones (the context's stand-in rows)
     int* err;
     double b;
@@ -450,8 +453,23 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     if (cap64 <= 0 || cap64 > maxcap || cap64 > 64 * CR) return;   // the host sizes both
     const int ncap = (int)cap64;
 
-    const double w = a.width[q];
-    const bool wok = w > 0.0 && w < HUGE_VAL;        // else a data error
+    // Affine mode (Eq. (3)): a batch of size s whose slowest member takes l
+    // runs c0 + c1 s l, so its latency histogram is the base grid's with
+    // bins c1 s w wide, shifted by c0.  Everything below works on that
+    // grid: the bin width is c1 s w, the time left is tau - c0, and
+    // E[L_B] = c0 + c1 s E[max] (Eq. (5)).  Tabulated mode: c0 = 0, width w.
+    const bool affine = a.c1 != nullptr;
+    const double wq = a.width[q];
+    double c0q = 0.0;
+    bool aok = true;
+    double w = wq;
+    if (affine) {
+        c0q = a.c0[q];
+        const double c1 = a.c1[q];
+        aok = c0q >= 0.0 && c0q < HUGE_VAL && c1 > 0.0 && c1 < HUGE_VAL;
+        w = c1 * (double)bsz * wq;
+    }
+    const bool wok = wq > 0.0 && wq < HUGE_VAL && aok && w > 0.0 && w < HUGE_VAL;   // else a data error
     const double nowq = a.now[q];
     const double b = a.b;
     const double bw = b * w;
@@ -472,7 +490,8 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         if (isnan(D)) flag |= kErrDeadlineNaN;
         if (m > 0 && D < a.deadline[q0 + m - 1]) flag |= kErrUnsorted;
         if (m == 0 && isnan(nowq)) flag |= kErrNowNaN;
-        if (m == 0 && !wok) flag |= kErrWidth;
+        if (m == 0 && !(wq > 0.0 && wq < HUGE_VAL)) flag |= kErrWidth;
+        if (m == 0 && !aok) flag |= kErrAffine;
         double cm = a.cost ? a.cost[q0 + m] : 1.0;
         if (!(cm >= 0.0 && cm < HUGE_VAL)) { flag |= kErrCost; cm = 0.0; }
         if (flag) atomicOr(a.err, flag);
@@ -483,7 +502,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         mb.cW = mb.cG = mb.cA = mb.fq = 0.0f;
         mb.wq[0] = mb.wq[1] = mb.wq[2] = mb.wq[3] = 0.0f;
         mb.theta = mb.cg = mb.psi = 0.0f;
-        const double tau = D - nowq;
+        const double tau = D - nowq - c0q;
         int kz = -1;   // bin whose discounted prefix Z the priority needs
         if (tau > 0.0 && wok) {
             const double u = tau / w;
@@ -561,13 +580,15 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         cand += c;
         prob += c * (c + 1) / 2;
     }
-    const float* tab_qb = a.tab + ((size_t)q * (size_t)a.nbs + (size_t)bi) * (size_t)a.C * (size_t)K;
+    // rows of this (model, batch size); affine mode has one set per model
+    const size_t qb = affine ? (size_t)q : (size_t)q * (size_t)a.nbs + (size_t)bi;
+    const float* tab_qb = a.tab + qb * (size_t)a.C * (size_t)K;
     wave_lds_fence();
 
     // class and support of member n in lane n % 64 of register n / 64;
     // first member of each panel in lane p
     LaneCarry<CR> cls_r, lo_r, hi_r;
-    const int32_t* sup_qb = a.sup ? a.sup + ((size_t)q * (size_t)a.nbs + (size_t)bi) * (size_t)a.C * 2 : nullptr;
+    const int32_t* sup_qb = a.sup ? a.sup + qb * (size_t)a.C * 2 : nullptr;
 #pragma unroll
     for (int r = 0; r < CR; ++r) {
         const int m = min(r * 64 + lane, ncap - 1);
@@ -776,7 +797,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     for (int r = 0; r < CR; ++r) {
         const int n = r * 64 + lane;
         if (n < ncap) {
-            const double el = w * (0.5 + cE.mine(r));
+            const double el = c0q + w * (0.5 + cE.mine(r));
             a.E[cand + n] = cP.mine(r);
             a.EL[cand + n] = (float)el;
             a.S[cand + n] = (float)((double)cN.mine(r) / el);
@@ -1468,7 +1489,7 @@ int orloj_sync(orloj_ctx* ctx) {
     if (flags) {
         e = hipMemset(ctx->d_err, 0, sizeof(int));
         if (e != hipSuccess) return hip_fail(ctx, e, "clearing the device status word");
-        return fail(ctx, ORLOJ_E_DATA, "device data error:%s%s%s%s%s%s%s%s",
+        return fail(ctx, ORLOJ_E_DATA, "device data error:%s%s%s%s%s%s%s%s%s",
                     (flags & kErrEmptyHistogram) ? " histogram-with-no-samples" : "",
                     (flags & kErrClassRange) ? " class-id-out-of-range" : "",
                     (flags & kErrDeadlineNaN) ? " NaN-deadline" : "",
@@ -1476,7 +1497,8 @@ int orloj_sync(orloj_ctx* ctx) {
                     (flags & kErrNowNaN) ? " NaN-now" : "",
                     (flags & kErrWidth) ? " bin-width-not-positive" : "",
                     (flags & kErrWeights) ? " class-weights-invalid" : "",
-                    (flags & kErrCost) ? " cost-or-steps-invalid" : "");
+                    (flags & kErrCost) ? " cost-or-steps-invalid" : "",
+                    (flags & kErrAffine) ? " affine-constants-invalid" : "");
     }
     return ORLOJ_OK;
 }
@@ -1543,11 +1565,17 @@ int orloj_output_sizes(const orloj_grid* grid, const orloj_queues* queues, int32
     return ORLOJ_OK;
 }
 
-int orloj_score_candidates(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
-                           const int32_t* d_support, const orloj_queues* queues, double b_expo_per_ms, int32_t prefix_mode,
-                           const int64_t* d_cand_off, const int64_t* d_prob_off,
-                           float* d_finish_prob, double* d_expected_finish,
-                           float* d_expected_latency_ms, float* d_score) {
+}  // extern "C"
+
+namespace {
+
+// Validation and launch shared by the tabulated and the affine scorer
+// (d_c0 / d_c1 NULL: tabulated).
+int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
+                 const int32_t* d_support, const double* d_c0, const double* d_c1,
+                 const orloj_queues* queues, double b_expo_per_ms, int32_t prefix_mode,
+                 const int64_t* d_cand_off, const int64_t* d_prob_off, float* d_finish_prob,
+                 double* d_expected_finish, float* d_expected_latency_ms, float* d_score) {
     if (!ctx) return ORLOJ_E_INVALID;
     int rc = check_grid(ctx, grid);
     if (rc) return rc;
@@ -1581,6 +1609,8 @@ int orloj_score_candidates(orloj_ctx* ctx, const orloj_grid* grid, const float* 
     ScoreArgs a;
     a.tab = d_ccdf;
     a.sup = d_support;
+    a.c0 = d_c0;
+    a.c1 = d_c1;
     a.cost = queues->d_cost;
     a.fill = ctx->d_fill;
     a.queue_off = queues->d_queue_off;
@@ -1619,6 +1649,35 @@ int orloj_score_candidates(orloj_ctx* ctx, const orloj_grid* grid, const float* 
     }
     if (e != hipSuccess) return hip_fail(ctx, e, "score_kernel launch");
     return ORLOJ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int orloj_score_candidates(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
+                           const int32_t* d_support, const orloj_queues* queues, double b_expo_per_ms, int32_t prefix_mode,
+                           const int64_t* d_cand_off, const int64_t* d_prob_off,
+                           float* d_finish_prob, double* d_expected_finish,
+                           float* d_expected_latency_ms, float* d_score) {
+    return score_common(ctx, grid, d_ccdf, d_support, nullptr, nullptr, queues, b_expo_per_ms,
+                        prefix_mode, d_cand_off, d_prob_off, d_finish_prob, d_expected_finish,
+                        d_expected_latency_ms, d_score);
+}
+
+int orloj_score_candidates_affine(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
+                                  const int32_t* d_support, const double* d_c0_ms,
+                                  const double* d_c1, const orloj_queues* queues,
+                                  double b_expo_per_ms, int32_t prefix_mode,
+                                  const int64_t* d_cand_off, const int64_t* d_prob_off,
+                                  float* d_finish_prob, double* d_expected_finish,
+                                  float* d_expected_latency_ms, float* d_score) {
+    if (!ctx) return ORLOJ_E_INVALID;
+    if (grid && grid->n_models > 0 && (!d_c0_ms || !d_c1))
+        return fail(ctx, ORLOJ_E_INVALID, "d_c0_ms / d_c1 is NULL");
+    return score_common(ctx, grid, d_ccdf, d_support, d_c0_ms, d_c1, queues, b_expo_per_ms,
+                        prefix_mode, d_cand_off, d_prob_off, d_finish_prob, d_expected_finish,
+                        d_expected_latency_ms, d_score);
 }
 
 int orloj_build_model_laws(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,

@@ -59,7 +59,7 @@ _I64P = ctypes.POINTER(ctypes.c_int64)
 
 EXPORTS = ("orloj_create", "orloj_destroy", "orloj_set_stream", "orloj_last_error", "orloj_sync",
            "orloj_build_cdfs", "orloj_output_sizes", "orloj_score_candidates",
-           "orloj_select_batch", "orloj_build_model_laws", "orloj_iterate", "orloj_accumulate")
+           "orloj_score_candidates_affine", "orloj_select_batch", "orloj_build_model_laws", "orloj_iterate", "orloj_accumulate")
 
 
 def load(path: Optional[str] = None):
@@ -90,6 +90,9 @@ def load(path: Optional[str] = None):
     L.orloj_score_candidates.argtypes = [_VP, _GP, _VP, _VP, _QP, ctypes.c_double, ctypes.c_int32,
                                          _VP, _VP, _VP, _VP, _VP, _VP]
     L.orloj_score_candidates.restype = ctypes.c_int
+    L.orloj_score_candidates_affine.argtypes = [_VP, _GP, _VP, _VP, _VP, _VP, _QP, ctypes.c_double,
+                                                ctypes.c_int32, _VP, _VP, _VP, _VP, _VP, _VP]
+    L.orloj_score_candidates_affine.restype = ctypes.c_int
     L.orloj_select_batch.argtypes = [_VP, _GP, _QP, ctypes.c_int32, _VP, _VP, _VP, _VP, _VP]
     L.orloj_select_batch.restype = ctypes.c_int
     L.orloj_build_model_laws.argtypes = [_VP, _GP, _VP, _VP, ctypes.c_double, _VP, _VP, _VP]
@@ -213,7 +216,9 @@ def output_sizes(grid: Grid, queues: Queues, prefix_mode: int = PREFIX_TRIANGLE)
 class Scorer:
     """A workload resident in HBM plus its output buffers: uploads the
     histograms and queues once, then builds the CDF tables, scores all
-    candidates and selects a batch per model through the C ABI."""
+    candidates and selects a batch per model through the C ABI.  An affine
+    workload (``wl.affine``: counts [M][C][K] and per-model c0, c1) is
+    scored with orloj_score_candidates_affine."""
 
     def __init__(self, wl, ctx: Optional[Context] = None, prefix_mode: int = PREFIX_TRIANGLE,
                  counts_device: Optional[torch.Tensor] = None, trim: bool = True):
@@ -230,6 +235,10 @@ class Scorer:
         self.support = torch.empty(self.counts.shape[:-1] + (2,), dtype=torch.int32, device=dev)
         self.width = torch.from_numpy(np.ascontiguousarray(wl.bin_width_ms, np.float64)).to(dev)
         self.grid = make_grid(wl.n_models, wl.n_classes, wl.n_bins, wl.batch_sizes, self.width)
+        self.affine = bool(getattr(wl, "affine", False))
+        if self.affine:
+            self.c0 = torch.from_numpy(np.ascontiguousarray(wl.c0_ms, np.float64)).to(dev)
+            self.c1 = torch.from_numpy(np.ascontiguousarray(wl.c1, np.float64)).to(dev)
         self.set_queues(wl.queue_off, wl.cls, wl.deadline_ms, wl.now_ms)
         M = wl.n_models
         self.sel_n = torch.zeros(M, dtype=torch.int32, device=dev)
@@ -263,12 +272,17 @@ class Scorer:
     def score(self, b_expo: Optional[float] = None):
         b = self.wl.b_expo if b_expo is None else b_expo
         c = self.ctx
-        c._check(c.L.orloj_score_candidates(
-            c.ctx, ctypes.byref(self.grid), _ptr(self.ccdf),
-            _ptr(self.support) if self.trim else None, ctypes.byref(self.queues),
-            float(b), self.mode, _ptr(self.d_cand_off), _ptr(self.d_prob_off),
-            _ptr(self.finish_prob), _ptr(self.expected_finish), _ptr(self.expected_latency),
-            _ptr(self.score_out)))
+        sup = _ptr(self.support) if self.trim else None
+        outs = (_ptr(self.d_cand_off), _ptr(self.d_prob_off), _ptr(self.finish_prob),
+                _ptr(self.expected_finish), _ptr(self.expected_latency), _ptr(self.score_out))
+        if self.affine:
+            c._check(c.L.orloj_score_candidates_affine(
+                c.ctx, ctypes.byref(self.grid), _ptr(self.ccdf), sup, _ptr(self.c0), _ptr(self.c1),
+                ctypes.byref(self.queues), float(b), self.mode, *outs))
+        else:
+            c._check(c.L.orloj_score_candidates(
+                c.ctx, ctypes.byref(self.grid), _ptr(self.ccdf), sup, ctypes.byref(self.queues),
+                float(b), self.mode, *outs))
 
     def select(self):
         c = self.ctx

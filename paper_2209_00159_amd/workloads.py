@@ -143,6 +143,16 @@ class Workload:
     b_expo: float = DEFAULT_B_EXPO
     description: str = ""
     cost: Optional[np.ndarray] = None  # float64 [N_total] miss cost per request (None: 1)
+    class_p50_ms: Optional[np.ndarray] = None  # float64 [M, C] analytic class medians at batch size 1
+    # Affine batch-latency mode (a batch of size s whose slowest member takes
+    # l runs c0 + c1 s l): counts is then [M, C, K], one solo-latency
+    # histogram per class, and these hold the per-model constants.
+    c0_ms: Optional[np.ndarray] = None  # float64 [M]
+    c1: Optional[np.ndarray] = None     # float64 [M]
+
+    @property
+    def affine(self) -> bool:
+        return self.c1 is not None
 
     @property
     def n_bs(self) -> int:
@@ -181,7 +191,10 @@ class Workload:
             deadline_ms=np.concatenate(dl) if dl else np.zeros(0),
             now_ms=self.now_ms[models].copy(), b_expo=self.b_expo,
             description=self.description,
-            cost=(np.concatenate(co) if co else np.zeros(0)) if self.cost is not None else None)
+            cost=(np.concatenate(co) if co else np.zeros(0)) if self.cost is not None else None,
+            class_p50_ms=None if self.class_p50_ms is None else self.class_p50_ms[models].copy(),
+            c0_ms=None if self.c0_ms is None else self.c0_ms[models].copy(),
+            c1=None if self.c1 is None else self.c1[models].copy())
 
     def with_queues(self, queues: List[tuple], now_ms: np.ndarray) -> "Workload":
         """Same histograms, new queues: ``queues[q] = (cls, deadline_ms)``."""
@@ -287,7 +300,7 @@ def config1(slo_scale: float = 1.0) -> Workload:
     cls, dl = _aged_backlog(rng, 64, C, lambda r, c: slo_scale * r.uniform(50.0, 300.0, size=c.size), now)
     return Workload("cfg1-tiny", 1, 1, C, K, bs, np.array([w]), counts,
                     np.array([0, cls.size], np.int64), cls, dl, np.array([now]),
-                    description=config1.__doc__)
+                    description=config1.__doc__, class_p50_ms=np.exp(mu)[None])
 
 
 def config2(slo_scale: float = 1.0) -> Workload:
@@ -309,7 +322,7 @@ def config2(slo_scale: float = 1.0) -> Workload:
                                min_latency=med)
     return Workload("cfg2-nlp", 2, 1, C, K, bs, np.array([w]), counts,
                     np.array([0, cls.size], np.int64), cls, dl, np.array([now]),
-                    description=config2.__doc__)
+                    description=config2.__doc__, class_p50_ms=med[None])
 
 
 def config3(slo_scale: float = 1.0) -> Workload:
@@ -331,7 +344,7 @@ def config3(slo_scale: float = 1.0) -> Workload:
                             lambda r, c: slo_scale * r.uniform(1.5, 4.0, size=c.size) * p50[c], now)
     return Workload("cfg3-cv", 3, 1, C, K, bs, np.array([w]), counts,
                     np.array([0, cls.size], np.int64), cls, dl, np.array([now]),
-                    description=config3.__doc__)
+                    description=config3.__doc__, class_p50_ms=p50[None])
 
 
 def _mixture_models(config_id, M, C, K, span, bs, med_lo, med_hi, queue_fn,
@@ -343,6 +356,7 @@ def _mixture_models(config_id, M, C, K, span, bs, med_lo, med_hi, queue_fn,
     counts = np.empty((len(models), len(bs), C, K), dtype=np.uint32)
     queues = [None] * len(models)
     nows = np.zeros(len(models))
+    p50s = np.zeros((len(models), C))
 
     def one(i):
         rng = streams[models[i]]
@@ -356,6 +370,7 @@ def _mixture_models(config_id, M, C, K, span, bs, med_lo, med_hi, queue_fn,
         now = 60_000.0 + rng.uniform(0.0, 1.0)
         queues[i] = queue_fn(rng, C, p50, now)
         nows[i] = now
+        p50s[i] = p50
 
     if workers > 1 and len(models) > 1:
         from concurrent.futures import ThreadPoolExecutor
@@ -364,10 +379,10 @@ def _mixture_models(config_id, M, C, K, span, bs, med_lo, med_hi, queue_fn,
     else:
         for i in range(len(models)):
             one(i)
-    return counts, queues, nows, w
+    return counts, queues, nows, w, p50s
 
 
-def _assemble(name, cid, C, K, bs, counts, queues, nows, w, doc):
+def _assemble(name, cid, C, K, bs, counts, queues, nows, w, doc, p50s=None):
     M = counts.shape[0]
     offs = np.zeros(M + 1, dtype=np.int64)
     for q, (c, _) in enumerate(queues):
@@ -375,7 +390,7 @@ def _assemble(name, cid, C, K, bs, counts, queues, nows, w, doc):
     cls = np.concatenate([c for c, _ in queues]).astype(np.int32)
     dl = np.concatenate([d for _, d in queues])
     return Workload(name, cid, M, C, K, bs, np.full(M, w), counts, offs, cls, dl,
-                    nows, description=doc)
+                    nows, description=doc, class_p50_ms=p50s)
 
 
 def config4(models: Optional[Sequence[int]] = None, workers: int = 1,
@@ -391,9 +406,9 @@ def config4(models: Optional[Sequence[int]] = None, workers: int = 1,
         return _poisson_backlog(rng, 2048, 0.5, C_,
                                 lambda r, c: slo_scale * r.uniform(2.0, 5.0, size=c.size) * p50[c],
                                 now, min_latency=p50)
-    counts, queues, nows, w = _mixture_models(4, M, C, K, 1000.0, bs, 20.0, 200.0, qfn, models,
-                                          workers)
-    return _assemble("cfg4-multi", 4, C, K, bs, counts, queues, nows, w, config4.__doc__)
+    counts, queues, nows, w, p50s = _mixture_models(4, M, C, K, 1000.0, bs, 20.0, 200.0, qfn,
+                                                    models, workers)
+    return _assemble("cfg4-multi", 4, C, K, bs, counts, queues, nows, w, config4.__doc__, p50s)
 
 
 CFG5_BACKLOG = 256
@@ -412,9 +427,9 @@ def config5(models: Optional[Sequence[int]] = None, workers: int = 1,
     def qfn(rng, C_, p50, now):
         return _aged_backlog(rng, CFG5_BACKLOG, C_,
                              lambda r, c: slo_scale * r.uniform(1.5, 5.0, size=c.size) * p50[c], now)
-    counts, queues, nows, w = _mixture_models(5, M, C, K, 1000.0, bs, 5.0, 40.0, qfn, models,
-                                          workers)
-    return _assemble("cfg5-stress", 5, C, K, bs, counts, queues, nows, w, config5.__doc__)
+    counts, queues, nows, w, p50s = _mixture_models(5, M, C, K, 1000.0, bs, 5.0, 40.0, qfn,
+                                                    models, workers)
+    return _assemble("cfg5-stress", 5, C, K, bs, counts, queues, nows, w, config5.__doc__, p50s)
 
 
 def config5_p50(models: Optional[Sequence[int]] = None) -> np.ndarray:
@@ -467,6 +482,40 @@ def make(config_id: int, models: Optional[Sequence[int]] = None, workers: int = 
     if slo_scale != 1.0:
         wl.name = f"{wl.name}-slo{slo_scale:g}x"
     return wl
+
+
+# --------------------------------------------------------------------------
+# Affine batch-latency mode inputs
+# --------------------------------------------------------------------------
+AFFINE_C1 = 0.08
+
+
+def affine(wl: Workload, c1: float = AFFINE_C1) -> Workload:
+    """The affine-mode counterpart of a configuration: each class keeps its
+    batch-size-1 histogram as the solo-latency histogram (counts [M, C, K]),
+    and the model's batch law is c0 + c1 s l with c1 = 0.08 and
+    c0 = (1 - c1) x the median of the model's class medians, so that at that
+    median the law gives the configurations' 1 + 0.08 (s - 1) scaling.
+    Queues, grid and batch sizes are unchanged."""
+    if wl.class_p50_ms is None:
+        raise ValueError(f"{wl.name} records no class medians")
+    if wl.affine:
+        return wl
+    m = np.median(np.asarray(wl.class_p50_ms, np.float64), axis=1)
+    return dataclasses.replace(
+        wl, name=f"{wl.name}-affine", counts=np.ascontiguousarray(wl.counts[:, 0]),
+        c0_ms=(1.0 - c1) * m, c1=np.full(wl.n_models, float(c1)))
+
+
+def random_affine(seed: int, c0_range=(0.0, 3.0), c1_range=(0.05, 1.0), **kw) -> Workload:
+    """random_case with one histogram per class (its batch-size-0 table) and
+    per-model constants c0 ~ U[c0_range] ms, c1 ~ U[c1_range]."""
+    wl = random_case(seed, **kw)
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([SEED_ROOT, 98, seed])))
+    M = wl.n_models
+    return dataclasses.replace(
+        wl, name=f"{wl.name}-affine", counts=np.ascontiguousarray(wl.counts[:, 0]),
+        c0_ms=rng.uniform(*c0_range, size=M), c1=rng.uniform(*c1_range, size=M))
 
 
 # --------------------------------------------------------------------------

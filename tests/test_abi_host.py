@@ -82,6 +82,10 @@ def test_null_context_is_rejected_without_touching_the_gpu(lib):
     rc = lib.orloj_select_batch(None, ctypes.byref(g), ctypes.byref(qs), 0, None, None, None,
                                 None, None)
     assert rc == O.ORLOJ_E_INVALID
+    rc = lib.orloj_score_candidates_affine(None, ctypes.byref(g), None, None, None, None,
+                                           ctypes.byref(qs), 1e-4, 0, None, None, None, None,
+                                           None, None)
+    assert rc == O.ORLOJ_E_INVALID
     assert lib.orloj_build_cdfs(None, 1, 4, None, None, None) == O.ORLOJ_E_INVALID
     assert lib.orloj_sync(None) == O.ORLOJ_E_INVALID
     assert lib.orloj_last_error(None)
@@ -100,3 +104,20 @@ def test_workload_shapes():
     assert np.all(np.diff(wl.deadline_ms) >= 0)
     wl = W.random_case(1, n_models=3, queue_lens=[0, 5, 2])
     assert wl.queue_len(0) == 0 and wl.queue_len(1) == 5
+
+
+def test_affine_workloads():
+    wl = W.make(2)
+    aff = W.affine(wl)
+    assert aff.affine and not wl.affine
+    assert aff.counts.shape == (1, 32, 1024)
+    assert np.array_equal(aff.counts[0], wl.counts[0, 0])
+    assert aff.c1[0] == W.AFFINE_C1
+    assert np.isclose(aff.c0_ms[0], (1 - W.AFFINE_C1) * np.median(wl.class_p50_ms[0]))
+    assert np.array_equal(aff.deadline_ms, wl.deadline_ms)
+    r = W.random_affine(3, n_models=4)
+    base = W.random_case(3, n_models=4)
+    assert np.array_equal(r.counts, base.counts[:, 0])
+    assert np.all((r.c0_ms >= 0) & (r.c0_ms <= 3.0)) and np.all((r.c1 >= 0.05) & (r.c1 <= 1.0))
+    sub = r.subset([2, 0])
+    assert np.array_equal(sub.c0_ms, r.c0_ms[[2, 0]]) and np.array_equal(sub.c1, r.c1[[2, 0]])
