@@ -649,6 +649,8 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     // those of step n-1 and the update, its loads and its reductions are
     // skipped.
     bool pass_zero = false;                  // G == 0 on every bin of this pass's panel
+    Member pass_mb;                          // CR == 1: this lane's member of the pass
+    bool pass_valid = false;
     float etot_prev = 0.0f, T_prev = 0.0f, gl_prev = 0.0f;
 
     for (int it0 = 0; it0 < iters; it0 += PF) {
@@ -660,6 +662,12 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
 #pragma unroll
                 for (int j = 0; j < CPL; ++j) Gacc[j] = 1.0;
                 pass_zero = false;
+                if constexpr (CR == 1) {
+                    // at most 64 members: lane l scores member mlo + l of this
+                    // pass at every step, so its plan is read from LDS once
+                    pass_valid = mlo + lane < mend;
+                    pass_mb = s_mem[min(mlo + lane, ncap - 1)];
+                }
             }
             const int p0 = p * PW;                        // first bin of the panel
             const int pbase = p0 + base;                  // first bin of this lane chunk
@@ -741,8 +749,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                         double pP = 0.0;
                         float pN = 0.0f;
                         const int nn = n + 1;
-                        for (int m = mlo + lane; m < mhi; m += 64) {
-                            const Member mb = s_mem[m];
+                        auto score_member = [&](const Member& mb, int m) {
                             const float g0 = s_g[max((int)mb.ig0, 0)];
                             const float g1 = s_g[max((int)mb.ig1, 0)];
                             const float al0 = s_A[max((int)mb.la, 0)];
@@ -769,6 +776,12 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                             a.P[prob + (int64_t)n * nn / 2 + m] = P;
                             pP += (double)P;
                             pN += num;
+                        };
+                        if constexpr (CR == 1) {
+                            // the lane's member of this pass, already in registers
+                            if (pass_valid && mlo + lane < mhi) score_member(pass_mb, mlo + lane);
+                        } else {
+                            for (int m = mlo + lane; m < mhi; m += 64) score_member(s_mem[m], m);
                         }
                         pP = wave_scan_sum64(pP);
                         pN = wave_scan_sum(pN);
