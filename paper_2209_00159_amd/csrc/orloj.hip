@@ -854,16 +854,25 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const SelectArgs a) {
     __shared__ Best s_best[kWaves];
     const int q = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    __shared__ int64_t s_wsum[kWaves];
     const int64_t N = a.queue_off[q + 1] - a.queue_off[q];
-    if (tid == 0) {
-        int64_t acc = 0;
-        for (int bi = 0; bi < a.nbs; ++bi) {
-            s_start[bi] = acc;
-            const int bsz = a.bs[bi];
-            acc += a.rect ? N : (N < bsz ? N : (int64_t)bsz);
-        }
-        s_start[a.nbs] = acc;
+    // block starts: an exclusive scan of the prefix caps over the batch
+    // sizes, kThreads at a time (a workgroup scan of per-wave scans)
+    int64_t carry = 0;
+    for (int b0 = 0; b0 < a.nbs; b0 += kThreads) {
+        const int bi = b0 + tid;
+        const int bsz = bi < a.nbs ? a.bs[bi] : 0;
+        const int64_t cap = bi < a.nbs ? (a.rect ? N : (N < bsz ? N : (int64_t)bsz)) : 0;
+        const int64_t incl = wave_incl_scan_u64((uint64_t)cap, lane);
+        if (lane == 63) s_wsum[wv] = incl;
+        __syncthreads();
+        int64_t before = carry;
+        for (int w = 0; w < wv; ++w) before += s_wsum[w];
+        if (bi < a.nbs) s_start[bi] = before + incl - cap;
+        for (int w = 0; w < kWaves; ++w) carry += s_wsum[w];
+        __syncthreads();
     }
+    if (tid == 0) s_start[a.nbs] = carry;
     __syncthreads();
     const int64_t total = s_start[a.nbs];
     const float* S = a.S + a.cand_off[q];
