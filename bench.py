@@ -82,18 +82,22 @@ def support_table_bytes(wl, mode=0):
     return total * 4
 
 
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "score_kernel_cfg5_traffic.txt")
+TRAFFIC_SUMMARY = {
+    "tabulated": os.path.join(ROOT, "profiles", "score_kernel_cfg5_traffic.txt"),
+    "affine": os.path.join(ROOT, "profiles", "score_kernel_affine_cfg5_traffic.txt"),
+}
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2209_00159_amd", "csrc", "orloj.hip")
 
 
-def measured_traffic():
+def measured_traffic(mode="tabulated"):
     """HBM bytes per score launch from the committed rocprofv3 counter
-    summary, or None when it is missing or was taken on another version of
-    the kernel source."""
+    summary of that mode, or None when it is missing or was taken on
+    another version of the kernel source."""
     from paper_2209_00159_amd import profsum
-    if not os.path.exists(TRAFFIC_SUMMARY):
+    path = TRAFFIC_SUMMARY[mode]
+    if not os.path.exists(path):
         return None
-    d = profsum.read_summary(TRAFFIC_SUMMARY)
+    d = profsum.read_summary(path)
     if d.get("source_sha256") != profsum.source_sha(KERNEL_SOURCE):
         return None
     return float(d["traffic_bytes_per_launch"])
@@ -119,7 +123,7 @@ def valid_candidates(wl):
     return sum(min(int(s), wl.queue_len(q)) for q in range(wl.n_models) for s in wl.batch_sizes)
 
 
-def cpu_baseline(config_id, max_models, budget_s=15.0):
+def cpu_baseline(config_id, max_models, budget_s=15.0, affine=False):
     """The oracle, as it stands, on the workload's models in order until
     about budget_s seconds of host time are spent (one host thread).
     Returns evals/s over that sample."""
@@ -127,11 +131,17 @@ def cpu_baseline(config_id, max_models, budget_s=15.0):
     from paper_2209_00159_amd import workloads as W
 
     wl = W.make(config_id, models=list(range(max_models)) if config_id in (4, 5) else None)
+    if affine:
+        wl = W.affine(wl)
     t0 = time.perf_counter()
     done = 0
     ev = 0
     for q in range(wl.n_models):
-        oracle.score_workload(wl.subset([q]))
+        sub = wl.subset([q])
+        if affine:
+            oracle.score_workload_affine(sub, sub.c0_ms, sub.c1)
+        else:
+            oracle.score_workload(sub)
         done += 1
         ev += sum(min(int(s), wl.queue_len(q)) for s in wl.batch_sizes) * wl.n_bins
         if time.perf_counter() - t0 > budget_s:
@@ -162,6 +172,34 @@ def oracle_on_states(wl, recorded, budget_s=10.0):
                 cores=1)
 
 
+def tabulated_roofline(wl, ab, kms):
+    achieved = ab["total"] / (kms * 1e-3) / 1e9
+    traffic = measured_traffic("tabulated")
+    sup_bytes = ab["total"] - ab["table"] + support_table_bytes(wl)
+    roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                frac=round(achieved / HBM_PEAK_GBS, 4),
+                traffic=None if traffic is None else round(traffic),
+                traffic_unit="bytes/launch",
+                kernel="score_kernel", kernel_ms=round(kms, 5),
+                algorithmic_bytes=ab["total"],
+                support_only_bytes=sup_bytes,
+                support_only_frac=round(sup_bytes / (kms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4))
+    if traffic is not None:
+        roof["traffic_gbs"] = round(traffic / (kms * 1e-3) / 1e9, 1)
+    return roof
+
+
+def affine_roofline(aw, kms):
+    flops = affine_algorithmic_flops(aw)
+    achieved = flops / (kms * 1e-3) / 1e12
+    traffic = measured_traffic("affine")
+    return dict(bound="alu", achieved=round(achieved, 2), peak=round(FP64_VECTOR_PEAK_TFLOPS, 1),
+                unit="TFLOP/s", frac=round(achieved / FP64_VECTOR_PEAK_TFLOPS, 4),
+                traffic=None if traffic is None else round(traffic),
+                traffic_unit="bytes/launch", kernel="score_kernel (affine)",
+                kernel_ms=round(kms, 5), algorithmic_flops=flops)
+
+
 def bench_affine(wl, ctx, args, torch, O, W):
     """Time orloj_score_candidates_affine (+ select) on the same queues with
     one solo-latency table per class and the batch law c0 + c1 s l."""
@@ -188,8 +226,6 @@ def bench_affine(wl, ctx, args, torch, O, W):
     kms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in evs]))
     ms = wall * 1e3 / args.steps
     evals = valid_candidates(aw) * aw.n_bins
-    flops = affine_algorithmic_flops(aw)
-    achieved = flops / (kms * 1e-3) / 1e12
     print(f"[bench] affine: {ms:.4f} ms/step, score kernel {kms:.4f} ms", file=sys.stderr,
           flush=True)
     del sc
@@ -198,11 +234,7 @@ def bench_affine(wl, ctx, args, torch, O, W):
              "(one solo-latency table per class), same queues, grid and batch sizes",
         workload=aw.name, c1=float(aw.c1[0]), ms_per_step=round(ms, 5),
         evals_per_s=evals / (ms * 1e-3), decisions_per_s=aw.n_models / (ms * 1e-3),
-        table_bytes=int(aw.counts.size * 4),
-        roofline=dict(bound="alu", achieved=round(achieved, 2), peak=round(FP64_VECTOR_PEAK_TFLOPS, 1),
-                      unit="TFLOP/s", frac=round(achieved / FP64_VECTOR_PEAK_TFLOPS, 4),
-                      traffic=None, kernel="score_kernel (affine)", kernel_ms=round(kms, 5),
-                      algorithmic_flops=flops))
+        table_bytes=int(aw.counts.size * 4), roofline=affine_roofline(aw, kms))
 
 
 def main():
@@ -224,6 +256,10 @@ def main():
                     help="score without the table support (every table entry is read)")
     ap.add_argument("--no-affine", action="store_true",
                     help="skip timing the affine batch-latency mode on the same state")
+    ap.add_argument("--mode", choices=("tabulated", "affine"), default="tabulated",
+                    help="batch-latency law of the timed step: per-batch-size tables "
+                         "(default) or the affine law c0 + c1 s l (then the affine, iteration "
+                         "and scheduling-loop legs are skipped)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after timing, copy a 1 GiB buffer once (a plain copy kernel of "
                          "known size, for scaling HBM traffic counters)")
@@ -248,9 +284,14 @@ def main():
     wl = W.make(args.config, workers=args.workers)
     print(f"[bench] generated {wl.name} in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
           flush=True)
+    affine = args.mode == "affine"
+    if affine:
+        wl = W.affine(wl)
+        args.no_affine = args.no_iterate = True
+        args.trace_arrivals = 0
     ctx = O.Context(0)
     sc = O.Scorer(wl, ctx, trim=not args.no_trim)
-    ab = algorithmic_bytes(wl)
+    ab = None if affine else algorithmic_bytes(wl)
     K = wl.n_bins
     evals = valid_candidates(wl) * K
 
@@ -287,19 +328,10 @@ def main():
     print(f"[bench] timed {args.steps} steps: {ms_per_step:.4f} ms/step, score kernel "
           f"{score_ms:.4f} ms", file=sys.stderr, flush=True)
 
-    achieved = ab["total"] / (score_ms * 1e-3) / 1e9
-    traffic = measured_traffic()
-    sup_bytes = ab["total"] - ab["table"] + support_table_bytes(wl)
-    roof = dict(bound="hbm", achieved=round(achieved, 1), peak=HBM_PEAK_GBS, unit="GB/s",
-                frac=round(achieved / HBM_PEAK_GBS, 4),
-                traffic=None if traffic is None else round(traffic),
-                traffic_unit="bytes/launch",
-                kernel="score_kernel", kernel_ms=round(score_ms, 5),
-                algorithmic_bytes=ab["total"],
-                support_only_bytes=sup_bytes,
-                support_only_frac=round(sup_bytes / (score_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4))
-    if traffic is not None:
-        roof["traffic_gbs"] = round(traffic / (score_ms * 1e-3) / 1e9, 1)
+    if affine:
+        roof = affine_roofline(wl, score_ms)
+    else:
+        roof = tabulated_roofline(wl, ab, score_ms)
     line = dict(
         metric=METRIC, value=evals / (ms_per_step * 1e-3), unit="evals/s", n_gpus=1,
         steps=args.steps, warmup=args.warmup, ms_per_step=round(ms_per_step, 5),
@@ -308,7 +340,8 @@ def main():
         config=dict(workload=wl.name, models=wl.n_models, classes=wl.n_classes, bins=K,
                     batch_sizes=f"{int(wl.batch_sizes[0])}..{int(wl.batch_sizes[-1])}",
                     candidates=valid_candidates(wl), evals_per_step=evals,
-                    prefix_mode="triangle", b_expo_per_ms=wl.b_expo),
+                    prefix_mode="triangle", b_expo_per_ms=wl.b_expo,
+                    batch_law="affine c0 + c1 s l" if affine else "per-batch-size tables"),
         decisions_per_s=wl.n_models / (ms_per_step * 1e-3),
         build_cdfs_ms=round(build_ms, 4),
         build_cdfs_gbs=round(wl.counts.nbytes * 2 / (build_ms * 1e-3) / 1e9, 1),
@@ -383,7 +416,7 @@ def main():
               f"({d['device_s']:.2f} s on device)", file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = cpu_baseline(args.config, args.cpu_models)
+        line["cpu_baseline"] = cpu_baseline(args.config, args.cpu_models, affine=affine)
         if recorded:
             line["cpu_baseline"]["trace"] = oracle_on_states(wl, recorded, budget_s=10.0)
     print(json.dumps(line), flush=True)

@@ -29,11 +29,23 @@ def test_traffic_summary_is_ignored_for_other_code(tmp_path, monkeypatch):
     summ = tmp_path / "t.txt"
     summ.write_text(f"# comment: not a key\nsource_sha256: {profsum.source_sha(src)}\n"
                     "traffic_bytes_per_launch: 1234\n")
-    monkeypatch.setattr(bench, "TRAFFIC_SUMMARY", str(summ))
+    monkeypatch.setattr(bench, "TRAFFIC_SUMMARY", {"tabulated": str(summ),
+                                                   "affine": str(tmp_path / "missing.txt")})
     monkeypatch.setattr(bench, "KERNEL_SOURCE", str(src))
-    assert bench.measured_traffic() == 1234.0
+    assert bench.measured_traffic("tabulated") == 1234.0
+    assert bench.measured_traffic("affine") is None
     src.write_text("int k2;\n")
-    assert bench.measured_traffic() is None
+    assert bench.measured_traffic("tabulated") is None
+
+
+def test_affine_flops_by_hand():
+    wl = W.random_affine(4, n_models=2, queue_lens=[5, 3], batch_sizes=(1, 4), n_bins=16)
+    # per model: 2 K per prefix length up to the longest prefix, 2 K per candidate
+    want = 0
+    for N in (5, 3):
+        caps = [min(1, N), min(4, N)]
+        want += 2 * 16 * max(caps) + 2 * 16 * sum(caps)
+    assert bench.affine_algorithmic_flops(wl) == want
 
 
 def test_algorithmic_bytes_by_hand():
