@@ -17,6 +17,9 @@
  *   orloj_iterate           one Algorithm 1 iteration per model (drop phase,
  *                           candidate batch size, PopBatch by priority)
  *   orloj_accumulate        profiler feedback into the histograms
+ *   orloj_sched_*           host runtime: per-model deadline queues, drop
+ *                           phase, one score + select round per call
+ *   orloj_simulate_trace    trace-driven worker simulation on that runtime
  *
  * Conventions.  Pointers named d_* are device (HBM) pointers owned by the
  * caller; h_* pointers and the structs are host memory read during the call
@@ -314,6 +317,105 @@ int orloj_accumulate(orloj_ctx *ctx, const orloj_grid *grid, int64_t n_samples,
                      const int32_t *d_model, const int32_t *d_bs_index, const int32_t *d_class,
                      const double *d_latency_ms, uint32_t *d_counts,
                      unsigned long long *d_n_rejected);
+
+/*
+ * Host scheduling runtime around the scorer (§3.1: one worker per model
+ * runs one batch at a time; §3.2 Algorithm 1: drop the requests that can no
+ * longer finish, then pick the next batch).  It keeps one queue of pending
+ * requests per model in deadline order and makes a decision round per call
+ * to orloj_sched_decide: for every idle model it drops the requests that can
+ * no longer finish, stages the model's first s_max requests (s_max = the
+ * largest batch size: no longer prefix is a candidate), uploads every idle
+ * model's queue in one copy from pinned memory, runs orloj_score_candidates
+ * and orloj_select_batch (TRIANGLE prefixes) in one launch each, reads the
+ * selections back and removes the selected members from their queues.
+ *
+ * orloj_sched_create copies the grid (its d_bin_width_ms must stay valid)
+ * and keeps d_ccdf / d_support (orloj_build_cdfs' table of the model's
+ * per-batch-size histograms and its support, NULL = none; both stay owned by
+ * the caller and must outlive the runtime).  h_drop_ms [M][C] (copied): a
+ * request of class c at model q is dropped once its time left
+ * (deadline - now) is <= h_drop_ms[q][c], e.g. the smallest latency its
+ * class can take run alone.  The runtime allocates pinned host and device
+ * buffers for M * s_max requests and the outputs of a full round; it uses
+ * the context's stream and device.  Not thread-safe.
+ *
+ * orloj_sched_admit inserts n requests (model, class, finite deadline) into
+ * their queues; equal deadlines keep admission order.  A bad model, class or
+ * deadline rejects the whole call (ORLOJ_E_INVALID) before any insertion.
+ *
+ * orloj_sched_decide runs one round at time now_ms.  h_idle [M] (NULL = all)
+ * marks the models whose worker is free; the others are neither dropped nor
+ * scored.  Outputs (host): h_sel_n[M], h_sel_bs[M] (0, 0 = no batch);
+ * *h_n_dropped (optional) is incremented by the requests dropped; the
+ * removed members in queue order, model by model, in h_batch_off[M+1],
+ * h_batch_class[], h_batch_deadline[] (optional, room for M * s_max).  The
+ * call returns after the selections are on the host (it synchronises the
+ * context's stream); data errors of the scoring kernels are reported by
+ * the next orloj_sync.
+ *
+ * orloj_sched_queue_length: pending requests of a model (-1 if out of range).
+ */
+typedef struct orloj_sched orloj_sched;
+
+int orloj_sched_create(orloj_sched **out, orloj_ctx *ctx, const orloj_grid *grid,
+                       const float *d_ccdf, const int32_t *d_support, const double *h_drop_ms,
+                       double b_expo_per_ms);
+void orloj_sched_destroy(orloj_sched *s);
+int orloj_sched_admit(orloj_sched *s, int64_t n, const int32_t *h_model, const int32_t *h_class,
+                      const double *h_deadline_ms);
+int orloj_sched_decide(orloj_sched *s, double now_ms, const uint8_t *h_idle, int32_t *h_sel_n,
+                       int32_t *h_sel_bs, int64_t *h_n_dropped, int64_t *h_batch_off,
+                       int32_t *h_batch_class, double *h_batch_deadline);
+int64_t orloj_sched_queue_length(const orloj_sched *s, int32_t model);
+
+/*
+ * Trace-driven run of the runtime: one worker per model, one batch at a time
+ * (§3.1), a decision round every tick_ms of simulated time.  Each tick admits
+ * the trace's arrivals released by then (h_release_ms sorted), and, if some
+ * idle model has pending requests, runs orloj_sched_decide over the idle
+ * models.  A selected batch of batch-size index b keeps its worker busy for
+ * h_bs_scale[b] x the max of its members' latencies, each drawn from its
+ * class's solo-latency histogram h_solo_counts [M][C][K] (a bin with
+ * probability proportional to its count, then uniform inside it, bins
+ * h_bin_width_ms[q] wide) with a splitmix64 stream seeded by `seed`.  A
+ * member finishing at or before its deadline is on time.  The run ends when
+ * the trace is exhausted and every queue is empty, or after max_ticks ticks
+ * (> 0).  Statistics go to *out; rec (optional) records every every-th
+ * decision's state (the scored queue, the time and the selection), up to
+ * `limit` of them, into caller buffers: h_off [limit+1] and h_class /
+ * h_deadline_ms with room for limit * s_max entries.
+ */
+typedef struct orloj_trace {
+    int64_t n;
+    const double *h_release_ms;
+    const int32_t *h_model;
+    const int32_t *h_class;
+    const double *h_deadline_ms;
+} orloj_trace;
+
+typedef struct orloj_sim_stats {
+    int64_t ticks, launches, decisions, dispatched, dropped, on_time, late, arrivals;
+    double sim_ms;      /* simulated time */
+    double wall_s;      /* host wall time of the whole run */
+    double device_s;    /* upload + score + select + download of the rounds */
+} orloj_sim_stats;
+
+typedef struct orloj_sim_record {
+    int32_t every, limit;
+    int32_t n;                                  /* out: states recorded */
+    int32_t *h_model;
+    double *h_now_ms;
+    int32_t *h_sel_n, *h_sel_bs;
+    int64_t *h_off;
+    int32_t *h_class;
+    double *h_deadline_ms;
+} orloj_sim_record;
+
+int orloj_simulate_trace(orloj_sched *s, const orloj_trace *trace, double tick_ms,
+                         const uint32_t *h_solo_counts, const double *h_bin_width_ms,
+                         const double *h_bs_scale, uint64_t seed, int64_t max_ticks,
+                         orloj_sim_record *rec, orloj_sim_stats *out);
 
 #ifdef __cplusplus
 }

@@ -8,7 +8,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRC = os.path.join(HERE, "csrc", "orloj.hip")
+SRCS = [os.path.join(HERE, "csrc", "orloj.hip"), os.path.join(HERE, "csrc", "sched.hip")]
 LIB = os.path.join(HERE, "liborloj.so")
 ARCH = os.environ.get("ORLOJ_OFFLOAD_ARCH", "gfx950")
 
@@ -31,7 +31,7 @@ def hipcc() -> str:
 
 def build(out: str = LIB, extra=()) -> str:
     tmp = out + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, *extra, SRC, "-o", tmp]
+    cmd = [hipcc(), *HIPCC_FLAGS, *extra, *SRCS, "-o", tmp]
     subprocess.run(cmd, check=True)
     os.replace(tmp, out)
     return out

@@ -27,6 +27,7 @@
 #include <new>
 
 #include "../../include/orloj.h"
+#include "orloj_ctx.h"
 
 namespace {
 
@@ -1321,64 +1322,46 @@ __global__ __launch_bounds__(kThreads) void accumulate_kernel(const AccArgs a) {
 
 }  // namespace
 
-struct orloj_ctx {
-    int device;
-    hipStream_t stream;
-    int* d_err;      // device status word (data error bits)
-    float* d_fill;   // kFillFloats stand-in table entries: 16 zeros, 16 ones
-    char msg[512];
-};
-
 namespace {
 
-int fail(orloj_ctx* ctx, int code, const char* fmt, ...) __attribute__((format(printf, 3, 4)));
-int fail(orloj_ctx* ctx, int code, const char* fmt, ...) {
-    if (ctx) {
-        va_list ap;
-        va_start(ap, fmt);
-        vsnprintf(ctx->msg, sizeof ctx->msg, fmt, ap);
-        va_end(ap);
-    }
-    return code;
-}
 
 int hip_fail(orloj_ctx* ctx, hipError_t e, const char* what) {
-    return fail(ctx, ORLOJ_E_HIP, "%s: %s", what, hipGetErrorString(e));
+    return orloj_ctx_fail(ctx, ORLOJ_E_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
 int check_grid(orloj_ctx* ctx, const orloj_grid* g) {
-    if (!g) return fail(ctx, ORLOJ_E_INVALID, "grid is NULL");
-    if (g->n_models < 0) return fail(ctx, ORLOJ_E_INVALID, "n_models < 0");
-    if (g->n_classes < 1) return fail(ctx, ORLOJ_E_INVALID, "n_classes < 1");
-    if (g->n_bins < 1) return fail(ctx, ORLOJ_E_INVALID, "n_bins < 1");
+    if (!g) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "grid is NULL");
+    if (g->n_models < 0) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "n_models < 0");
+    if (g->n_classes < 1) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "n_classes < 1");
+    if (g->n_bins < 1) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "n_bins < 1");
     if (g->n_bins > ORLOJ_MAX_BINS)
-        return fail(ctx, ORLOJ_E_UNSUPPORTED, "n_bins %d > %d", g->n_bins, ORLOJ_MAX_BINS);
-    if (g->n_bs < 1) return fail(ctx, ORLOJ_E_INVALID, "n_bs < 1");
+        return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "n_bins %d > %d", g->n_bins, ORLOJ_MAX_BINS);
+    if (g->n_bs < 1) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "n_bs < 1");
     if (g->n_bs > ORLOJ_MAX_BATCH_SIZES)
-        return fail(ctx, ORLOJ_E_UNSUPPORTED, "n_bs %d > %d", g->n_bs, ORLOJ_MAX_BATCH_SIZES);
-    if (!g->batch_sizes) return fail(ctx, ORLOJ_E_INVALID, "batch_sizes is NULL");
+        return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "n_bs %d > %d", g->n_bs, ORLOJ_MAX_BATCH_SIZES);
+    if (!g->batch_sizes) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "batch_sizes is NULL");
     for (int i = 0; i < g->n_bs; ++i) {
-        if (g->batch_sizes[i] < 1) return fail(ctx, ORLOJ_E_INVALID, "batch size < 1");
+        if (g->batch_sizes[i] < 1) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "batch size < 1");
         if (i > 0 && g->batch_sizes[i] <= g->batch_sizes[i - 1])
-            return fail(ctx, ORLOJ_E_INVALID, "batch sizes not strictly increasing");
+            return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "batch sizes not strictly increasing");
     }
     if (g->n_models > 0 && !g->d_bin_width_ms)
-        return fail(ctx, ORLOJ_E_INVALID, "d_bin_width_ms is NULL");
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "d_bin_width_ms is NULL");
     return ORLOJ_OK;
 }
 
 int check_queues(orloj_ctx* ctx, const orloj_grid* g, const orloj_queues* qs) {
-    if (!qs) return fail(ctx, ORLOJ_E_INVALID, "queues is NULL");
-    if (!qs->h_queue_off) return fail(ctx, ORLOJ_E_INVALID, "h_queue_off is NULL");
-    if (qs->h_queue_off[0] != 0) return fail(ctx, ORLOJ_E_INVALID, "h_queue_off[0] != 0");
+    if (!qs) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "queues is NULL");
+    if (!qs->h_queue_off) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "h_queue_off is NULL");
+    if (qs->h_queue_off[0] != 0) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "h_queue_off[0] != 0");
     for (int q = 0; q < g->n_models; ++q)
         if (qs->h_queue_off[q + 1] < qs->h_queue_off[q])
-            return fail(ctx, ORLOJ_E_INVALID, "h_queue_off decreases at model %d", q);
+            return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "h_queue_off decreases at model %d", q);
     if (g->n_models > 0) {
         if (!qs->d_queue_off || !qs->d_now_ms)
-            return fail(ctx, ORLOJ_E_INVALID, "d_queue_off / d_now_ms is NULL");
+            return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "d_queue_off / d_now_ms is NULL");
         if (qs->h_queue_off[g->n_models] > 0 && (!qs->d_class || !qs->d_deadline_ms))
-            return fail(ctx, ORLOJ_E_INVALID, "d_class / d_deadline_ms is NULL");
+            return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "d_class / d_deadline_ms is NULL");
     }
     return ORLOJ_OK;
 }
@@ -1511,7 +1494,7 @@ int orloj_sync(orloj_ctx* ctx) {
     if (flags) {
         e = hipMemset(ctx->d_err, 0, sizeof(int));
         if (e != hipSuccess) return hip_fail(ctx, e, "clearing the device status word");
-        return fail(ctx, ORLOJ_E_DATA, "device data error:%s%s%s%s%s%s%s%s%s",
+        return orloj_ctx_fail(ctx, ORLOJ_E_DATA, "device data error:%s%s%s%s%s%s%s%s%s",
                     (flags & kErrEmptyHistogram) ? " histogram-with-no-samples" : "",
                     (flags & kErrClassRange) ? " class-id-out-of-range" : "",
                     (flags & kErrDeadlineNaN) ? " NaN-deadline" : "",
@@ -1528,22 +1511,22 @@ int orloj_sync(orloj_ctx* ctx) {
 int orloj_build_cdfs(orloj_ctx* ctx, int64_t n_rows, int32_t n_bins, const uint32_t* d_counts,
                      float* d_ccdf, int32_t* d_support) {
     if (!ctx) return ORLOJ_E_INVALID;
-    if (n_rows < 0) return fail(ctx, ORLOJ_E_INVALID, "n_rows < 0");
-    if (n_bins < 1) return fail(ctx, ORLOJ_E_INVALID, "n_bins < 1");
+    if (n_rows < 0) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "n_rows < 0");
+    if (n_bins < 1) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "n_bins < 1");
     if (n_bins > ORLOJ_MAX_BINS)
-        return fail(ctx, ORLOJ_E_UNSUPPORTED, "n_bins %d > %d", n_bins, ORLOJ_MAX_BINS);
+        return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "n_bins %d > %d", n_bins, ORLOJ_MAX_BINS);
     if (n_rows == 0) return ORLOJ_OK;
-    if (!d_counts || !d_ccdf) return fail(ctx, ORLOJ_E_INVALID, "NULL buffer");
+    if (!d_counts || !d_ccdf) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "NULL buffer");
     const char* cb = (const char*)d_counts;
     const char* ob = (const char*)d_ccdf;
     const size_t bytes = (size_t)n_rows * (size_t)n_bins * 4;
     if (cb < ob + bytes && ob < cb + bytes)
-        return fail(ctx, ORLOJ_E_INVALID, "d_counts and d_ccdf overlap");
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "d_counts and d_ccdf overlap");
     if (d_support) {
         const char* sb = (const char*)d_support;
         const size_t sbytes = (size_t)n_rows * 8;
         if ((sb < ob + bytes && ob < sb + sbytes) || (sb < cb + bytes && cb < sb + sbytes))
-            return fail(ctx, ORLOJ_E_INVALID, "d_support overlaps d_counts or d_ccdf");
+            return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "d_support overlaps d_counts or d_ccdf");
     }
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
@@ -1604,9 +1587,9 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
     rc = check_queues(ctx, grid, queues);
     if (rc) return rc;
     if (prefix_mode != ORLOJ_PREFIX_TRIANGLE && prefix_mode != ORLOJ_PREFIX_RECT)
-        return fail(ctx, ORLOJ_E_INVALID, "prefix_mode %d", prefix_mode);
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "prefix_mode %d", prefix_mode);
     if (!(b_expo_per_ms > 0.0) || !isfinite(b_expo_per_ms))
-        return fail(ctx, ORLOJ_E_INVALID, "b_expo_per_ms must be finite and > 0");
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "b_expo_per_ms must be finite and > 0");
     const int M = grid->n_models;
     if (M == 0) return ORLOJ_OK;
     int64_t maxcap = 0, total = 0;
@@ -1619,14 +1602,14 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
         }
     }
     if (maxcap > ORLOJ_MAX_PREFIX)
-        return fail(ctx, ORLOJ_E_UNSUPPORTED, "prefix of %lld members > %d",
+        return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "prefix of %lld members > %d",
                     (long long)maxcap, ORLOJ_MAX_PREFIX);
     if (total == 0) return ORLOJ_OK;
     if (!d_ccdf || !d_cand_off || !d_prob_off || !d_finish_prob || !d_expected_finish ||
         !d_expected_latency_ms || !d_score)
-        return fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
     const int64_t nblk = (int64_t)M * grid->n_bs;
-    if (nblk > 0x7fffffff) return fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (model, batch size) pairs");
+    if (nblk > 0x7fffffff) return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (model, batch size) pairs");
 
     ScoreArgs a;
     a.tab = d_ccdf;
@@ -1696,7 +1679,7 @@ int orloj_score_candidates_affine(orloj_ctx* ctx, const orloj_grid* grid, const 
                                   float* d_expected_latency_ms, float* d_score) {
     if (!ctx) return ORLOJ_E_INVALID;
     if (grid && grid->n_models > 0 && (!d_c0_ms || !d_c1))
-        return fail(ctx, ORLOJ_E_INVALID, "d_c0_ms / d_c1 is NULL");
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "d_c0_ms / d_c1 is NULL");
     return score_common(ctx, grid, d_ccdf, d_support, d_c0_ms, d_c1, queues, b_expo_per_ms,
                         prefix_mode, d_cand_off, d_prob_off, d_finish_prob, d_expected_finish,
                         d_expected_latency_ms, d_score);
@@ -1709,12 +1692,12 @@ int orloj_build_model_laws(orloj_ctx* ctx, const orloj_grid* grid, const float* 
     int rc = check_grid(ctx, grid);
     if (rc) return rc;
     if (!(b_expo_per_ms > 0.0) || !isfinite(b_expo_per_ms))
-        return fail(ctx, ORLOJ_E_INVALID, "b_expo_per_ms must be finite and > 0");
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "b_expo_per_ms must be finite and > 0");
     if (grid->n_models == 0) return ORLOJ_OK;
     if (!d_ccdf || !d_law || !d_disc || !d_model_el)
-        return fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
     const int64_t nblk = (int64_t)grid->n_models * grid->n_bs;
-    if (nblk > 0x7fffffff) return fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (model, batch size) pairs");
+    if (nblk > 0x7fffffff) return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (model, batch size) pairs");
     LawArgs a;
     a.tab = d_ccdf;
     a.weights = d_class_weights;
@@ -1756,30 +1739,30 @@ int orloj_iterate(orloj_ctx* ctx, const orloj_grid* grid, const int32_t* d_suppo
     rc = check_queues(ctx, grid, queues);
     if (rc) return rc;
     if (!(b_expo_per_ms > 0.0) || !isfinite(b_expo_per_ms))
-        return fail(ctx, ORLOJ_E_INVALID, "b_expo_per_ms must be finite and > 0");
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "b_expo_per_ms must be finite and > 0");
     const int M = grid->n_models;
     if (M == 0) return ORLOJ_OK;
     const int bs_max = grid->batch_sizes[grid->n_bs - 1];
     if (bs_max > kIterMaxBatch)
-        return fail(ctx, ORLOJ_E_UNSUPPORTED, "batch size %d > %d", bs_max, kIterMaxBatch);
+        return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "batch size %d > %d", bs_max, kIterMaxBatch);
     for (int q = 0; q < M; ++q) {
         const int64_t N = queues->h_queue_off[q + 1] - queues->h_queue_off[q];
         if (N > kIterMaxQueue)
-            return fail(ctx, ORLOJ_E_UNSUPPORTED, "queue of model %d holds %lld > %d requests", q,
+            return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "queue of model %d holds %lld > %d requests", q,
                         (long long)N, kIterMaxQueue);
     }
     if (!d_support || !d_law || !d_disc || !d_model_el || !d_cand_bs || !d_batch)
-        return fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
     if (queues->h_queue_off[M] > 0 && (!d_timed_out || !d_score))
-        return fail(ctx, ORLOJ_E_INVALID, "NULL per-request output");
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "NULL per-request output");
     if (steps) {
         const int64_t* so = steps->h_step_off;
         if (!so || !steps->d_step_off || !steps->d_step_deadline_ms || !steps->d_step_cost)
-            return fail(ctx, ORLOJ_E_INVALID, "incomplete orloj_steps");
-        if (so[0] != 0) return fail(ctx, ORLOJ_E_INVALID, "h_step_off[0] != 0");
+            return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "incomplete orloj_steps");
+        if (so[0] != 0) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "h_step_off[0] != 0");
         for (int64_t r = 0; r < queues->h_queue_off[M]; ++r)
             if (so[r + 1] <= so[r])
-                return fail(ctx, ORLOJ_E_INVALID, "request %lld has no cost step", (long long)r);
+                return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "request %lld has no cost step", (long long)r);
     }
     IterArgs a;
     a.sup = d_support;
@@ -1823,10 +1806,10 @@ int orloj_accumulate(orloj_ctx* ctx, const orloj_grid* grid, int64_t n_samples,
     if (!ctx) return ORLOJ_E_INVALID;
     int rc = check_grid(ctx, grid);
     if (rc) return rc;
-    if (n_samples < 0) return fail(ctx, ORLOJ_E_INVALID, "n_samples < 0");
+    if (n_samples < 0) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "n_samples < 0");
     if (n_samples == 0) return ORLOJ_OK;
     if (!d_model || !d_bs_index || !d_class || !d_latency_ms || !d_counts || !grid->d_bin_width_ms)
-        return fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
     AccArgs a;
     a.model = d_model;
     a.bs_index = d_bs_index;
@@ -1859,13 +1842,13 @@ int orloj_select_batch(orloj_ctx* ctx, const orloj_grid* grid, const orloj_queue
     rc = check_queues(ctx, grid, queues);
     if (rc) return rc;
     if (prefix_mode != ORLOJ_PREFIX_TRIANGLE && prefix_mode != ORLOJ_PREFIX_RECT)
-        return fail(ctx, ORLOJ_E_INVALID, "prefix_mode %d", prefix_mode);
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "prefix_mode %d", prefix_mode);
     const int M = grid->n_models;
     if (M == 0) return ORLOJ_OK;
     if (!d_cand_off || !d_sel_n || !d_sel_bs || !d_sel_score)
-        return fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
     const int64_t total = queues->h_queue_off[M];
-    if (total > 0 && !d_score) return fail(ctx, ORLOJ_E_INVALID, "d_score is NULL");
+    if (total > 0 && !d_score) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "d_score is NULL");
     SelectArgs a;
     a.queue_off = queues->d_queue_off;
     a.cand_off = d_cand_off;

@@ -50,6 +50,26 @@ class Steps(ctypes.Structure):
                 ("d_step_deadline_ms", ctypes.c_void_p), ("d_step_cost", ctypes.c_void_p)]
 
 
+class Trace(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int64), ("h_release_ms", ctypes.c_void_p),
+                ("h_model", ctypes.c_void_p), ("h_class", ctypes.c_void_p),
+                ("h_deadline_ms", ctypes.c_void_p)]
+
+
+class SimStats(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_int64) for k in ("ticks", "launches", "decisions", "dispatched",
+                                             "dropped", "on_time", "late", "arrivals")] + \
+               [(k, ctypes.c_double) for k in ("sim_ms", "wall_s", "device_s")]
+
+
+class SimRecord(ctypes.Structure):
+    _fields_ = [("every", ctypes.c_int32), ("limit", ctypes.c_int32), ("n", ctypes.c_int32),
+                ("h_model", ctypes.c_void_p), ("h_now_ms", ctypes.c_void_p),
+                ("h_sel_n", ctypes.c_void_p), ("h_sel_bs", ctypes.c_void_p),
+                ("h_off", ctypes.c_void_p), ("h_class", ctypes.c_void_p),
+                ("h_deadline_ms", ctypes.c_void_p)]
+
+
 _LIB = None
 _VP = ctypes.c_void_p
 _GP = ctypes.POINTER(Grid)
@@ -59,7 +79,10 @@ _I64P = ctypes.POINTER(ctypes.c_int64)
 
 EXPORTS = ("orloj_create", "orloj_destroy", "orloj_set_stream", "orloj_last_error", "orloj_sync",
            "orloj_build_cdfs", "orloj_output_sizes", "orloj_score_candidates",
-           "orloj_score_candidates_affine", "orloj_select_batch", "orloj_build_model_laws", "orloj_iterate", "orloj_accumulate")
+           "orloj_score_candidates_affine", "orloj_select_batch", "orloj_build_model_laws",
+           "orloj_iterate", "orloj_accumulate", "orloj_sched_create", "orloj_sched_destroy",
+           "orloj_sched_admit", "orloj_sched_decide", "orloj_sched_queue_length",
+           "orloj_simulate_trace")
 
 
 def load(path: Optional[str] = None):
@@ -102,6 +125,20 @@ def load(path: Optional[str] = None):
     L.orloj_iterate.restype = ctypes.c_int
     L.orloj_accumulate.argtypes = [_VP, _GP, ctypes.c_int64, _VP, _VP, _VP, _VP, _VP, _VP]
     L.orloj_accumulate.restype = ctypes.c_int
+    L.orloj_sched_create.argtypes = [ctypes.POINTER(_VP), _VP, _GP, _VP, _VP, _VP, ctypes.c_double]
+    L.orloj_sched_create.restype = ctypes.c_int
+    L.orloj_sched_destroy.argtypes = [_VP]
+    L.orloj_sched_destroy.restype = None
+    L.orloj_sched_admit.argtypes = [_VP, ctypes.c_int64, _VP, _VP, _VP]
+    L.orloj_sched_admit.restype = ctypes.c_int
+    L.orloj_sched_decide.argtypes = [_VP, ctypes.c_double, _VP, _VP, _VP, _VP, _VP, _VP, _VP]
+    L.orloj_sched_decide.restype = ctypes.c_int
+    L.orloj_sched_queue_length.argtypes = [_VP, ctypes.c_int32]
+    L.orloj_sched_queue_length.restype = ctypes.c_int64
+    L.orloj_simulate_trace.argtypes = [_VP, ctypes.POINTER(Trace), ctypes.c_double, _VP, _VP, _VP,
+                                       ctypes.c_uint64, ctypes.c_int64, ctypes.POINTER(SimRecord),
+                                       ctypes.POINTER(SimStats)]
+    L.orloj_simulate_trace.restype = ctypes.c_int
     if default:
         _LIB = L
     return L
@@ -413,3 +450,99 @@ def accumulate(ctx: Context, grid: Grid, counts: torch.Tensor, model, bs_index, 
                                       _ptr(cls), _ptr(latency_ms), _ptr(counts), _ptr(rej)))
     ctx.sync()
     return int(rej.item())
+
+
+def _host(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _vp(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+class Sched:
+    """The host scheduling runtime (orloj_sched_*): per-model deadline queues,
+    the drop phase and one score + select round per decide() call.  The
+    tables (ccdf, support) and the grid's bin-width tensor must outlive it."""
+
+    def __init__(self, ctx: Context, grid: Grid, ccdf: torch.Tensor,
+                 support: Optional[torch.Tensor], drop_ms: np.ndarray, b_expo: float):
+        self.ctx = ctx
+        self.grid = grid
+        self._keep = (ccdf, support, grid)
+        self.M = grid.n_models
+        self.smax = int(grid.batch_sizes[grid.n_bs - 1])
+        d = _host(drop_ms, np.float64)
+        if d.shape != (grid.n_models, grid.n_classes):
+            raise ValueError("drop_ms must be [n_models, n_classes]")
+        self.s = ctypes.c_void_p()
+        ctx._check(ctx.L.orloj_sched_create(ctypes.byref(self.s), ctx.ctx, ctypes.byref(grid),
+                                            _ptr(ccdf), _ptr(support), _vp(d), float(b_expo)))
+
+    def __del__(self):
+        finalizing = sys is None or sys.is_finalizing()
+        if getattr(self, "s", None) and self.s.value and not finalizing:
+            self.ctx.L.orloj_sched_destroy(self.s)
+            self.s = None
+
+    def admit(self, model, cls, deadline_ms):
+        m, c, d = _host(model, np.int32), _host(cls, np.int32), _host(deadline_ms, np.float64)
+        if not (m.size == c.size == d.size):
+            raise ValueError("admit: arrays differ in length")
+        self.ctx._check(self.ctx.L.orloj_sched_admit(self.s, m.size, _vp(m), _vp(c), _vp(d)))
+
+    def queue_length(self, model: int) -> int:
+        return int(self.ctx.L.orloj_sched_queue_length(self.s, int(model)))
+
+    def decide(self, now_ms: float, idle=None) -> dict:
+        M = self.M
+        idle_a = None if idle is None else _host(idle, np.uint8)
+        sn = np.zeros(M, np.int32)
+        sb = np.zeros(M, np.int32)
+        dropped = np.zeros(1, np.int64)
+        boff = np.zeros(M + 1, np.int64)
+        bcls = np.zeros(M * self.smax, np.int32)
+        bdl = np.zeros(M * self.smax, np.float64)
+        self.ctx._check(self.ctx.L.orloj_sched_decide(
+            self.s, float(now_ms), None if idle_a is None else _vp(idle_a), _vp(sn), _vp(sb),
+            _vp(dropped), _vp(boff), _vp(bcls), _vp(bdl)))
+        n = int(boff[-1])
+        return dict(sel_n=sn, sel_bs=sb, dropped=int(dropped[0]), batch_off=boff,
+                    batch_class=bcls[:n], batch_deadline_ms=bdl[:n])
+
+    def simulate(self, trace, tick_ms: float, solo_counts: np.ndarray, bin_width_ms, bs_scale,
+                 seed: int = 0, max_ticks: int = 0, record_every: int = 0, record_limit: int = 0):
+        """orloj_simulate_trace over trace = (release_ms, model, class,
+        deadline_ms).  Returns (stats dict, recorded states as a list of
+        (model, now_ms, class[], deadline_ms[], sel_n, sel_bs))."""
+        rel, mod, cls, dl = (_host(trace[0], np.float64), _host(trace[1], np.int32),
+                             _host(trace[2], np.int32), _host(trace[3], np.float64))
+        tr = Trace(rel.size, _vp(rel), _vp(mod), _vp(cls), _vp(dl))
+        counts = _host(solo_counts, np.uint32)
+        if counts.shape != (self.M, self.grid.n_classes, self.grid.n_bins):
+            raise ValueError("solo_counts must be [n_models, n_classes, n_bins]")
+        w = _host(bin_width_ms, np.float64)
+        sc = _host(bs_scale, np.float64)
+        if w.size != self.M or sc.size != self.grid.n_bs:
+            raise ValueError("bin_width_ms must be [n_models] and bs_scale [n_bs]")
+        L = max(int(record_limit), 0) if record_every > 0 else 0
+        bufs = dict(model=np.zeros(max(L, 1), np.int32), now=np.zeros(max(L, 1)),
+                    sn=np.zeros(max(L, 1), np.int32), sb=np.zeros(max(L, 1), np.int32),
+                    off=np.zeros(L + 1, np.int64),
+                    cls=np.zeros(max(L, 1) * self.smax, np.int32),
+                    dl=np.zeros(max(L, 1) * self.smax))
+        rec = SimRecord(int(record_every), L, 0, _vp(bufs["model"]), _vp(bufs["now"]),
+                        _vp(bufs["sn"]), _vp(bufs["sb"]), _vp(bufs["off"]), _vp(bufs["cls"]),
+                        _vp(bufs["dl"]))
+        st = SimStats()
+        self.ctx._check(self.ctx.L.orloj_simulate_trace(
+            self.s, ctypes.byref(tr), float(tick_ms), _vp(counts), _vp(w), _vp(sc), int(seed),
+            int(max_ticks), ctypes.byref(rec) if L > 0 else None, ctypes.byref(st)))
+        stats = {k: getattr(st, k) for k, _ in SimStats._fields_}
+        states = []
+        o = bufs["off"]
+        for r in range(rec.n if L > 0 else 0):
+            a, b = int(o[r]), int(o[r + 1])
+            states.append((int(bufs["model"][r]), float(bufs["now"][r]), bufs["cls"][a:b].copy(),
+                           bufs["dl"][a:b].copy(), int(bufs["sn"][r]), int(bufs["sb"][r])))
+        return stats, states

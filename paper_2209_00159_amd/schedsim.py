@@ -19,8 +19,10 @@ of simulated time) the loop:
      members' latencies (each drawn from its class's batch-size-1
      histogram, scaled by the batch size's scaling factor).
 
-All scoring runs in the HIP library; this module only moves queues between
-host and device and keeps the simulated clock.  A decision is one model's
+All scoring runs in the HIP library.  TraceLoop keeps the queues and the
+clock in Python; NativeTraceLoop runs the same loop in the library's native
+runtime (orloj_sched_* and orloj_simulate_trace), with one pinned upload and
+one download per round and no Python in the loop.  A decision is one model's
 selection with a non-empty batch.  Each decision state (model, queue, time)
 can be recorded so that it can be scored again elsewhere.
 """
@@ -269,6 +271,55 @@ class TraceLoop:
         return self.stats
 
 
+class NativeTraceLoop:
+    """The loop of TraceLoop run by the library's native runtime: the same
+    tick, drop rule (time left at most the smallest latency the class's
+    batch-size-1 histogram holds mass at), scored prefixes, latency model and
+    on-time rule, with latencies drawn by the runtime's own generator."""
+
+    def __init__(self, wl: W.Workload, trace, ctx: Optional[O.Context] = None,
+                 tick_ms: float = 0.5, seed: int = 0, record_every: int = 0,
+                 record_limit: int = 0, tables=None):
+        self.ctx = ctx or O.Context()
+        self.wl = wl
+        self.trace = trace
+        self.tick = float(tick_ms)
+        self.seed = int(seed)
+        self.record_every = int(record_every)
+        self.record_limit = int(record_limit)
+        dev = self.ctx.device
+        M, B, C, K = wl.counts.shape
+        if tables is None:
+            counts = torch.from_numpy(np.ascontiguousarray(wl.counts).view(np.int32)).to(dev)
+            self.ccdf = torch.empty(counts.shape, dtype=torch.float32, device=dev)
+            self.support = torch.empty(counts.shape[:-1] + (2,), dtype=torch.int32, device=dev)
+            self.ctx.build_cdfs(counts, self.ccdf, self.support)
+            del counts
+        else:
+            self.ccdf, self.support = tables
+        self.width = np.asarray(wl.bin_width_ms, np.float64)
+        self.d_width = torch.from_numpy(self.width.copy()).to(dev)
+        self.grid = O.make_grid(M, C, K, wl.batch_sizes, self.d_width)
+        self.solo = np.ascontiguousarray(wl.counts[:, 0])             # [M, C, K]
+        first = np.argmax(self.solo > 0, axis=-1)                      # [M, C]
+        self.drop_ms = first * self.width[:, None]
+        self.sched = O.Sched(self.ctx, self.grid, self.ccdf, self.support, self.drop_ms, wl.b_expo)
+
+    def run(self, max_ticks: int = 0) -> LoopStats:
+        st, states = self.sched.simulate(
+            self.trace, self.tick, self.solo, self.width, W.linear_scale(self.wl.batch_sizes),
+            seed=self.seed, max_ticks=max_ticks, record_every=self.record_every,
+            record_limit=self.record_limit)
+        self.ctx.sync()
+        out = LoopStats(ticks=st["ticks"], launches=st["launches"], decisions=st["decisions"],
+                        dispatched=st["dispatched"], dropped=st["dropped"], on_time=st["on_time"],
+                        late=st["late"], wall_s=st["wall_s"], device_s=st["device_s"],
+                        sim_ms=st["sim_ms"])
+        out.recorded = [Decision(m, t, c, d, sn, sb) for m, t, c, d, sn, sb in states]
+        self.arrivals = st["arrivals"]
+        return out
+
+
 def config5_trace(n_arrivals: int, models=None, rate_per_s: float = 20_000.0):
     """Configuration 5's Poisson trace (SLO U[1.5,5] x class p50).  With
     `models`, the trace of that subset, its rate scaled by the subset's
@@ -278,9 +329,12 @@ def config5_trace(n_arrivals: int, models=None, rate_per_s: float = 20_000.0):
 
 
 def config5_loop(n_arrivals: int, ctx: Optional[O.Context] = None, models=None, workers: int = 16,
-                 rate_per_s: float = 20_000.0, wl: Optional[W.Workload] = None, **kw) -> TraceLoop:
+                 rate_per_s: float = 20_000.0, wl: Optional[W.Workload] = None,
+                 native: bool = False, **kw):
     """Configuration 5's loop: its models' tables (wl, or generated here)
-    and the Poisson trace of n_arrivals at rate_per_s."""
+    and the Poisson trace of n_arrivals at rate_per_s; native=True runs it
+    in the library's runtime."""
     if wl is None:
         wl = W.make(5, models=models, workers=workers)
-    return TraceLoop(wl, config5_trace(n_arrivals, models, rate_per_s), ctx=ctx, **kw)
+    cls = NativeTraceLoop if native else TraceLoop
+    return cls(wl, config5_trace(n_arrivals, models, rate_per_s), ctx=ctx, **kw)

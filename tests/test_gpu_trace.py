@@ -37,3 +37,70 @@ def test_trace_loop_selections_match_oracle():
         sub = wl.subset([dec.model]).with_queues([(dec.cls, dec.deadline_ms)], [dec.now_ms])
         ora = oracle.score_workload(sub)
         parity.check_selection(sub, 0, 0, ora["score"], (dec.sel_n, dec.sel_bs))
+
+
+def test_native_loop_selections_match_oracle():
+    ctx = O.Context()
+    models = list(range(8))
+    say("config 5 native loop: 8 models, 3000 arrivals")
+    loop = S.config5_loop(3000, ctx=ctx, models=models, workers=8, native=True, record_every=3,
+                          record_limit=60)
+    st = loop.run()
+    say("  stats", st.as_dict())
+    assert loop.arrivals == 3000
+    assert st.decisions >= 60 and len(st.recorded) == 60
+    assert st.on_time + st.late == st.dispatched
+    # every arrival was dispatched or dropped: the run ends with empty queues
+    assert st.dispatched + st.dropped == 3000
+    assert all(loop.sched.queue_length(q) == 0 for q in range(8))
+    wl = loop.wl
+    bs = set(int(b) for b in wl.batch_sizes)
+    for dec in st.recorded:
+        assert dec.sel_bs in bs and 1 <= dec.sel_n <= min(dec.sel_bs, dec.cls.size)
+        assert dec.cls.size <= int(wl.batch_sizes[-1])
+        assert np.all(np.diff(dec.deadline_ms) >= 0)
+        # nothing staged could have been dropped
+        assert np.all(dec.deadline_ms - dec.now_ms > loop.drop_ms[dec.model][dec.cls])
+        sub = wl.subset([dec.model]).with_queues([(dec.cls, dec.deadline_ms)], [dec.now_ms])
+        ora = oracle.score_workload(sub)
+        parity.check_selection(sub, 0, 0, ora["score"], (dec.sel_n, dec.sel_bs))
+
+
+def test_native_runtime_rounds():
+    """admit / decide by hand: the round drops what cannot finish, scores the
+    first s_max requests, and pops exactly the selected prefix."""
+    from paper_2209_00159_amd import workloads as W
+    ctx = O.Context()
+    wl = W.make(1, slo_scale=4.0)
+    loop = S.NativeTraceLoop(wl, (np.zeros(0), np.zeros(0, np.int32), np.zeros(0, np.int32),
+                                  np.zeros(0)), ctx=ctx)
+    sched = loop.sched
+    now = float(wl.now_ms[0])
+    cls, dl = wl.cls, wl.deadline_ms
+    # admit in reverse order: the runtime restores deadline order
+    sched.admit(np.zeros(cls.size, np.int32), cls[::-1], dl[::-1])
+    assert sched.queue_length(0) == cls.size
+    keep = dl - now > loop.drop_ms[0][cls]
+    # the scored queue: the first s_max kept requests in deadline order
+    order = np.argsort(dl, kind="stable")
+    k_cls, k_dl = cls[order][keep[order]], dl[order][keep[order]]
+    smax = int(wl.batch_sizes[-1])
+    sub = wl.with_queues([(k_cls[:smax], k_dl[:smax])], [now])
+    ora = oracle.score_workload(sub)
+    r = sched.decide(now)
+    say("  round", r["sel_n"], r["sel_bs"], "dropped", r["dropped"])
+    assert r["dropped"] == int((~keep).sum())
+    parity.check_selection(sub, 0, 0, ora["score"], (int(r["sel_n"][0]), int(r["sel_bs"][0])))
+    n = int(r["sel_n"][0])
+    assert np.array_equal(r["batch_class"], k_cls[:n])
+    assert np.array_equal(r["batch_deadline_ms"], k_dl[:n])
+    assert sched.queue_length(0) == k_cls.size - n
+    # a busy model is neither dropped nor scored
+    r2 = sched.decide(now + 1e6, idle=np.zeros(1, np.uint8))
+    assert r2["sel_n"][0] == 0 and r2["dropped"] == 0
+    assert sched.queue_length(0) == k_cls.size - n
+    # bad admissions are rejected whole
+    import pytest as _pt
+    with _pt.raises(O.OrlojError):
+        sched.admit([0, 5], [0, 0], [1.0, 2.0])
+    assert sched.queue_length(0) == k_cls.size - n
