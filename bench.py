@@ -123,53 +123,98 @@ def valid_candidates(wl):
     return sum(min(int(s), wl.queue_len(q)) for q in range(wl.n_models) for s in wl.batch_sizes)
 
 
-def cpu_baseline(config_id, max_models, budget_s=15.0, affine=False):
-    """The oracle, as it stands, on the workload's models in order until
-    about budget_s seconds of host time are spent (one host thread).
-    Returns evals/s over that sample."""
+def _oracle_over_models(wl, affine, budget_s, threads):
+    """The oracle on the workload's models, `threads` host threads at a
+    time (the C oracle releases the GIL), each thread taking the next model
+    until about budget_s seconds have passed.  Returns (models, evals, s)."""
+    import threading
+    from concurrent.futures import ThreadPoolExecutor
+
     import oracle
+
+    lock = threading.Lock()
+    state = dict(next=0, done=0, evals=0)
+    t0 = time.perf_counter()
+
+    def worker():
+        while True:
+            with lock:
+                if state["next"] >= wl.n_models or time.perf_counter() - t0 > budget_s:
+                    return
+                q = state["next"]
+                state["next"] += 1
+            sub = wl.subset([q])
+            if affine:
+                oracle.score_workload_affine(sub, sub.c0_ms, sub.c1)
+            else:
+                oracle.score_workload(sub)
+            ev = sum(min(int(s), wl.queue_len(q)) for s in wl.batch_sizes) * wl.n_bins
+            with lock:
+                state["done"] += 1
+                state["evals"] += ev
+
+    with ThreadPoolExecutor(threads) as ex:
+        for f in [ex.submit(worker) for _ in range(threads)]:
+            f.result()
+    return state["done"], state["evals"], time.perf_counter() - t0
+
+
+def cpu_baseline(config_id, max_models, budget_s=10.0, affine=False, threads=16):
+    """The oracle, as it stands, on the models of the same state: once on
+    one host thread and once on `threads` host threads (the GPU machine's CPU
+    share), each for about budget_s seconds.  value = the all-threads
+    evals/s; the one-thread figure is kept beside it."""
     from paper_2209_00159_amd import workloads as W
 
-    wl = W.make(config_id, models=list(range(max_models)) if config_id in (4, 5) else None)
+    wl = W.make(config_id, models=list(range(max_models)) if config_id in (4, 5) else None,
+                workers=threads)
     if affine:
         wl = W.affine(wl)
-    t0 = time.perf_counter()
-    done = 0
-    ev = 0
-    for q in range(wl.n_models):
-        sub = wl.subset([q])
-        if affine:
-            oracle.score_workload_affine(sub, sub.c0_ms, sub.c1)
-        else:
-            oracle.score_workload(sub)
-        done += 1
-        ev += sum(min(int(s), wl.queue_len(q)) for s in wl.batch_sizes) * wl.n_bins
-        if time.perf_counter() - t0 > budget_s:
-            break
-    dt = time.perf_counter() - t0
-    return dict(value=ev / dt, unit="evals/s", cores=1, kind="oracle",
-                sample=f"{wl.name}: first {done} model(s) of the same state, full triangles, "
-                       f"fp64 C oracle, {dt:.1f} s on one host thread",
-                seconds=dt, decisions_per_s=done / dt)
+    d1, e1, t1 = _oracle_over_models(wl, affine, budget_s, 1)
+    dn, en, tn = _oracle_over_models(wl, affine, budget_s, threads)
+    whole = dn == wl.n_models
+    return dict(value=en / tn, unit="evals/s", cores=threads, kind="oracle",
+                sample=(f"{wl.name}: {'all ' if whole else 'the first '}{dn} model(s) of the same "
+                        f"state, full triangles, fp64 C oracle, {tn:.1f} s on {threads} host "
+                        f"threads (one model per thread at a time)"),
+                seconds=round(tn, 2), decisions_per_s=dn / tn,
+                single_thread=dict(value=e1 / t1, unit="evals/s", cores=1, models=d1,
+                                   seconds=round(t1, 2), decisions_per_s=d1 / t1))
 
 
-def oracle_on_states(wl, recorded, budget_s=10.0):
-    """The oracle on decision states recorded by the scheduling loop, in
-    order, for about budget_s seconds: decisions/s, and how many of its
-    selections equal the GPU's."""
+def oracle_on_states(wl, recorded, budget_s=10.0, threads=16):
+    """The oracle on decision states recorded by the scheduling loop, on
+    `threads` host threads, for about budget_s seconds: decisions/s, and how
+    many of its selections equal the GPU's."""
+    import threading
+    from concurrent.futures import ThreadPoolExecutor
+
     import oracle
+
+    lock = threading.Lock()
+    state = dict(next=0, done=0, same=0)
     t0 = time.perf_counter()
-    done = same = 0
-    for dec in recorded:
-        sub = wl.subset([dec.model]).with_queues([(dec.cls, dec.deadline_ms)], [dec.now_ms])
-        o = oracle.score_workload(sub)
-        done += 1
-        same += int((int(o["sel_n"][0]), int(o["sel_bs"][0])) == (dec.sel_n, dec.sel_bs))
-        if time.perf_counter() - t0 > budget_s:
-            break
+
+    def worker():
+        while True:
+            with lock:
+                if state["next"] >= len(recorded) or time.perf_counter() - t0 > budget_s:
+                    return
+                dec = recorded[state["next"]]
+                state["next"] += 1
+            sub = wl.subset([dec.model]).with_queues([(dec.cls, dec.deadline_ms)], [dec.now_ms])
+            o = oracle.score_workload(sub)
+            same = int((int(o["sel_n"][0]), int(o["sel_bs"][0])) == (dec.sel_n, dec.sel_bs))
+            with lock:
+                state["done"] += 1
+                state["same"] += same
+
+    with ThreadPoolExecutor(threads) as ex:
+        for f in [ex.submit(worker) for _ in range(threads)]:
+            f.result()
     dt = time.perf_counter() - t0
-    return dict(decisions_per_s=done / dt, states=done, same_selection=same, seconds=round(dt, 2),
-                cores=1)
+    return dict(decisions_per_s=state["done"] / dt, states=state["done"],
+                same_selection=state["same"], seconds=round(dt, 2), cores=threads)
 
 
 def tabulated_roofline(wl, ab, kms):
@@ -244,7 +289,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=5)
     ap.add_argument("--cpu-models", type=int, default=128,
-                    help="most models the CPU oracle sample may take (it stops after ~15 s)")
+                    help="most models the CPU oracle sample may take (each leg stops after ~10 s)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workers", type=int, default=16)
     ap.add_argument("--trace-arrivals", type=int, default=1_000_000,
@@ -417,9 +462,11 @@ def main():
               f"({d['device_s']:.2f} s on device)", file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = cpu_baseline(args.config, args.cpu_models, affine=affine)
+        line["cpu_baseline"] = cpu_baseline(args.config, args.cpu_models, affine=affine,
+                                            threads=args.workers)
         if recorded:
-            line["cpu_baseline"]["trace"] = oracle_on_states(wl, recorded, budget_s=10.0)
+            line["cpu_baseline"]["trace"] = oracle_on_states(wl, recorded, budget_s=10.0,
+                                                             threads=args.workers)
     print(json.dumps(line), flush=True)
 
 
