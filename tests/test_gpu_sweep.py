@@ -19,7 +19,7 @@ from paper_2209_00159_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
 
-SETTINGS = dict(max_examples=40, deadline=None, derandomize=True, database=None,
+SETTINGS = dict(max_examples=80, deadline=None, derandomize=True, database=None,
                 suppress_health_check=[HealthCheck.too_slow, HealthCheck.function_scoped_fixture])
 
 
