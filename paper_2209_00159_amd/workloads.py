@@ -144,6 +144,7 @@ class Workload:
     description: str = ""
     cost: Optional[np.ndarray] = None  # float64 [N_total] miss cost per request (None: 1)
     class_p50_ms: Optional[np.ndarray] = None  # float64 [M, C] analytic class medians at batch size 1
+    bs_scale: Optional[np.ndarray] = None      # float64 [B] latency scale of each batch size
     # Affine batch-latency mode (a batch of size s whose slowest member takes
     # l runs c0 + c1 s l): counts is then [M, C, K], one solo-latency
     # histogram per class, and these hold the per-model constants.
@@ -193,6 +194,7 @@ class Workload:
             description=self.description,
             cost=(np.concatenate(co) if co else np.zeros(0)) if self.cost is not None else None,
             class_p50_ms=None if self.class_p50_ms is None else self.class_p50_ms[models].copy(),
+            bs_scale=self.bs_scale,
             c0_ms=None if self.c0_ms is None else self.c0_ms[models].copy(),
             c1=None if self.c1 is None else self.c1[models].copy())
 
@@ -300,7 +302,8 @@ def config1(slo_scale: float = 1.0) -> Workload:
     cls, dl = _aged_backlog(rng, 64, C, lambda r, c: slo_scale * r.uniform(50.0, 300.0, size=c.size), now)
     return Workload("cfg1-tiny", 1, 1, C, K, bs, np.array([w]), counts,
                     np.array([0, cls.size], np.int64), cls, dl, np.array([now]),
-                    description=config1.__doc__, class_p50_ms=np.exp(mu)[None])
+                    description=config1.__doc__, class_p50_ms=np.exp(mu)[None],
+                    bs_scale=linear_scale(bs))
 
 
 def config2(slo_scale: float = 1.0) -> Workload:
@@ -322,7 +325,8 @@ def config2(slo_scale: float = 1.0) -> Workload:
                                min_latency=med)
     return Workload("cfg2-nlp", 2, 1, C, K, bs, np.array([w]), counts,
                     np.array([0, cls.size], np.int64), cls, dl, np.array([now]),
-                    description=config2.__doc__, class_p50_ms=med[None])
+                    description=config2.__doc__, class_p50_ms=med[None],
+                    bs_scale=linear_scale(bs))
 
 
 def config3(slo_scale: float = 1.0) -> Workload:
@@ -344,7 +348,8 @@ def config3(slo_scale: float = 1.0) -> Workload:
                             lambda r, c: slo_scale * r.uniform(1.5, 4.0, size=c.size) * p50[c], now)
     return Workload("cfg3-cv", 3, 1, C, K, bs, np.array([w]), counts,
                     np.array([0, cls.size], np.int64), cls, dl, np.array([now]),
-                    description=config3.__doc__, class_p50_ms=p50[None])
+                    description=config3.__doc__, class_p50_ms=p50[None],
+                    bs_scale=np.power(bs.astype(np.float64), 0.6))
 
 
 def _mixture_models(config_id, M, C, K, span, bs, med_lo, med_hi, queue_fn,
@@ -390,7 +395,7 @@ def _assemble(name, cid, C, K, bs, counts, queues, nows, w, doc, p50s=None):
     cls = np.concatenate([c for c, _ in queues]).astype(np.int32)
     dl = np.concatenate([d for _, d in queues])
     return Workload(name, cid, M, C, K, bs, np.full(M, w), counts, offs, cls, dl,
-                    nows, description=doc, class_p50_ms=p50s)
+                    nows, description=doc, class_p50_ms=p50s, bs_scale=linear_scale(bs))
 
 
 def config4(models: Optional[Sequence[int]] = None, workers: int = 1,
@@ -487,24 +492,30 @@ def make(config_id: int, models: Optional[Sequence[int]] = None, workers: int = 
 # --------------------------------------------------------------------------
 # Affine batch-latency mode inputs
 # --------------------------------------------------------------------------
-AFFINE_C1 = 0.08
-
-
-def affine(wl: Workload, c1: float = AFFINE_C1) -> Workload:
+def affine(wl: Workload) -> Workload:
     """The affine-mode counterpart of a configuration: each class keeps its
     batch-size-1 histogram as the solo-latency histogram (counts [M, C, K]),
-    and the model's batch law is c0 + c1 s l with c1 = 0.08 and
-    c0 = (1 - c1) x the median of the model's class medians, so that at that
-    median the law gives the configurations' 1 + 0.08 (s - 1) scaling.
-    Queues, grid and batch sizes are unchanged."""
-    if wl.class_p50_ms is None:
-        raise ValueError(f"{wl.name} records no class medians")
+    and the model's batch law c0 + c1 s l is the secant of the
+    configuration's scaling law scale(s) l between the smallest and the
+    largest batch size, at the model's fastest class median m:
+        c1 = (scale(s_max) - scale(s_min)) / (s_max - s_min),
+        c0 = (scale(s_min) - c1 s_min) m.
+    (For 1 + 0.08 (s - 1): c1 = 0.08, c0 = 0.92 m.)  A fixed overhead above
+    what the fastest class needs would leave the earliest deadlines no
+    chance.  Queues, grid and batch sizes are unchanged."""
+    if wl.class_p50_ms is None or wl.bs_scale is None:
+        raise ValueError(f"{wl.name} records no class medians or scaling law")
     if wl.affine:
         return wl
-    m = np.median(np.asarray(wl.class_p50_ms, np.float64), axis=1)
+    bs = np.asarray(wl.batch_sizes, np.float64)
+    sc = np.asarray(wl.bs_scale, np.float64)
+    c1 = (sc[-1] - sc[0]) / (bs[-1] - bs[0]) if bs.size > 1 else 0.0
+    if not c1 > 0.0:
+        raise ValueError("the scaling law must grow with the batch size")
+    m = np.min(np.asarray(wl.class_p50_ms, np.float64), axis=1)
     return dataclasses.replace(
         wl, name=f"{wl.name}-affine", counts=np.ascontiguousarray(wl.counts[:, 0]),
-        c0_ms=(1.0 - c1) * m, c1=np.full(wl.n_models, float(c1)))
+        c0_ms=(sc[0] - c1 * bs[0]) * m, c1=np.full(wl.n_models, float(c1)))
 
 
 def random_affine(seed: int, c0_range=(0.0, 3.0), c1_range=(0.05, 1.0), **kw) -> Workload:

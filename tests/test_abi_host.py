@@ -112,8 +112,12 @@ def test_affine_workloads():
     assert aff.affine and not wl.affine
     assert aff.counts.shape == (1, 32, 1024)
     assert np.array_equal(aff.counts[0], wl.counts[0, 0])
-    assert aff.c1[0] == W.AFFINE_C1
-    assert np.isclose(aff.c0_ms[0], (1 - W.AFFINE_C1) * np.median(wl.class_p50_ms[0]))
+    # secant of 1 + 0.08 (s - 1) at the fastest class median
+    assert np.isclose(aff.c1[0], 0.08)
+    assert np.isclose(aff.c0_ms[0], 0.92 * np.min(wl.class_p50_ms[0]))
+    a3 = W.affine(W.make(3))
+    assert np.isclose(a3.c1[0], (128 ** 0.6 - 1) / 127)
+    assert np.isclose(a3.c0_ms[0], (1 - a3.c1[0]) * np.min(a3.class_p50_ms[0]))
     assert np.array_equal(aff.deadline_ms, wl.deadline_ms)
     r = W.random_affine(3, n_models=4)
     base = W.random_case(3, n_models=4)

@@ -144,13 +144,15 @@ def test_reduces_to_tabulated_path(ctx):
 
 
 @pytest.mark.parametrize("cid,scale", [(1, 1.0), (1, 4.0), (2, 1.0), (2, 3.0), (3, 1.0),
-                                       (4, 1.0), (4, 3.0)])
+                                       (3, 3.0), (4, 1.0), (4, 3.0)])
 def test_config_full_size(ctx, cid, scale):
     say(f"affine config {cid} slo x{scale}")
     wl = W.affine(W.make(cid, workers=8, slo_scale=scale))
     _, got = run_gpu(wl, ctx)
     err = parity.compare(wl, got, run_oracle(wl))
-    say("  max errors", err)
+    say("  max errors", err, "P > 0:", float((got["finish_prob"] > 0).mean()))
+    if scale > 1.0:     # relaxed SLOs: the comparison is not a trivial one
+        assert int((got["finish_prob"] > 0).sum()) >= 1000 and np.all(got["sel_n"] > 0)
 
 
 def test_config5_full_launch_sampled_models(ctx):
@@ -163,6 +165,8 @@ def test_config5_full_launch_sampled_models(ctx):
     say("  max errors", err)
     P = got["finish_prob"]
     assert np.all((P >= 0) & (P <= 1))
+    # the timed state is not a trivial one: members can finish, models pick batches
+    assert (P > 0).mean() > 0.1 and (got["sel_n"] > 0).mean() > 0.9
     # E[L_B] >= c0 + c1 s w / 2 for every candidate
     for q in range(wl.n_models):
         a, b = sc.h_cand_off[q], sc.h_cand_off[q + 1]
