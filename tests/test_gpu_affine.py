@@ -152,7 +152,8 @@ def test_config_full_size(ctx, cid, scale):
     err = parity.compare(wl, got, run_oracle(wl))
     say("  max errors", err, "P > 0:", float((got["finish_prob"] > 0).mean()))
     if scale > 1.0:     # relaxed SLOs: the comparison is not a trivial one
-        assert int((got["finish_prob"] > 0).sum()) >= 1000 and np.all(got["sel_n"] > 0)
+        P = got["finish_prob"]
+        assert int((P > 0).sum()) >= min(1000, P.size // 2) and np.all(got["sel_n"] > 0)
 
 
 def test_config5_full_launch_sampled_models(ctx):
