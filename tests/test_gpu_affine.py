@@ -144,7 +144,7 @@ def test_reduces_to_tabulated_path(ctx):
 
 
 @pytest.mark.parametrize("cid,scale", [(1, 1.0), (1, 4.0), (2, 1.0), (2, 3.0), (3, 1.0),
-                                       (3, 3.0), (4, 1.0), (4, 3.0)])
+                                       (3, 3.0), (3, 5.0), (4, 1.0), (4, 3.0)])
 def test_config_full_size(ctx, cid, scale):
     say(f"affine config {cid} slo x{scale}")
     wl = W.affine(W.make(cid, workers=8, slo_scale=scale))

@@ -171,8 +171,11 @@ def test_delay_rate_sweep(ctx, b):
     parity.compare(wl, got, ora)
 
 
+# Configuration 3's earliest-deadline prefixes (the first 128 of 4096 aged
+# requests) can hardly finish at its nominal SLOs: x5 gives ~11 000 member
+# slots with 0 < P.
 @pytest.mark.parametrize("cid,scale", [(1, 1.0), (1, 4.0), (2, 1.0), (2, 3.0), (3, 1.0),
-                                       (4, 1.0), (4, 3.0)])
+                                       (3, 5.0), (4, 1.0), (4, 3.0)])
 def test_config_full_size(ctx, cid, scale):
     say(f"config {cid} slo x{scale}")
     wl = W.make(cid, workers=8, slo_scale=scale)
@@ -180,6 +183,9 @@ def test_config_full_size(ctx, cid, scale):
     ora = oracle.score_workload(wl)
     err = parity.compare(wl, got, ora)
     say("  max errors", err)
+    if scale > 1.0:     # relaxed SLOs: the comparison is not a trivial one
+        P = got["finish_prob"]
+        assert int((P > 0).sum()) >= min(1000, P.size // 2) and np.all(got["sel_n"] > 0)
 
 
 @pytest.fixture(scope="module")
@@ -201,6 +207,8 @@ def test_config5_full_launch_sampled_models(ctx, cfg5):
     # properties that hold at any size, over every model
     P = got["finish_prob"]
     assert np.all((P >= 0) & (P <= 1))
+    # the timed state is not a trivial one: members can finish, models pick batches
+    assert (P > 0).mean() > 0.1 and (got["sel_n"] > 0).mean() > 0.9
     assert np.all(got["expected_latency_ms"] >= 0.5 * wl.bin_width_ms[0] * (1 - 1e-6))
     for q in range(wl.n_models):
         E = got["expected_finish"][sc.h_cand_off[q]:sc.h_cand_off[q + 1]]
