@@ -380,7 +380,7 @@ def main():
     line = dict(
         metric=METRIC, value=evals / (ms_per_step * 1e-3), unit="evals/s", n_gpus=1,
         steps=args.steps, warmup=args.warmup, ms_per_step=round(ms_per_step, 5),
-        higher_is_better=True, scaling="weak", vs_baseline=None, dtype="f32",
+        higher_is_better=True, scaling="weak", vs_baseline=None, dtype="f64+f32",
         data="synthetic",
         config=dict(workload=wl.name, models=wl.n_models, classes=wl.n_classes, bins=K,
                     batch_sizes=f"{int(wl.batch_sizes[0])}..{int(wl.batch_sizes[-1])}",
