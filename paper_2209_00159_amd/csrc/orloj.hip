@@ -950,6 +950,48 @@ struct LawArgs {
     int bs[ORLOJ_MAX_BATCH_SIZES];
 };
 
+// One thread's VPT consecutive entries of a table row: F = 1 - t, and 1
+// beyond the row's end.  Whole float4s when the row length is a multiple
+// of 4 (rows and thread chunks are then 16-byte aligned).
+template <int VPT>
+__device__ __forceinline__ void load_cdf_chunk(double (&F)[VPT], const float* __restrict__ t, int base,
+                                               int K) {
+    if constexpr (VPT % 4 == 0) {
+        if ((K & 3) == 0) {
+#pragma unroll
+            for (int j = 0; j < VPT; j += 4) {
+                if (base + j < K) {
+                    const float4 v = *reinterpret_cast<const float4*>(t + base + j);
+                    F[j] = 1.0 - (double)v.x; F[j + 1] = 1.0 - (double)v.y;
+                    F[j + 2] = 1.0 - (double)v.z; F[j + 3] = 1.0 - (double)v.w;
+                } else {
+                    F[j] = F[j + 1] = F[j + 2] = F[j + 3] = 1.0;
+                }
+            }
+            return;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) F[j] = base + j < K ? 1.0 - (double)t[base + j] : 1.0;
+}
+
+// Store one thread's VPT entries (those below K) of a row.
+template <int VPT>
+__device__ __forceinline__ void store_chunk(float* __restrict__ o, const float (&v)[VPT], int base, int K) {
+    if constexpr (VPT % 4 == 0) {
+        if ((K & 3) == 0) {
+#pragma unroll
+            for (int j = 0; j < VPT; j += 4)
+                if (base + j < K)
+                    *reinterpret_cast<float4*>(o + base + j) = make_float4(v[j], v[j + 1], v[j + 2], v[j + 3]);
+            return;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < VPT; ++j)
+        if (base + j < K) o[base + j] = v[j];
+}
+
 template <int VPT>
 __global__ __launch_bounds__(kThreads) void laws_kernel(const LawArgs a) {
     __shared__ float s_wave[kWaves];
@@ -981,13 +1023,10 @@ __global__ __launch_bounds__(kThreads) void laws_kernel(const LawArgs a) {
     }
     for (int c = 0; c < C; ++c) {
         const double pc = (a.weights ? a.weights[(size_t)q * C + c] : 1.0) / wsum;
-        const float* t = a.tab + (row0 + (size_t)c) * (size_t)K;
+        double F[VPT];
+        load_cdf_chunk<VPT>(F, a.tab + (row0 + (size_t)c) * (size_t)K, base, K);
 #pragma unroll
-        for (int j = 0; j < VPT; ++j) {
-            const int k = base + j;
-            const double F = k < K ? 1.0 - (double)t[k] : 1.0;
-            mix[j] = fma(pc, F, mix[j]);
-        }
+        for (int j = 0; j < VPT; ++j) mix[j] = fma(pc, F[j], mix[j]);
     }
     double pm[VPT];
     double el = 0.0;
@@ -1017,14 +1056,12 @@ __global__ __launch_bounds__(kThreads) void laws_kernel(const LawArgs a) {
 
     for (int c = 0; c < C; ++c) {
         const size_t r = (row0 + (size_t)c) * (size_t)K;
-        const float* t = a.tab + r;
         double g[VPT];
+        load_cdf_chunk<VPT>(g, a.tab + r, base, K);
         double z = 0.0;
 #pragma unroll
         for (int j = 0; j < VPT; ++j) {
-            const int k = base + j;
-            const double F = k < K ? 1.0 - (double)t[k] : 1.0;
-            g[j] = F * pm[j];
+            g[j] *= pm[j];
             z = fma(z, d, g[j]);
         }
         // in-wave weighted scan of the chunk totals, then across the waves
@@ -1040,15 +1077,15 @@ __global__ __launch_bounds__(kThreads) void laws_kernel(const LawArgs a) {
         const float prev = __shfl_up(A, 1, 64);
         const float before = (lane > 0 ? prev : 0.0f) + carry * exp2_hw(log2d * (float)(VPT * lane));
         double zz = (double)before;
+        float lv[VPT], dv[VPT];
 #pragma unroll
         for (int j = 0; j < VPT; ++j) {
-            const int k = base + j;
             zz = fma(zz, d, g[j]);
-            if (k < K) {
-                a.law[r + k] = (float)g[j];
-                a.disc[r + k] = (float)zz;
-            }
+            lv[j] = (float)g[j];
+            dv[j] = (float)zz;
         }
+        store_chunk<VPT>(a.law + r, lv, base, K);
+        store_chunk<VPT>(a.disc + r, dv, base, K);
     }
 }
 
