@@ -65,6 +65,7 @@ struct orloj_sched {
     unsigned char* h_stage = nullptr;
     unsigned char* d_stage = nullptr;
     int64_t staged = 0;            // n of the last round
+    std::vector<int32_t> cls_stage;  // classes of a round, before they are packed after the deadlines
 
     float* d_P = nullptr;
     double* d_E = nullptr;
@@ -106,8 +107,8 @@ int decide(orloj_sched* s, double now, const uint8_t* idle, int32_t* sel_n, int3
     off[0] = 0;
     // drop, then stage each idle model's first smax requests: no longer
     // prefix is a candidate at any batch size
-    std::vector<int32_t> cls_tmp;
-    cls_tmp.reserve((size_t)M * s->smax);
+    std::vector<int32_t>& cls_tmp = s->cls_stage;
+    cls_tmp.clear();
     for (int q = 0; q < M; ++q) {
         if (!idle || idle[q]) {
             std::deque<Req>& Q = s->queue[q];
@@ -243,6 +244,7 @@ int orloj_sched_create(orloj_sched** out, orloj_ctx* ctx, const orloj_grid* grid
     s->drop.assign(h_drop_ms, h_drop_ms + (size_t)s->M * s->C);
     s->b = b_expo_per_ms;
     s->queue.resize((size_t)s->M);
+    s->cls_stage.reserve((size_t)s->M * smax);
     const int M = s->M;
     const size_t cap = (size_t)M * smax;
     s->fixed = align8(3 * 8 * (size_t)(M + 1) + 8 * (size_t)M);
