@@ -850,17 +850,22 @@ __device__ __forceinline__ bool better(const Best& x, const Best& y) {
     return x.bs < y.bs;
 }
 
-__global__ __launch_bounds__(kThreads) void select_kernel(const SelectArgs a) {
+// 16 waves per model: the kernel is a chain of latencies (block starts,
+// candidate loads, reductions), so more threads per model shorten it.
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / 64;
+
+__global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a) {
     __shared__ int64_t s_start[ORLOJ_MAX_BATCH_SIZES + 1];
-    __shared__ Best s_best[kWaves];
+    __shared__ Best s_best[kSelWaves];
     const int q = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    __shared__ int64_t s_wsum[kWaves];
+    __shared__ int64_t s_wsum[kSelWaves];
     const int64_t N = a.queue_off[q + 1] - a.queue_off[q];
     // block starts: an exclusive scan of the prefix caps over the batch
-    // sizes, kThreads at a time (a workgroup scan of per-wave scans)
+    // sizes, kSelThreads at a time (a workgroup scan of per-wave scans)
     int64_t carry = 0;
-    for (int b0 = 0; b0 < a.nbs; b0 += kThreads) {
+    for (int b0 = 0; b0 < a.nbs; b0 += kSelThreads) {
         const int bi = b0 + tid;
         const int bsz = bi < a.nbs ? a.bs[bi] : 0;
         const int64_t cap = bi < a.nbs ? (a.rect ? N : (N < bsz ? N : (int64_t)bsz)) : 0;
@@ -870,7 +875,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const SelectArgs a) {
         int64_t before = carry;
         for (int w = 0; w < wv; ++w) before += s_wsum[w];
         if (bi < a.nbs) s_start[bi] = before + incl - cap;
-        for (int w = 0; w < kWaves; ++w) carry += s_wsum[w];
+        for (int w = 0; w < kSelWaves; ++w) carry += s_wsum[w];
         __syncthreads();
     }
     if (tid == 0) s_start[a.nbs] = carry;
@@ -878,7 +883,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const SelectArgs a) {
     const int64_t total = s_start[a.nbs];
     const float* S = a.S + a.cand_off[q];
     Best best{0.0f, 0, 0};
-    for (int64_t i = tid; i < total; i += kThreads) {
+    for (int64_t i = tid; i < total; i += kSelThreads) {
         int lo = 0, hi = a.nbs - 1;          // last bi with s_start[bi] <= i
         while (lo < hi) {
             const int mid = (lo + hi + 1) >> 1;
@@ -903,7 +908,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const SelectArgs a) {
     if (lane == 0) s_best[wv] = best;
     __syncthreads();
     if (tid == 0) {
-        for (int w = 1; w < kWaves; ++w)
+        for (int w = 1; w < kSelWaves; ++w)
             if (better(s_best[w], best)) best = s_best[w];
         if (best.n > 0 && best.s > 0.0f) {
             a.sel_n[q] = best.n;
@@ -1899,7 +1904,7 @@ int orloj_select_batch(orloj_ctx* ctx, const orloj_grid* grid, const orloj_queue
     for (int i = 0; i < grid->n_bs; ++i) a.bs[i] = grid->batch_sizes[i];
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-    hipLaunchKernelGGL(select_kernel, dim3((unsigned)M), dim3(kThreads), 0, ctx->stream, a);
+    hipLaunchKernelGGL(select_kernel, dim3((unsigned)M), dim3(kSelThreads), 0, ctx->stream, a);
     e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(ctx, e, "select_kernel launch");
     return ORLOJ_OK;
