@@ -86,6 +86,9 @@ CASES = [
     dict(seed=11, n_bins=64, tau_range=(-50.0, -1.0)),
     dict(seed=12, n_bins=64, tau_range=(500.0, 900.0)),
     dict(seed=13, n_bins=300, sparsity=0.9, total=3),
+    # 128-bit table accesses with the last thread chunks past the row's end
+    dict(seed=14, n_bins=1000, n_classes=4, queue_lens=[40, 17], batch_sizes=(1, 5, 16)),
+    dict(seed=15, n_models=1, n_bins=8192, n_classes=3, queue_lens=[30], batch_sizes=(4, 32)),
 ]
 
 
