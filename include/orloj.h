@@ -75,7 +75,9 @@ int orloj_create(orloj_ctx **out, int32_t hip_device, void *hip_stream);
 /* Free a context (waits for its stream first).  NULL is a no-op. */
 void orloj_destroy(orloj_ctx *ctx);
 
-/* Switch the stream later calls enqueue on. */
+/* Switch the stream later calls enqueue on.  If the context holds a
+ * scratch block (orloj_score_candidates_affine), work already enqueued on
+ * the previous stream is waited for first. */
 int orloj_set_stream(orloj_ctx *ctx, void *hip_stream);
 
 /* Text of the last error of `ctx` (never NULL; "" when none). */
@@ -206,6 +208,13 @@ int orloj_score_candidates(orloj_ctx *ctx, const orloj_grid *grid, const float *
  * orloj_score_candidates; orloj_select_batch applies unchanged.  A
  * negative or non-finite c0, or a c1 that is not finite and > 0, is a data
  * error (orloj_sync); that model's requests then score as dead.
+ * The sums of 1 - G behind E[X] do not depend on the batch size, so they
+ * are formed once per (model, prefix length) into a scratch block the
+ * context owns (M x ceil(K / 1024) x the longest prefix floats).  The
+ * first call that needs a larger block waits for the context's
+ * stream, frees the old block and allocates the new one (ORLOJ_E_NOMEM if
+ * that fails); the block is reused by later calls and freed by
+ * orloj_destroy.  Calls on one context are ordered by its stream.
  */
 int orloj_score_candidates_affine(orloj_ctx *ctx, const orloj_grid *grid, const float *d_ccdf,
                                   const int32_t *d_support, const double *d_c0_ms,

@@ -1,7 +1,7 @@
 // Candidate-batch scoring against latency SLOs on MI355X (gfx950).
 //
 // Implements the C ABI of include/orloj.h: the hot path of Orloj
-// ("Predictably Serving Unpredictable DNNs", arXiv 2209.00159) as three
+// ("Predictably Serving Unpredictable DNNs", arXiv 2209.00159) as
 // hand-written HIP kernels for CDNA4:
 //
 //   cdf_kernel     histogram rows -> 1 - CDF (exact 64-bit running sums)
@@ -9,7 +9,13 @@
 //                  position of the members' CDF rows into the batch CDF,
 //                  E[L_B], finish probabilities and Eq. (2) priorities of
 //                  every prefix candidate, all in one pass
+//   emax_kernel    affine mode: the sums behind E[L_B], once per prefix
+//                  length instead of once per batch size
 //   select_kernel  one workgroup per model: argmax over its candidates
+//
+// and, around the path, laws_kernel / iterate_kernel (one Algorithm 1
+// iteration with the paper's own priority) and accumulate_kernel (profiler
+// samples into the histograms).
 //
 // The work is a scan plus reductions over HBM-resident tables, not a dense
 // contraction, so it runs on the vector ALUs (no MFMA): row loads
@@ -244,6 +250,7 @@ struct ScoreArgs {
     const double* c0;          // affine mode: [M] fixed batch overhead (ms); else NULL
     const double* c1;          // affine mode: [M] per-member slope; NULL = tabulated mode
     const float* fill;         // [2][16] zeros, ones (the context's stand-in rows)
+    float* psum;               // affine mode: [M][panels][maxcap] panel sums of 1 - G
     int* err;
     double b;
     int M, C, K, nbs, rect, maxcap;
@@ -272,30 +279,32 @@ constexpr int kFillFloats = 32;
 //   A[]   = in-panel discounted scan of the lane chunk totals
 //   g[], zq[]  snapshot of G and of each chunk's quarter-end prefixes
 // and assembles
-//   G(x_k)     = g[ig0]  (ig0 = kPrevPanel: gl; kNone: 0)
-//   G(x_{k+1}) = g[ig1]  (kNone: 0, the deadline has passed)
-//   both 1 when ig1 = kBeyond (the deadline lies beyond the grid)
-//   Z(k-2) = cW W + cG gl + cA A[la] + fq zq[izq] + sum_r wq[r] g[ig4 + r]
+//   G(x_k)     = f[o0]
+//   G(x_{k+1}) = f[o1]
+//   Z(k-2) = cW W + cG gl + cA f[oa] + fq f[oz] + sum_r wq[r] f[o4 + r]
 //   P   = G(x_k) + theta (G(x_{k+1}) - G(x_k))
 //   num = cg (G(x_k) - (1 - d) Z(k-2)) + psi (G(x_{k+1}) - G(x_k))
-// Index kNone reads as 0.
-constexpr int kNone = -1;
+// where f is the float area of the workgroup's LDS (g, zq, A and three
+// constant slots: 0, 1 and gl, the last written at every scoring step).  The
+// plan resolves every case into an offset: G(x_k) is gl when bin k-1 lies
+// in the previous panel, 0 when k = 0; both G values are 0 when the deadline
+// has passed and 1 when it lies beyond the grid; a term the member does not
+// need has weight 0 and reads any finite slot.  So the lookup takes no
+// branch and no select.
 constexpr int kMaxPanels = 63;   // panels per row (their first members sit in one lane each)
-constexpr int kPrevPanel = -2;
-constexpr int kBeyond = -2;
 
 struct Member {
     int cls;        // class id (clamped into range)
     int16_t hp;     // home panel
-    int16_t ig0;    // snapshot index of G(x_k), or kNone / kPrevPanel
-    int16_t ig1;    // snapshot index of G(x_{k+1}), or kNone / kBeyond
-    int16_t ig4;    // snapshot index of the quarter holding bin k-2, or kNone
-    int16_t izq;    // quarter-end index before that quarter, or kNone
-    int16_t la;     // lane whose in-panel scan precedes bin k-2, or kNone
+    uint16_t o0;    // LDS byte offsets (into the float area) of G(x_k),
+    uint16_t o1;    //   G(x_{k+1}),
+    uint16_t o4;    //   the quarter holding bin k-2,
+    uint16_t oz;    //   the quarter-end prefix before that quarter,
+    uint16_t oa;    //   and the in-panel scan before bin k-2's lane
     float cW;       // weight of W
     float cG;       // weight of gl
-    float cA;       // weight of A[la]
-    float fq;       // weight of zq[izq]
+    float cA;       // weight of f[oa]
+    float fq;       // weight of f[oz]
     float wq[4];    // weights of the quarter's G values
     float theta;    // position inside bin k
     float cg;       // gamma exp(-b theta w), or gamma exp(-b (tau - K w))
@@ -313,11 +322,16 @@ struct Quarters {
 //   g[64 CPL]   snapshot of G over the current panel (float4-interleaved)
 //   zq[64 NQ]   quarter-end discounted prefixes of each lane chunk
 //   A[64]       in-panel discounted scan of the lane chunk totals
+//   k[4]        constant slots: 0, 1, gl (G carried in), unused
 //   mlo[]       first member of each panel
 //   mem[maxcap] Member
 template <int CPL>
+__host__ __device__ constexpr int score_const_slot() {   // float index of k[0]
+    return 64 * CPL + 64 * Quarters<CPL>::NQ + 64;
+}
+template <int CPL>
 __host__ __device__ constexpr size_t score_fixed_bytes() {
-    return 4 * (64 * (size_t)CPL + 64 * (size_t)Quarters<CPL>::NQ + 64 + kMaxPanels + 1);
+    return 4 * ((size_t)score_const_slot<CPL>() + 4 + kMaxPanels + 1);
 }
 __host__ __device__ constexpr size_t score_bytes_per_member() { return sizeof(Member); }
 
@@ -430,7 +444,7 @@ struct LaneCarry64 {
 // some member's deadline falls in this panel, a snapshot in LDS that the
 // same wave then reads to score those members.  Rows are prefetched PF
 // iterations ahead through a register ring.
-template <int CPL, int PF, bool EXACT, int CR>
+template <int CPL, int PF, bool EXACT, int CR, bool AFF>
 __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     using Q = Quarters<CPL>;
     constexpr int PW = 64 * CPL;                   // bins per panel
@@ -438,7 +452,8 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     float* s_g = reinterpret_cast<float*>(smem_raw);
     float* s_zq = s_g + 64 * CPL;
     float* s_A = s_zq + 64 * Q::NQ;
-    int* s_mlo = reinterpret_cast<int*>(s_A + 64);          // kMaxPanels + 1 ints
+    float* s_k = s_A + 64;                                  // constant slots
+    int* s_mlo = reinterpret_cast<int*>(s_k + 4);           // kMaxPanels + 1 ints
     Member* s_mem = reinterpret_cast<Member*>(s_mlo + kMaxPanels + 1);
     const int maxcap = a.maxcap;
 
@@ -459,12 +474,14 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     // bins c1 s w wide, shifted by c0.  Everything below works on that
     // grid: the bin width is c1 s w, the time left is tau - c0, and
     // E[L_B] = c0 + c1 s E[max] (Eq. (5)).  Tabulated mode: c0 = 0, width w.
-    const bool affine = a.c1 != nullptr;
+    // The product over members is the same for every batch size there, so
+    // E[max]'s sums come from emax_kernel, and a wave walks only the panels
+    // up to its last member's home panel.
     const double wq = a.width[q];
     double c0q = 0.0;
     bool aok = true;
     double w = wq;
-    if (affine) {
+    if constexpr (AFF) {
         c0q = a.c0[q];
         const double c1 = a.c1[q];
         aok = c0q >= 0.0 && c0q < HUGE_VAL && c1 > 0.0 && c1 < HUGE_VAL;
@@ -499,7 +516,10 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         Member mb;
         mb.cls = c;
         mb.cost = (float)cm;
-        int hp = 0, ig0 = kNone, ig1 = kNone, ig4 = kNone, izq = kNone, la = kNone;
+        // float indices into the LDS float area; kZ reads 0, kZ + 1 reads 1,
+        // kZ + 2 reads gl
+        constexpr int kZ = score_const_slot<CPL>();
+        int hp = 0, o0 = kZ, o1 = kZ, o4 = 0, oz = kZ, oa = kZ;
         mb.cW = mb.cG = mb.cA = mb.fq = 0.0f;
         mb.wq[0] = mb.wq[1] = mb.wq[2] = mb.wq[3] = 0.0f;
         mb.theta = mb.cg = mb.psi = 0.0f;
@@ -508,7 +528,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         if (tau > 0.0 && wok) {
             const double u = tau / w;
             if (u >= (double)K) {                  // beyond the grid: P = 1
-                ig1 = kBeyond;
+                o0 = o1 = kZ + 1;
                 mb.cg = gamma * (float)exp(-b * (tau - (double)K * w));
                 hp = NP - 1;
                 kz = K - 2;
@@ -520,8 +540,8 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                 mb.theta = (float)th;
                 mb.cg = gamma * (float)exp(-b * th * w);
                 mb.psi = (float)(-expm1(-b * th * w) / bw);
-                ig1 = snap_index<CPL>(k - hp * PW);
-                if (k >= 1) ig0 = k - 1 >= hp * PW ? snap_index<CPL>(k - 1 - hp * PW) : kPrevPanel;
+                o1 = snap_index<CPL>(k - hp * PW);
+                if (k >= 1) o0 = k - 1 >= hp * PW ? snap_index<CPL>(k - 1 - hp * PW) : kZ + 2;
                 kz = k - 2;
             }
         }
@@ -532,14 +552,14 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                 const int qq = j / Q::QW, rq = j - qq * Q::QW;
                 mb.cW = hp > 0 ? exp2f(log2d * (float)(kz - p0 + 1)) : 0.0f;
                 if (l > 0) {
-                    la = l - 1;
+                    oa = 64 * CPL + 64 * Q::NQ + l - 1;
                     mb.cA = exp2f(log2d * (float)(j + 1));
                 }
                 if (qq > 0) {
-                    izq = l * Q::NQ + qq - 1;
+                    oz = 64 * CPL + l * Q::NQ + qq - 1;
                     mb.fq = exp2f(log2d * (float)(rq + 1));
                 }
-                ig4 = snap_index<CPL>(r - rq);     // first bin of the quarter
+                o4 = snap_index<CPL>(r - rq);      // first bin of the quarter
 #pragma unroll
                 for (int rr = 0; rr < 4; ++rr)
                     mb.wq[rr] = rr <= rq ? exp2f(log2d * (float)(rq - rr)) : 0.0f;
@@ -550,9 +570,16 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                 mb.cG = -(float)exp(bw);
             }
         }
-        mb.hp = (int16_t)hp; mb.ig0 = (int16_t)ig0; mb.ig1 = (int16_t)ig1;
-        mb.ig4 = (int16_t)ig4; mb.izq = (int16_t)izq; mb.la = (int16_t)la;
+        mb.hp = (int16_t)hp;
+        mb.o0 = (uint16_t)(4 * o0); mb.o1 = (uint16_t)(4 * o1); mb.o4 = (uint16_t)(4 * o4);
+        mb.oz = (uint16_t)(4 * oz); mb.oa = (uint16_t)(4 * oa);
         s_mem[m] = mb;
+    }
+    if (lane == 0) {
+        s_k[0] = 0.0f;
+        s_k[1] = 1.0f;
+        s_k[2] = 0.0f;
+        s_k[3] = 0.0f;
     }
     wave_lds_fence();
     // first member of each panel (home panels are non-decreasing in m)
@@ -582,7 +609,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         prob += c * (c + 1) / 2;
     }
     // rows of this (model, batch size); affine mode has one set per model
-    const size_t qb = affine ? (size_t)q : (size_t)q * (size_t)a.nbs + (size_t)bi;
+    const size_t qb = AFF ? (size_t)q : (size_t)q * (size_t)a.nbs + (size_t)bi;
     const float* tab_qb = a.tab + qb * (size_t)a.C * (size_t)K;
     wave_lds_fence();
 
@@ -599,6 +626,12 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         hi_r.v[r] = __builtin_bit_cast(float, sup_qb ? sup_qb[2 * c + 1] : K);
     }
     const int mlo_r = s_mlo[min(lane, NP)];
+    // Home panel of the last member (the latest deadline): past it no member
+    // needs G or the discounted prefix, only E[L_B] needs the sums of 1 - G.
+    // The wave walks every panel when it sums E[L_B] itself (those past
+    // LASTP are E-only steps), else only panels up to LASTP.
+    const int LASTP = __builtin_amdgcn_readfirstlane((int)s_mem[ncap - 1].hp);
+    const int NPW = AFF ? LASTP + 1 : NP;
     // Load the lane chunk starting at bin c0 of member n's row; chunks wholly
     // outside the row's support, and every chunk when `none` (the row's
     // values cannot change G), read a constant row instead.
@@ -625,7 +658,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     // always holds iteration it0 + i.  The row of iteration it + PF is
     // loaded PF iterations ahead; (p, n) and the prefetch position advance
     // by counting.
-    const int total = NP * ncap;
+    const int total = NPW * ncap;
     const int iters = (total + PF - 1) / PF * PF;
     const int base = lane * CPL;
 
@@ -637,7 +670,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         load_step(buf[i], pf_n, pf_p * PW + base, false);
         // keep the priming loads in ring order, as the loop issues them
         __builtin_amdgcn_sched_barrier(0);
-        if (++pf_n == ncap) { pf_n = 0; pf_p = min(pf_p + 1, NP - 1); }
+        if (++pf_n == ncap) { pf_n = 0; pf_p = min(pf_p + 1, NPW - 1); }
     }
     int p = 0, n = 0;
     int mlo = __builtin_amdgcn_readlane(mlo_r, 0);
@@ -675,7 +708,8 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             const int hi_n = __builtin_bit_cast(int, hi_r.get(n));
             const int lo_n = __builtin_bit_cast(int, lo_r.get(n));
             const int mhi = min(mend, n + 1);             // members of this panel among the first n+1
-            const bool skip = p >= NP || (n > 0 && (pass_zero || p0 >= hi_n) && !(mlo < mhi));
+            const bool skip = p >= NPW || (n > 0 && (pass_zero || p0 >= hi_n) && !(mlo < mhi));
+            const bool needz = p <= LASTP;                // else an E-only step
             // G <- G * F = G - G (1 - F), in fp64; per-quarter sums
             double gs[Q::QW];
             float zqv[Q::NQ];
@@ -688,7 +722,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                         const int j = qq * Q::QW + r;
                         const float t = (EXACT || pbase + j < K) ? buf[i][j] : 0.0f;
                         Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
-                        gs[r] = qq == 0 ? Gacc[j] : gs[r] + Gacc[j];
+                        if constexpr (!AFF) gs[r] = qq == 0 ? Gacc[j] : gs[r] + Gacc[j];
                         zz = r == 0 ? Gacc[j] : fma(zz, d64, Gacc[j]);
                     }
                     zqv[qq] = (float)zz;
@@ -702,12 +736,13 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             // G == 0 over the pass from here on: later steps of it need no row
             const bool zero_after = pass_zero || min(p0 + PW, K) <= lo_n;
             load_step(buf[i], pf_n, pf_p * PW + base, zero_after && pf_p == p);
-            if (++pf_n == ncap) { pf_n = 0; pf_p = min(pf_p + 1, NP - 1); }
-            if (p < NP) {                                 // else a ghost iteration
+            if (++pf_n == ncap) { pf_n = 0; pf_p = min(pf_p + 1, NPW - 1); }
+            if (p < NPW) {                                // else a ghost iteration
                 float etot = etot_prev, T = T_prev, glast_here = gl_prev;
                 const float Win = cW.get(n);              // carries in from the previous
                 const float glin = cGl.get(n);            // panel pass (zero in the first)
-                if (!skip) {
+                float A = 0.0f;
+                if (!skip && needz) {
                     // quarter ends of the in-chunk discounted prefix, and its total
                     float zc = zqv[0];
 #pragma unroll
@@ -715,16 +750,21 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                         zc = fmaf(zc, dQ, zqv[qq]);
                         zqv[qq] = zc;
                     }
-                    double gsum = gs[0];
-#pragma unroll
-                    for (int r = 1; r < Q::QW; ++r) gsum += gs[r];
-                    // 1 - G summed over the lane's bins (padding bins hold G = 1)
-                    const float e = (float)((double)CPL - gsum);
-                    etot = lane63(wave_scan_sum(e));
-                    const float A = wave_wscan(zc, rp, w15, w31);
+                    A = wave_wscan(zc, rp, w15, w31);
                     T = lane63(A);                        // discounted prefix at the panel end
+                    T_prev = T;
+                }
+                if (!skip) {
+                    if constexpr (!AFF) {
+                        double gsum = gs[0];
+#pragma unroll
+                        for (int r = 1; r < Q::QW; ++r) gsum += gs[r];
+                        // 1 - G summed over the lane's bins (padding bins hold G = 1)
+                        const float e = (float)((double)CPL - gsum);
+                        etot = lane63(wave_scan_sum(e));
+                    }
                     glast_here = lane63((float)Gacc[CPL - 1]);
-                    etot_prev = etot; T_prev = T; gl_prev = glast_here;
+                    etot_prev = etot; gl_prev = glast_here;
 
                     if (mlo < mhi) {
                         // snapshot of G over the panel (rounded again from the
@@ -746,31 +786,30 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
 #pragma unroll
                         for (int qq = 0; qq < Q::NQ; ++qq) s_zq[lane * Q::NQ + qq] = zqv[qq];
                         s_A[lane] = A;
+                        if (lane == 0) s_k[2] = glin;
                         wave_lds_fence();
                         double pP = 0.0;
                         float pN = 0.0f;
                         const int nn = n + 1;
                         auto score_member = [&](const Member& mb, int m) {
-                            const float g0 = s_g[max((int)mb.ig0, 0)];
-                            const float g1 = s_g[max((int)mb.ig1, 0)];
-                            const float al0 = s_A[max((int)mb.la, 0)];
-                            const float zq0 = s_zq[max((int)mb.izq, 0)];
+                            const unsigned char* f = reinterpret_cast<const unsigned char*>(s_g);
+                            auto at = [&](int off) { return *reinterpret_cast<const float*>(f + off); };
+                            const float gk = at(mb.o0);
+                            const float gk1 = at(mb.o1);
+                            const float al0 = at(mb.oa);
+                            const float zq0 = at(mb.oz);
                             float g4[4];
                             if constexpr (Q::QW == 4) {
-                                const float4 t4 = *reinterpret_cast<const float4*>(s_g + max((int)mb.ig4, 0));
+                                const float4 t4 = *reinterpret_cast<const float4*>(f + mb.o4);
                                 g4[0] = t4.x; g4[1] = t4.y; g4[2] = t4.z; g4[3] = t4.w;
                             } else {
 #pragma unroll
-                                for (int r = 0; r < 4; ++r) g4[r] = r < Q::QW ? s_g[max((int)mb.ig4, 0) + r] : 0.0f;
+                                for (int r = 0; r < 4; ++r) g4[r] = r < Q::QW ? at(mb.o4 + 4 * r) : 0.0f;
                             }
-                            const bool beyond = mb.ig1 == kBeyond;
-                            const float gk = beyond ? 1.0f
-                                                    : (mb.ig0 >= 0 ? g0 : (mb.ig0 == kPrevPanel ? glin : 0.0f));
-                            const float gk1 = beyond ? 1.0f : (mb.ig1 >= 0 ? g1 : 0.0f);
-                            float zin = mb.fq * (mb.izq >= 0 ? zq0 : 0.0f);
+                            float zin = mb.fq * zq0;
 #pragma unroll
-                            for (int r = 0; r < 4; ++r) zin = fmaf(mb.wq[r], mb.ig4 >= 0 ? g4[r] : 0.0f, zin);
-                            const float Zv = fmaf(mb.cW, Win, fmaf(mb.cG, glin, fmaf(mb.cA, mb.la >= 0 ? al0 : 0.0f, zin)));
+                            for (int r = 0; r < 4; ++r) zin = fmaf(mb.wq[r], g4[r], zin);
+                            const float Zv = fmaf(mb.cW, Win, fmaf(mb.cG, glin, fmaf(mb.cA, al0, zin)));
                             const float h = gk1 - gk;
                             const float P = fmaf(mb.theta, h, gk);
                             const float num = mb.cost * fmaf(mb.cg, fmaf(-omd, Zv, gk), h * mb.psi);
@@ -792,10 +831,12 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                     }
                 }
                 pass_zero = zero_after;
-                // carries out to the next panel pass, per-step sums
-                cW.set(n, fmaf(Win, dPW, T));
-                cGl.set(n, glast_here);
-                cE.set(n, cE.get(n) + (double)etot);
+                // carries out to the next panel pass (needed up to LASTP), per-step sums
+                if (p < LASTP) {
+                    cW.set(n, fmaf(Win, dPW, T));
+                    cGl.set(n, glast_here);
+                }
+                if constexpr (!AFF) cE.set(n, cE.get(n) + (double)etot);
             }
             if (++n == ncap) {
                 n = 0;
@@ -811,10 +852,117 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     for (int r = 0; r < CR; ++r) {
         const int n = r * 64 + lane;
         if (n < ncap) {
-            const double el = c0q + w * (0.5 + cE.mine(r));
+            double esum = cE.mine(r);
+            if constexpr (AFF) {
+                // the panels' sums in panel order, as this kernel adds them
+                esum = 0.0;
+                const float* ps = a.psum + (size_t)q * (size_t)NP * (size_t)maxcap + n;
+                for (int pp = 0; pp < NP; ++pp) esum += (double)ps[(size_t)pp * (size_t)maxcap];
+            }
+            const double el = c0q + w * (0.5 + esum);
             a.E[cand + n] = cP.mine(r);
             a.EL[cand + n] = (float)el;
             a.S[cand + n] = (float)((double)cN.mine(r) / el);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// emax_kernel (affine mode): the sums behind E[L_B].  Under Eq. (3) every
+// batch size's histogram is the same product G_n of the members' solo CDFs
+// on the base grid, mapped onto a wider grid, so E[max] = w (1/2 +
+// sum_k (1 - G_n(x_{k+1}))) needs one product per prefix length n, not one
+// per batch size (Eq. (5) then gives c0 + c1 s E[max]).  One wave per
+// (model, panel) keeps the running product of its panel's bins over the
+// queue's longest prefix and writes each step's panel sum to
+// psum[(q * panels + p) * maxcap + n], rounded as score_kernel rounds its
+// own per-panel sums, so both modes give the same bits where they coincide.
+// Rows are loaded PFE steps ahead; the class and support of step n sit in
+// lane n % 64, so a step's row address needs no memory round trip.
+// ---------------------------------------------------------------------------
+template <int CPL, bool EXACT, int CR>
+__global__ __launch_bounds__(64) void emax_kernel(const ScoreArgs a) {
+    using Q = Quarters<CPL>;
+    constexpr int PW = 64 * CPL;
+    constexpr int PFE = 8;
+    const int K = a.K;
+    const int NP = (K + PW - 1) / PW;
+    const int q = (int)(blockIdx.x / (unsigned)NP);
+    const int p = (int)(blockIdx.x - (unsigned)q * (unsigned)NP);
+    const int64_t q0 = a.queue_off[q];
+    const int64_t N = a.queue_off[q + 1] - q0;
+    // the longest prefix of any batch size (batch sizes increase)
+    const int64_t cap64 = a.rect ? N : (N < a.bs[a.nbs - 1] ? N : (int64_t)a.bs[a.nbs - 1]);
+    if (cap64 <= 0 || cap64 > a.maxcap || cap64 > 64 * CR) return;
+    const int ncap = (int)cap64;
+    const int lane = threadIdx.x;
+    const int pbase = p * PW + lane * CPL;
+    const float* tab_q = a.tab + (size_t)q * (size_t)a.C * (size_t)K;
+    const int32_t* sup_q = a.sup ? a.sup + (size_t)q * (size_t)a.C * 2 : nullptr;
+    float* out = a.psum + ((size_t)q * (size_t)NP + (size_t)p) * (size_t)a.maxcap;
+
+    LaneCarry<CR> cls_r, lo_r, hi_r;
+#pragma unroll
+    for (int r = 0; r < CR; ++r) {
+        const int m = min(r * 64 + lane, ncap - 1);
+        int c = a.cls[q0 + m];
+        if (c < 0 || c >= a.C) c = 0;                     // score_kernel flags it
+        cls_r.v[r] = __builtin_bit_cast(float, c);
+        lo_r.v[r] = __builtin_bit_cast(float, sup_q ? sup_q[2 * c] : 0);
+        hi_r.v[r] = __builtin_bit_cast(float, sup_q ? sup_q[2 * c + 1] : K);
+    }
+    // the lane chunk of member n's row; chunks wholly outside the row's
+    // support read the constant rows (the same bits, see score_kernel)
+    auto load = [&](float (&v)[CPL], int n) {
+        const int c = __builtin_bit_cast(int, cls_r.get(n));
+        const int lo = __builtin_bit_cast(int, lo_r.get(n));
+        const int hi = __builtin_bit_cast(int, hi_r.get(n));
+        const bool ones = pbase + CPL <= lo, zeros = pbase >= hi;
+        const float* src = tab_q + (size_t)c * (size_t)K + pbase;
+        int lim = K - 1 - pbase;
+        if (ones || zeros) {
+            src = a.fill + (ones ? 16 : 0);
+            lim = CPL - 1;
+        }
+        load_chunk<CPL, EXACT>(v, src, lim);
+    };
+
+    double G[CPL];
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) G[j] = 1.0;
+    float buf[PFE][CPL];
+#pragma unroll
+    for (int i = 0; i < PFE; ++i) {
+        load(buf[i], min(i, ncap - 1));
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    for (int n0 = 0; n0 < ncap; n0 += PFE) {
+#pragma unroll
+        for (int i = 0; i < PFE; ++i) {
+            const int n = n0 + i;
+            if (n < ncap) {
+                double gs[Q::QW];
+#pragma unroll
+                for (int qq = 0; qq < Q::NQ; ++qq) {
+#pragma unroll
+                    for (int r = 0; r < Q::QW; ++r) {
+                        const int j = qq * Q::QW + r;
+                        const float t = (EXACT || pbase + j < K) ? buf[i][j] : 0.0f;
+                        G[j] = fma(-G[j], (double)t, G[j]);
+                        gs[r] = qq == 0 ? G[j] : gs[r] + G[j];
+                    }
+                }
+                double gsum = gs[0];
+#pragma unroll
+                for (int r = 1; r < Q::QW; ++r) gsum += gs[r];
+                const float e = (float)((double)CPL - gsum);    // padding bins hold G = 1
+                const float etot = lane63(wave_scan_sum(e));
+                if (lane == 0) out[n] = etot;
+            }
+            // refill the slot only after the update has read it
+#pragma unroll
+            for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(G[j])::"memory");
+            load(buf[i], min(n + PFE, ncap - 1));
         }
     }
 }
@@ -1420,18 +1568,25 @@ int chunk_per_lane(int K) {
 #define ORLOJ_SCORE_PREFETCH 2   // iterations a row is loaded ahead of its use
 #endif
 
-template <int CPL, bool EXACT, int CR>
+template <int CPL, bool EXACT, int CR, bool AFF>
 hipError_t launch_score_v(const ScoreArgs& a, unsigned grid, hipStream_t st) {
     constexpr int PF = ORLOJ_SCORE_PREFETCH;
     const size_t sm = score_fixed_bytes<CPL>() + (size_t)a.maxcap * score_bytes_per_member();
     static size_t attr_bytes = 0;   // per template instance; device-independent
     if (sm > attr_bytes) {
-        hipError_t e = hipFuncSetAttribute((const void*)score_kernel<CPL, PF, EXACT, CR>,
+        hipError_t e = hipFuncSetAttribute((const void*)score_kernel<CPL, PF, EXACT, CR, AFF>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
         if (e != hipSuccess) return e;
         attr_bytes = sm;
     }
-    hipLaunchKernelGGL((score_kernel<CPL, PF, EXACT, CR>), dim3(grid), dim3(64), sm, st, a);
+    if constexpr (AFF) {
+        // the E[max] panel sums first, on the same stream
+        const unsigned np = (unsigned)((a.K + 64 * CPL - 1) / (64 * CPL));
+        hipLaunchKernelGGL((emax_kernel<CPL, EXACT, CR>), dim3((unsigned)a.M * np), dim3(64), 0, st, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL((score_kernel<CPL, PF, EXACT, CR, AFF>), dim3(grid), dim3(64), sm, st, a);
     return hipGetLastError();
 }
 
@@ -1451,16 +1606,21 @@ int score_chunk(int K) {
 
 // Step carries: one register per 64 steps (longest prefix up to 64, or up to
 // the compiled limit).
-template <int CPL, bool EXACT>
+template <int CPL, bool EXACT, bool AFF>
 hipError_t launch_score_c(const ScoreArgs& a, unsigned grid, hipStream_t st) {
-    return a.maxcap <= 64 ? launch_score_v<CPL, EXACT, 1>(a, grid, st)
-                          : launch_score_v<CPL, EXACT, (ORLOJ_MAX_PREFIX + 63) / 64>(a, grid, st);
+    return a.maxcap <= 64 ? launch_score_v<CPL, EXACT, 1, AFF>(a, grid, st)
+                          : launch_score_v<CPL, EXACT, (ORLOJ_MAX_PREFIX + 63) / 64, AFF>(a, grid, st);
+}
+
+template <int CPL, bool AFF>
+hipError_t launch_score_m(const ScoreArgs& a, unsigned grid, hipStream_t st) {
+    return a.K % (64 * CPL) == 0 ? launch_score_c<CPL, true, AFF>(a, grid, st)
+                                 : launch_score_c<CPL, false, AFF>(a, grid, st);
 }
 
 template <int CPL>
 hipError_t launch_score(const ScoreArgs& a, unsigned grid, hipStream_t st) {
-    return a.K % (64 * CPL) == 0 ? launch_score_c<CPL, true>(a, grid, st)
-                                 : launch_score_c<CPL, false>(a, grid, st);
+    return a.c1 ? launch_score_m<CPL, true>(a, grid, st) : launch_score_m<CPL, false>(a, grid, st);
 }
 
 template <int VPT>
@@ -1485,6 +1645,8 @@ int orloj_create(orloj_ctx** out, int32_t hip_device, void* hip_stream) {
     ctx->stream = (hipStream_t)hip_stream;
     ctx->d_err = nullptr;
     ctx->d_fill = nullptr;
+    ctx->d_work = nullptr;
+    ctx->work_bytes = 0;
     ctx->msg[0] = 0;
     int n = 0;
     if (hipGetDeviceCount(&n) != hipSuccess || hip_device < 0 || hip_device >= n) {
@@ -1514,11 +1676,18 @@ void orloj_destroy(orloj_ctx* ctx) {
     (void)hipStreamSynchronize(ctx->stream);
     if (ctx->d_err) (void)hipFree(ctx->d_err);
     if (ctx->d_fill) (void)hipFree(ctx->d_fill);
+    if (ctx->d_work) (void)hipFree(ctx->d_work);
     delete ctx;
 }
 
 int orloj_set_stream(orloj_ctx* ctx, void* hip_stream) {
     if (!ctx) return ORLOJ_E_INVALID;
+    if ((hipStream_t)hip_stream != ctx->stream && ctx->d_work) {
+        // calls still queued on the old stream may use the scratch
+        hipError_t e = hipSetDevice(ctx->device);
+        if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+        if (e != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
+    }
     ctx->stream = (hipStream_t)hip_stream;
     return ORLOJ_OK;
 }
@@ -1616,6 +1785,30 @@ int orloj_output_sizes(const orloj_grid* grid, const orloj_queues* queues, int32
 
 namespace {
 
+// The context's scratch, grown to at least `bytes`.  Work already enqueued
+// on the context's stream may still use the old block, so the stream is
+// drained before it is freed.
+int ensure_work(orloj_ctx* ctx, size_t bytes) {
+    if (bytes <= ctx->work_bytes) return ORLOJ_OK;
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
+    if (ctx->d_work) {
+        e = hipFree(ctx->d_work);
+        ctx->d_work = nullptr;
+        ctx->work_bytes = 0;
+        if (e != hipSuccess) return hip_fail(ctx, e, "hipFree");
+    }
+    e = hipMalloc(&ctx->d_work, bytes);
+    if (e != hipSuccess) {
+        ctx->d_work = nullptr;
+        return e == hipErrorOutOfMemory
+                   ? orloj_ctx_fail(ctx, ORLOJ_E_NOMEM, "scratch of %zu bytes", bytes)
+                   : hip_fail(ctx, e, "hipMalloc");
+    }
+    ctx->work_bytes = bytes;
+    return ORLOJ_OK;
+}
+
 // Validation and launch shared by the tabulated and the affine scorer
 // (d_c0 / d_c1 NULL: tabulated).
 int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
@@ -1684,6 +1877,16 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
 
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    a.psum = nullptr;
+    if (d_c1) {
+        // emax_kernel's panel sums: [M][panels][maxcap] floats
+        const int64_t np = (grid->n_bins + 64 * score_chunk(grid->n_bins) - 1) / (64 * score_chunk(grid->n_bins));
+        if ((int64_t)M * np > 0x7fffffff)
+            return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (model, panel) pairs");
+        rc = ensure_work(ctx, (size_t)M * (size_t)np * (size_t)maxcap * sizeof(float));
+        if (rc) return rc;
+        a.psum = (float*)ctx->d_work;
+    }
     const unsigned g = (unsigned)nblk;
     static_assert(kMaxChunk == 16, "launch table below");
     static_assert((ORLOJ_MAX_BINS + 64 * kMaxChunk - 1) / (64 * kMaxChunk) <= kMaxPanels, "panels");

@@ -13,6 +13,8 @@ struct orloj_ctx {
     hipStream_t stream;
     int* d_err;      // device status word (data error bits)
     float* d_fill;   // stand-in table entries: 16 zeros, 16 ones
+    void* d_work;    // scratch of the affine scorer (grown on demand), or NULL
+    size_t work_bytes;
     char msg[512];
 };
 

@@ -141,6 +141,46 @@ def test_reduces_to_tabulated_path(ctx):
     _, g_tab = run_gpu(tab, ctx)
     _, g_aff = run_gpu(aff, ctx)
     assert_same_bits(g_tab, g_aff)
+    # rows of several panels (members homed in different panels; E[max] of
+    # the affine path comes from per-panel sums formed once per prefix
+    # length): c1 s = 1 exactly at s = 8 and s = 2
+    for seed, K, s, c1 in [(52, 2500, 8, 0.125), (53, 2048, 2, 0.5), (54, 5000, 4, 0.25)]:
+        base = W.random_case(seed, n_models=2, queue_lens=[s, s - 1], batch_sizes=(s,),
+                             n_bins=K, tau_range=(-10.0, 1.1 * K))
+        tab = dataclasses.replace(base, counts=np.ascontiguousarray(base.counts[:, :1]))
+        aff = dataclasses.replace(base, counts=np.ascontiguousarray(base.counts[:, 0]),
+                                  c0_ms=np.zeros(2), c1=np.full(2, c1))
+        _, g_tab = run_gpu(tab, ctx)
+        _, g_aff = run_gpu(aff, ctx)
+        assert_same_bits(g_tab, g_aff)
+
+
+def test_scratch_grows_and_is_reused(ctx):
+    # the context's scratch for the per-panel sums grows for a larger call
+    # and still serves a smaller one after it, with the same bits as before
+    small = W.random_affine(70, n_models=1, queue_lens=[5], n_bins=100)
+    large = W.random_affine(71, n_models=6, queue_lens=[64, 30, 64, 1, 0, 50], n_bins=5000,
+                            batch_sizes=(1, 8, 64))
+    runs = []
+    for wl in (small, large, small):
+        _, got = run_gpu(wl, ctx)
+        parity.compare(wl, got, run_oracle(wl))
+        runs.append(got)
+    assert_same_bits(runs[0], runs[2])
+
+
+def test_stream_switch_keeps_results():
+    c = O.Context()
+    wl = W.random_affine(73, n_models=3, queue_lens=[9, 40, 17], n_bins=3000)
+    _, first = run_gpu(wl, c)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        c.set_stream(s)
+        _, second = run_gpu(wl, c)
+        torch.cuda.synchronize()
+    c.set_stream(torch.cuda.current_stream())
+    assert_same_bits(first, second)
 
 
 @pytest.mark.parametrize("cid,scale", [(1, 1.0), (1, 4.0), (2, 1.0), (2, 3.0), (3, 1.0),
