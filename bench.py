@@ -103,20 +103,47 @@ def measured_traffic(mode="tabulated"):
     return float(d["traffic_bytes_per_launch"])
 
 
-def affine_algorithmic_flops(wl):
-    """Floating-point operations one affine-mode score launch must do at
-    least: per (model, prefix n, bin) the product update and the E[X] sum
-    (shared by every batch size), per (model, batch size, prefix, bin) the
-    discounted-prefix step at that batch size's rate (one multiply-add)."""
-    K = wl.n_bins
-    per_n = 0
-    per_cand = 0
-    for q in range(wl.n_models):
-        N = wl.queue_len(q)
-        caps = [min(int(s), N) for s in wl.batch_sizes]
-        per_n += max(caps, default=0)
-        per_cand += sum(caps)
-    return 2 * K * per_n + 2 * K * per_cand
+def affine_algorithmic(aw, mode=0):
+    """Work one affine-mode score pass must do at least.  Under Eq. (3)
+    every batch size of a model shares the members' product on the solo
+    grid, so:
+      bytes: each distinct solo-latency row among a model's longest prefix,
+             read once per model; each queued request read once; the
+             per-model scalars (now, width, c0, c1, offsets); every output;
+      flops: per (model, prefix length n, bin) the product update (one fma)
+             and the E[X] sum (one add), shared by every batch size; per
+             candidate the discounted-prefix step (one fma per bin) over the
+             bins its members' priorities read: up to bin k - 2 of its
+             latest deadline on that batch size's grid, the whole grid when
+             a member's deadline lies beyond it, none when all are dead."""
+    K = aw.n_bins
+    rows = reqs = n_c = n_p = 0
+    product_flops = prefix_flops = 0
+    for q in range(aw.n_models):
+        a, b = int(aw.queue_off[q]), int(aw.queue_off[q + 1])
+        N = b - a
+        caps = [N if mode else min(int(s), N) for s in aw.batch_sizes]
+        longest = max(caps, default=0)
+        cls = aw.cls[a:b]
+        rows += len(np.unique(cls[:longest]))
+        reqs += longest
+        product_flops += 3 * K * longest
+        tau = aw.deadline_ms[a:a + longest] - aw.now_ms[q] - aw.c0_ms[q]
+        for s, cap in zip(aw.batch_sizes, caps):
+            n_c += cap
+            n_p += cap * (cap + 1) // 2
+            if cap == 0:
+                continue
+            u = tau[:cap] / (aw.c1[q] * int(s) * aw.bin_width_ms[q])
+            kz = np.where(tau[:cap] <= 0.0, -1, np.where(u >= K, K - 2, np.floor(u) - 2))
+            need = np.maximum.accumulate(kz) + 1          # bins 0 .. max kz of prefix n
+            prefix_flops += 2 * int(np.clip(need, 0, None).sum())
+    table = rows * K * 4
+    queue = reqs * 12 + aw.n_models * (8 * 4 + 8 + 8 * 4)
+    outputs = n_p * 4 + n_c * 16
+    return dict(bytes=table + queue + outputs, table=table, queue=queue, outputs=outputs,
+                flops=product_flops + prefix_flops, product_flops=product_flops,
+                prefix_flops=prefix_flops)
 
 
 def valid_candidates(wl):
@@ -235,14 +262,27 @@ def tabulated_roofline(wl, ab, kms):
 
 
 def affine_roofline(aw, kms):
-    flops = affine_algorithmic_flops(aw)
-    achieved = flops / (kms * 1e-3) / 1e12
+    """Roofline of one affine scoring call (emax_kernel + score_kernel):
+    the bound is whichever of the algorithmic bytes at the HBM peak and the
+    algorithmic flops at the fp64 vector peak takes longer."""
+    w = affine_algorithmic(aw)
+    t = kms * 1e-3
+    gbs = w["bytes"] / t / 1e9
+    tflops = w["flops"] / t / 1e12
     traffic = measured_traffic("affine")
-    return dict(bound="alu", achieved=round(achieved, 2), peak=round(FP64_VECTOR_PEAK_TFLOPS, 1),
-                unit="TFLOP/s", frac=round(achieved / FP64_VECTOR_PEAK_TFLOPS, 4),
-                traffic=None if traffic is None else round(traffic),
-                traffic_unit="bytes/launch", kernel="score_kernel (affine)",
-                kernel_ms=round(kms, 5), algorithmic_flops=flops)
+    hbm_bound = w["bytes"] / (HBM_PEAK_GBS * 1e9) >= w["flops"] / (FP64_VECTOR_PEAK_TFLOPS * 1e12)
+    if hbm_bound:
+        head = dict(bound="hbm", achieved=round(gbs, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=round(gbs / HBM_PEAK_GBS, 4))
+    else:
+        head = dict(bound="alu", achieved=round(tflops, 2), peak=round(FP64_VECTOR_PEAK_TFLOPS, 1),
+                    unit="TFLOP/s", frac=round(tflops / FP64_VECTOR_PEAK_TFLOPS, 4))
+    return dict(head, traffic=None if traffic is None else round(traffic),
+                traffic_unit="bytes/launch", kernel="emax_kernel + score_kernel (affine)",
+                kernel_ms=round(kms, 5), algorithmic_bytes=w["bytes"],
+                algorithmic_flops=w["flops"],
+                alu_achieved_tflops=round(tflops, 3),
+                alu_frac=round(tflops / FP64_VECTOR_PEAK_TFLOPS, 4))
 
 
 def bench_affine(wl, ctx, args, torch, O, W):

@@ -7,7 +7,9 @@
             --kernel score_kernel --copy-bytes N --source <file> --out <summary.txt>
 
 `traffic` turns FETCH_SIZE and WRITE_SIZE (KiB per dispatch) into HBM bytes
-per launch of one kernel, each scaled by what the same counter reads for a
+per launch of one kernel (or per call, summed over the comma-separated
+kernels one call launches, e.g. --kernel emax_kernel,score_kernel), each
+scaled by what the same counter reads for a
 plain device copy of known size run in the same process (bench.py
 --calibrate-copy copies N bytes once): scale = N / (counter KiB x 1024).  It
 writes a `key: value` text summary that bench.py reads back while the
@@ -83,15 +85,19 @@ def pmc_table(paths) -> str:
 
 
 def _kernel_and_copy(path, counter, kernel):
+    """Mean per-dispatch value of `counter`, summed over the comma-separated
+    kernels (one call that launches several), and the copy's value."""
     agg = pmc_means([path])
-    ks = [v for k, d in agg.items() if kernel in k for c, v in d.items() if c == counter]
-    if not ks:
-        raise SystemExit(f"no {kernel} dispatch with {counter} in {path}")
-    vals = ks[0]
+    total = 0.0
+    for name in kernel.split(","):
+        ks = [v for k, d in agg.items() if name in k for c, v in d.items() if c == counter]
+        if not ks:
+            raise SystemExit(f"no {name} dispatch with {counter} in {path}")
+        total += statistics.mean(ks[0])
     copies = [max(d[counter]) for k, d in agg.items() if "copy" in k.lower() and counter in d]
     if not copies:
         raise SystemExit(f"no copy kernel with {counter} in {path} (run with --calibrate-copy)")
-    return statistics.mean(vals), max(copies)
+    return total, max(copies)
 
 
 def source_sha(path) -> str:
@@ -155,7 +161,8 @@ def main(argv=None):
     t = sub.add_parser("traffic")
     t.add_argument("--fetch", required=True)
     t.add_argument("--write", required=True)
-    t.add_argument("--kernel", default="score_kernel")
+    t.add_argument("--kernel", default="score_kernel",
+                   help="kernel name, or comma-separated names summed per call")
     t.add_argument("--copy-bytes", type=int, default=1 << 30)
     t.add_argument("--source", required=True)
     t.add_argument("--out")
