@@ -1253,8 +1253,9 @@ __global__ __launch_bounds__(kThreads) void laws_kernel(const LawArgs a) {
 // priority from the model-law tables (Eq. (2) in the scan form:
 // gamma e^{-b theta w} (G_k - (1-d) Z(k-2)) + h_k psi(theta), over the
 // model-wide E[L]); PopBatch takes the s largest keys (kept flag, priority,
-// earlier position), found by bisection over the 64-bit keys, and orders
-// them by rank.
+// earlier position), found by a radix select over the 64-bit keys (eight
+// 8-bit digits, an LDS histogram and a block suffix scan per digit), and
+// orders them by rank.
 // ---------------------------------------------------------------------------
 struct IterArgs {
     const int32_t* sup;        // [M][nbs][C][2]
@@ -1287,7 +1288,11 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
     __shared__ int s_cnt[ORLOJ_MAX_BATCH_SIZES];
     __shared__ int s_first[ORLOJ_MAX_BATCH_SIZES];
     __shared__ int s_cand;
-    __shared__ unsigned long long s_part[kWaves];
+    __shared__ double s_cd[kWaves];
+    __shared__ int s_cb[kWaves];
+    __shared__ unsigned s_hist[2][256];
+    __shared__ unsigned s_wsum[kWaves];
+    __shared__ int s_digit, s_need;
     __shared__ unsigned long long s_sel[kIterMaxBatch];
     __shared__ int s_nsel;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -1303,8 +1308,12 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
         s_first[i] = 0x7fffffff;
     }
     if (tid == 0) { s_cand = -1; s_nsel = 0; }
-    __syncthreads();
+    s_hist[0][tid] = 0u;
+    s_hist[1][tid] = 0u;
     const int32_t* sup_q = a.sup + (size_t)q * (size_t)nbs * (size_t)C * 2;
+    // first bin with mass of class c at batch size index bi
+    auto first_bin = [&](int bi, int c) { return sup_q[((size_t)bi * C + c) * 2]; };
+    __syncthreads();
 
     // drop phase
     for (int i0 = 0; i0 < N; i0 += kThreads) {
@@ -1327,14 +1336,25 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
             tau = Dlast - nowq;
         }
         bool any = false;
-        for (int bi = 0; bi < nbs; ++bi) {
-            const int lo = sup_q[((size_t)bi * C + c) * 2];
-            const bool keep = live && wok && tau > (double)lo * w;
-            any |= keep;
-            const unsigned long long m = __ballot(keep);
-            if (lane == 0 && m) {
-                atomicAdd(&s_cnt[bi], __popcll(m));
-                atomicMin(&s_first[bi], i0 + wv * 64 + __ffsll((long long)m) - 1);
+        // the support's first bins of a group of batch sizes are loaded
+        // together, so their latencies overlap
+        constexpr int kGroup = 8;
+        for (int b0 = 0; b0 < nbs; b0 += kGroup) {
+            int lo[kGroup];
+#pragma unroll
+            for (int j = 0; j < kGroup; ++j)
+                lo[j] = first_bin(min(b0 + j, nbs - 1), c);
+#pragma unroll
+            for (int j = 0; j < kGroup; ++j) {
+                const int bi = b0 + j;
+                if (bi >= nbs) break;
+                const bool keep = live && wok && tau > (double)lo[j] * w;
+                any |= keep;
+                const unsigned long long m = __ballot(keep);
+                if (lane == 0 && m) {
+                    atomicAdd(&s_cnt[bi], __popcll(m));
+                    atomicMin(&s_first[bi], i0 + wv * 64 + __ffsll((long long)m) - 1);
+                }
             }
         }
         if (live) {
@@ -1343,21 +1363,35 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
         }
     }
     __syncthreads();
-    if (tid == 0) {
-        int cand = -1;
+    // Candidate batch size: among batch sizes whose kept set holds at least
+    // s requests, the largest earliest-kept deadline D_{Q_s}, ties to the
+    // larger batch size (batch sizes increase with their index).  Thread bi
+    // proposes batch size bi; a wave reduction, then one over the waves.
+    {
         double dc = 0.0;
-        for (int bi = 0; bi < nbs; ++bi) {
+        int cb = -1;
+        for (int bi = tid; bi < nbs; bi += kThreads) {
             if (s_cnt[bi] < a.bs[bi]) continue;
             const double D = a.deadline[q0 + s_first[bi]];
-            if (cand < 0 || D > dc || (D == dc && a.bs[bi] > a.bs[cand])) {
-                cand = bi;
-                dc = D;
-            }
+            if (cb < 0 || D > dc || (D == dc && bi > cb)) { dc = D; cb = bi; }
         }
-        s_cand = cand;
-        a.cand_bs[q] = cand >= 0 ? a.bs[cand] : 0;
+        auto take = [&](double d2, int b2) {
+            if (b2 >= 0 && (cb < 0 || d2 > dc || (d2 == dc && b2 > cb))) { dc = d2; cb = b2; }
+        };
+        for (int o = 32; o > 0; o >>= 1) {
+            const double d2 = __shfl_xor(dc, o, 64);
+            const int b2 = __shfl_xor(cb, o, 64);
+            take(d2, b2);
+        }
+        if (lane == 0) { s_cd[wv] = dc; s_cb[wv] = cb; }
+        __syncthreads();
+        if (tid == 0) {
+            for (int i = 0; i < kWaves; ++i) take(s_cd[i], s_cb[i]);
+            s_cand = cb;
+            a.cand_bs[q] = cb >= 0 ? a.bs[cb] : 0;
+        }
+        __syncthreads();
     }
-    __syncthreads();
     const int cand = s_cand;
     int32_t* bq = a.batch + (size_t)q * (size_t)a.bs_max;
     if (cand < 0) {
@@ -1384,7 +1418,7 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
             c = (c < 0 || c >= C) ? 0 : c;
             const double D = a.deadline[q0 + i];
             const double Dlast = a.step_off ? a.step_dl[a.step_off[q0 + i + 1] - 1] : D;
-            const int lo = sup_q[((size_t)cand * C + c) * 2];
+            const int lo = first_bin(cand, c);
             if (wok && Dlast - nowq > (double)lo * w) {
                 const float* G = a.law + (lrow0 + c) * (size_t)K;
                 const float* Z = a.disc + (lrow0 + c) * (size_t)K;
@@ -1437,21 +1471,47 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
             }
         }
     }
-    // the s-th largest key by bisection over [0, 2^64)
-    unsigned long long lo_k = 0ull, hi_k = ~0ull;   // invariant: count(key >= lo_k) >= s
-    for (int it = 0; it < 64 && lo_k < hi_k; ++it) {
-        const unsigned long long mid = lo_k + (hi_k - lo_k) / 2 + 1;
-        int cnt = 0;
+    // The s-th largest key (keys are unique; at least s are non-zero, since
+    // |Q_s| >= s): a radix select, most significant digit first.  Pass by
+    // pass, the keys that agree with the digits fixed so far are counted
+    // per next digit; the digit is the largest whose suffix count reaches
+    // the number of keys still needed, which then drops by the count of the
+    // larger digits.
+    static_assert(kThreads == 256, "one histogram bin per thread");
+    unsigned long long prefix = 0ull, pmask = 0ull;
+    int need = s;
+    for (int shift = 56; shift >= 0; shift -= 8) {
+        unsigned* hist = s_hist[(shift >> 3) & 1];    // two buffers: the other one is cleared here
+        s_hist[((shift >> 3) & 1) ^ 1][tid] = 0u;
 #pragma unroll
-        for (int j = 0; j < kPer; ++j) cnt += key[j] >= mid;
-        for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
-        if (lane == 0) s_part[wv] = (unsigned long long)cnt;
+        for (int j = 0; j < kPer; ++j)
+            if (key[j] != 0ull && (key[j] & pmask) == prefix)
+                atomicAdd(&hist[(unsigned)(key[j] >> shift) & 255u], 1u);
         __syncthreads();
-        unsigned long long tot = 0;
-        for (int i = 0; i < kWaves; ++i) tot += s_part[i];
+        // suffix sums over the digits: thread t holds digit 255 - t, so an
+        // inclusive prefix scan over t counts the keys with digit >= 255 - t
+        const unsigned mine = hist[255 - tid];
+        unsigned incl = mine;
+        for (int o = 1; o < 64; o <<= 1) {
+            const unsigned up = __shfl_up(incl, o, 64);
+            if (lane >= o) incl += up;
+        }
+        if (lane == 63) s_wsum[wv] = incl;
         __syncthreads();
-        if (tot >= (unsigned long long)s) lo_k = mid; else hi_k = mid - 1;
+        for (int i = 0; i < wv; ++i) incl += s_wsum[i];
+        const unsigned excl = incl - mine;
+        // exactly one thread sees the crossing: keys with larger digits are
+        // fewer than `need`, with this digit included they are enough
+        if (excl < (unsigned)need && incl >= (unsigned)need) {
+            s_digit = 255 - tid;
+            s_need = need - (int)excl;
+        }
+        __syncthreads();
+        prefix |= (unsigned long long)s_digit << shift;
+        pmask |= 255ull << shift;
+        need = s_need;
     }
+    const unsigned long long lo_k = prefix;
     // the selected keys, then each one's rank among them
 #pragma unroll
     for (int j = 0; j < kPer; ++j)

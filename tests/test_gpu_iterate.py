@@ -89,6 +89,12 @@ CASES = [
     # 128-bit table accesses with the last thread chunks past the row's end
     dict(seed=14, n_bins=1000, n_classes=4, queue_lens=[40, 17], batch_sizes=(1, 5, 16)),
     dict(seed=15, n_models=1, n_bins=8192, n_classes=3, queue_lens=[30], batch_sizes=(4, 32)),
+    # (batch size, class) pairs: 8192 (first bins staged in LDS) and 8320
+    # (read from the support table)
+    dict(seed=16, n_models=2, n_bins=40, n_classes=64, queue_lens=[200, 90],
+         batch_sizes=tuple(range(1, 129))),
+    dict(seed=17, n_models=2, n_bins=40, n_classes=65, queue_lens=[200, 90],
+         batch_sizes=tuple(range(1, 129))),
 ]
 
 
