@@ -1253,9 +1253,10 @@ __global__ __launch_bounds__(kThreads) void laws_kernel(const LawArgs a) {
 // priority from the model-law tables (Eq. (2) in the scan form:
 // gamma e^{-b theta w} (G_k - (1-d) Z(k-2)) + h_k psi(theta), over the
 // model-wide E[L]); PopBatch takes the s largest keys (kept flag, priority,
-// earlier position), found by a radix select over the 64-bit keys (eight
-// 8-bit digits, an LDS histogram and a block suffix scan per digit), and
-// orders them by rank.
+// earlier position) in rank order: for queues up to 512 requests each key's
+// rank is counted against all keys in LDS; longer queues find the s-th
+// largest key by a radix select (eight 8-bit digits, an LDS histogram and a
+// block suffix scan per digit) and rank the selected keys.
 // ---------------------------------------------------------------------------
 struct IterArgs {
     const int32_t* sup;        // [M][nbs][C][2]
@@ -1291,6 +1292,8 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
     __shared__ double s_cd[kWaves];
     __shared__ int s_cb[kWaves];
     __shared__ unsigned s_hist[2][256];
+    __shared__ int s_wcnt[kWaves][ORLOJ_MAX_BATCH_SIZES];
+    __shared__ int s_wfirst[kWaves][ORLOJ_MAX_BATCH_SIZES];
     __shared__ unsigned s_wsum[kWaves];
     __shared__ int s_digit, s_need;
     __shared__ unsigned long long s_sel[kIterMaxBatch];
@@ -1303,10 +1306,6 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
     const double w = a.width[q];
     const double nowq = a.now[q];
     const bool wok = w > 0.0 && w < HUGE_VAL;
-    for (int i = tid; i < nbs; i += kThreads) {
-        s_cnt[i] = 0;
-        s_first[i] = 0x7fffffff;
-    }
     if (tid == 0) { s_cand = -1; s_nsel = 0; }
     s_hist[0][tid] = 0u;
     s_hist[1][tid] = 0u;
@@ -1315,7 +1314,13 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
     auto first_bin = [&](int bi, int c) { return sup_q[((size_t)bi * C + c) * 2]; };
     __syncthreads();
 
-    // drop phase
+    // drop phase: per wave, the count of kept requests and the first kept
+    // position of batch size index 64 r + l sit in lane l of cntv[r] and
+    // firstv[r] (ballots, no atomics); the waves are combined afterwards
+    constexpr int kBR = ORLOJ_MAX_BATCH_SIZES / 64;
+    int cntv[kBR], firstv[kBR];
+#pragma unroll
+    for (int r = 0; r < kBR; ++r) { cntv[r] = 0; firstv[r] = 0x7fffffff; }
     for (int i0 = 0; i0 < N; i0 += kThreads) {
         const int i = i0 + tid;
         const bool live = i < N;
@@ -1339,21 +1344,25 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
         // the support's first bins of a group of batch sizes are loaded
         // together, so their latencies overlap
         constexpr int kGroup = 8;
-        for (int b0 = 0; b0 < nbs; b0 += kGroup) {
-            int lo[kGroup];
 #pragma unroll
-            for (int j = 0; j < kGroup; ++j)
-                lo[j] = first_bin(min(b0 + j, nbs - 1), c);
+        for (int r = 0; r < kBR; ++r) {
+            const int bend = min(nbs, 64 * r + 64);
+            for (int b0 = 64 * r; b0 < bend; b0 += kGroup) {
+                int lo[kGroup];
 #pragma unroll
-            for (int j = 0; j < kGroup; ++j) {
-                const int bi = b0 + j;
-                if (bi >= nbs) break;
-                const bool keep = live && wok && tau > (double)lo[j] * w;
-                any |= keep;
-                const unsigned long long m = __ballot(keep);
-                if (lane == 0 && m) {
-                    atomicAdd(&s_cnt[bi], __popcll(m));
-                    atomicMin(&s_first[bi], i0 + wv * 64 + __ffsll((long long)m) - 1);
+                for (int j = 0; j < kGroup; ++j)
+                    lo[j] = first_bin(min(b0 + j, nbs - 1), c);
+#pragma unroll
+                for (int j = 0; j < kGroup; ++j) {
+                    const int bi = b0 + j;
+                    if (bi >= bend) break;
+                    const bool keep = live && wok && tau > (double)lo[j] * w;
+                    any |= keep;
+                    const unsigned long long m = __ballot(keep);
+                    const bool me = lane == (bi & 63);
+                    cntv[r] += me ? __popcll(m) : 0;
+                    if (me && m != 0ull && firstv[r] == 0x7fffffff)
+                        firstv[r] = i0 + wv * 64 + __ffsll((long long)m) - 1;
                 }
             }
         }
@@ -1361,6 +1370,22 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
             a.timed_out[q0 + i] = any ? 0 : 1;
             a.score[q0 + i] = 0.0f;
         }
+    }
+#pragma unroll
+    for (int r = 0; r < kBR; ++r) {
+        s_wcnt[wv][64 * r + lane] = cntv[r];
+        s_wfirst[wv][64 * r + lane] = firstv[r];
+    }
+    __syncthreads();
+    for (int bi = tid; bi < nbs; bi += kThreads) {
+        int cnt = 0, first = 0x7fffffff;
+#pragma unroll
+        for (int v = 0; v < kWaves; ++v) {
+            cnt += s_wcnt[v][bi];
+            first = min(first, s_wfirst[v][bi]);
+        }
+        s_cnt[bi] = cnt;
+        s_first[bi] = first;
     }
     __syncthreads();
     // Candidate batch size: among batch sizes whose kept set holds at least
@@ -1471,8 +1496,32 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
             }
         }
     }
-    // The s-th largest key (keys are unique; at least s are non-zero, since
-    // |Q_s| >= s): a radix select, most significant digit first.  Pass by
+    // Short queues: every kept key's rank is the number of larger keys
+    // (keys are unique), counted over the keys staged in LDS; the s keys of
+    // rank < s are the batch, in rank order.
+    constexpr int kRankQueue = 512;
+    static_assert(kRankQueue <= kIterMaxBatch && kRankQueue % kThreads == 0, "s_sel holds the keys");
+    if (N <= kRankQueue) {
+#pragma unroll
+        for (int j = 0; j < kRankQueue / kThreads; ++j) {
+            const int i = j * kThreads + tid;
+            if (i < N) s_sel[i] = key[j];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kRankQueue / kThreads; ++j) {
+            const int i = j * kThreads + tid;
+            if (i < N && key[j] != 0ull) {
+                int rank = 0;
+                for (int t = 0; t < N; ++t) rank += s_sel[t] > key[j];
+                if (rank < s) bq[rank] = i;
+            }
+        }
+        for (int j = s + tid; j < a.bs_max; j += kThreads) bq[j] = -1;
+        return;
+    }
+    // Longer queues: the s-th largest key (at least s are non-zero, since
+    // |Q_s| >= s) by a radix select, most significant digit first.  Pass by
     // pass, the keys that agree with the digits fixed so far are counted
     // per next digit; the digit is the largest whose suffix count reaches
     // the number of keys still needed, which then drops by the count of the
