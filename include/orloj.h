@@ -80,6 +80,16 @@ void orloj_destroy(orloj_ctx *ctx);
  * the previous stream is waited for first. */
 int orloj_set_stream(orloj_ctx *ctx, void *hip_stream);
 
+/* Prefix steps one score workgroup takes (orloj_score_candidates and
+ * orloj_score_candidates_affine).  A (model, batch size) pair's prefix
+ * lengths are scored in sequence; when a launch has too few pairs to fill
+ * the GPU, splitting them into chunks of `steps` (each chunk first rebuilds
+ * the batch CDF of the prefixes before it) shortens the launch.  -1 (the
+ * default): chosen per launch from the queue lengths and the device's
+ * compute units; 0: never split; k > 0: chunks of k.  The results are the
+ * same bits whatever the setting.  ORLOJ_E_INVALID for steps < -1. */
+int orloj_set_score_chunk(orloj_ctx *ctx, int32_t steps);
+
 /* Text of the last error of `ctx` (never NULL; "" when none). */
 const char *orloj_last_error(const orloj_ctx *ctx);
 

@@ -252,6 +252,8 @@ struct ScoreArgs {
     const float* fill;         // [2][16] zeros, ones (the context's stand-in rows)
     float* psum;               // affine mode: [M][panels][maxcap] panel sums of 1 - G
     int* err;
+    int chunk;                 // prefix lengths scored per workgroup (0: all of them)
+    int nchunk;                // workgroups per (model, batch size)
     double b;
     int M, C, K, nbs, rect, maxcap;
     int bs[ORLOJ_MAX_BATCH_SIZES];
@@ -459,15 +461,27 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
 
     const int lane = threadIdx.x;
 
-    // Largest batch sizes first: their workgroups run longest.
-    const int bi = a.nbs - 1 - (int)(blockIdx.x / (unsigned)a.M);
-    const int q = (int)(blockIdx.x % (unsigned)a.M);
+    // Largest batch sizes first, and their last chunks first: those
+    // workgroups run longest.
+    const unsigned per_bs = (unsigned)a.M * (unsigned)a.nchunk;
+    const int bi = a.nbs - 1 - (int)(blockIdx.x / per_bs);
+    const unsigned rem = blockIdx.x % per_bs;
+    const int kc = a.nchunk - 1 - (int)(rem / (unsigned)a.M);
+    const int q = (int)(rem % (unsigned)a.M);
     const int64_t q0 = a.queue_off[q];
     const int64_t N = a.queue_off[q + 1] - q0;
     const int bsz = a.bs[bi];
     const int64_t cap64 = a.rect ? N : (N < bsz ? N : (int64_t)bsz);
     if (cap64 <= 0 || cap64 > maxcap || cap64 > 64 * CR) return;   // the host sizes both
     const int ncap = (int)cap64;
+    // This workgroup scores prefix lengths n0 + 1 .. n1 (steps n0 .. n1 - 1).
+    // A launch too small to fill the chip splits them into chunks: the
+    // steps before n0 only rebuild G (warm-up steps), with the same fma
+    // sequence, so every chunk gives the bits a single workgroup would.
+    const int CH = a.chunk > 0 ? a.chunk : ncap;
+    const int n0 = kc * CH;
+    if (n0 >= ncap) return;
+    const int n1 = min(ncap, n0 + CH);
 
     // Affine mode (Eq. (3)): a batch of size s whose slowest member takes l
     // runs c0 + c1 s l, so its latency histogram is the base grid's with
@@ -499,8 +513,9 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     const float gamma = (float)(-expm1(-bw) / bw);   // (1 - d) / (b w)
     const float omd = (float)(-expm1(-bw));          // 1 - d
 
-    // ---- member lookup plans (fp64 time relative to now)
-    for (int m = lane; m < ncap; m += 64) {
+    // ---- member lookup plans (fp64 time relative to now); the last chunk
+    // checks every member
+    for (int m = lane; m < n1; m += 64) {
         int c = a.cls[q0 + m];
         const double D = a.deadline[q0 + m];
         int flag = 0;
@@ -585,9 +600,9 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     // first member of each panel (home panels are non-decreasing in m)
     for (int p = 0; p <= NP; ++p) {
         int cnt = 0;
-        for (int m0 = 0; m0 < ncap; m0 += 64) {
+        for (int m0 = 0; m0 < n1; m0 += 64) {
             const int m = m0 + lane;
-            const bool below = m < ncap && s_mem[m].hp < p;
+            const bool below = m < n1 && s_mem[m].hp < p;
             cnt += __builtin_popcountll(__ballot(below));
         }
         if (lane == 0) s_mlo[p] = cnt;
@@ -619,7 +634,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     const int32_t* sup_qb = a.sup ? a.sup + qb * (size_t)a.C * 2 : nullptr;
 #pragma unroll
     for (int r = 0; r < CR; ++r) {
-        const int m = min(r * 64 + lane, ncap - 1);
+        const int m = min(r * 64 + lane, n1 - 1);
         const int c = s_mem[m].cls;
         cls_r.v[r] = __builtin_bit_cast(float, c);
         lo_r.v[r] = __builtin_bit_cast(float, sup_qb ? sup_qb[2 * c] : 0);
@@ -630,7 +645,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     // needs G or the discounted prefix, only E[L_B] needs the sums of 1 - G.
     // The wave walks every panel when it sums E[L_B] itself (those past
     // LASTP are E-only steps), else only panels up to LASTP.
-    const int LASTP = __builtin_amdgcn_readfirstlane((int)s_mem[ncap - 1].hp);
+    const int LASTP = __builtin_amdgcn_readfirstlane((int)s_mem[n1 - 1].hp);
     const int NPW = AFF ? LASTP + 1 : NP;
     // Load the lane chunk starting at bin c0 of member n's row; chunks wholly
     // outside the row's support, and every chunk when `none` (the row's
@@ -658,7 +673,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     // always holds iteration it0 + i.  The row of iteration it + PF is
     // loaded PF iterations ahead; (p, n) and the prefetch position advance
     // by counting.
-    const int total = NPW * ncap;
+    const int total = NPW * n1;
     const int iters = (total + PF - 1) / PF * PF;
     const int base = lane * CPL;
 
@@ -670,7 +685,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         load_step(buf[i], pf_n, pf_p * PW + base, false);
         // keep the priming loads in ring order, as the loop issues them
         __builtin_amdgcn_sched_barrier(0);
-        if (++pf_n == ncap) { pf_n = 0; pf_p = min(pf_p + 1, NPW - 1); }
+        if (++pf_n == n1) { pf_n = 0; pf_p = min(pf_p + 1, NPW - 1); }
     }
     int p = 0, n = 0;
     int mlo = __builtin_amdgcn_readlane(mlo_r, 0);
@@ -700,7 +715,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                     // at most 64 members: lane l scores member mlo + l of this
                     // pass at every step, so its plan is read from LDS once
                     pass_valid = mlo + lane < mend;
-                    pass_mb = s_mem[min(mlo + lane, ncap - 1)];
+                    pass_mb = s_mem[min(mlo + lane, n1 - 1)];
                 }
             }
             const int p0 = p * PW;                        // first bin of the panel
@@ -708,7 +723,13 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             const int hi_n = __builtin_bit_cast(int, hi_r.get(n));
             const int lo_n = __builtin_bit_cast(int, lo_r.get(n));
             const int mhi = min(mend, n + 1);             // members of this panel among the first n+1
-            const bool skip = p >= NPW || (n > 0 && (pass_zero || p0 >= hi_n) && !(mlo < mhi));
+            const bool real = n >= n0;                    // else a warm-up step
+            const bool due = real && mlo < mhi;           // some member is scored at this step
+            // G unchanged by this step (a panel past the row's support, or G
+            // already 0 on it): a warm-up step then does nothing, a scored
+            // step after the chunk's first reuses the previous step's sums
+            const bool unchanged = pass_zero || p0 >= hi_n;
+            const bool skip = p >= NPW || (real ? (n > n0 && unchanged && !due) : unchanged);
             const bool needz = p <= LASTP;                // else an E-only step
             // G <- G * F = G - G (1 - F), in fp64; per-quarter sums
             double gs[Q::QW];
@@ -736,8 +757,8 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             // G == 0 over the pass from here on: later steps of it need no row
             const bool zero_after = pass_zero || min(p0 + PW, K) <= lo_n;
             load_step(buf[i], pf_n, pf_p * PW + base, zero_after && pf_p == p);
-            if (++pf_n == ncap) { pf_n = 0; pf_p = min(pf_p + 1, NPW - 1); }
-            if (p < NPW) {                                // else a ghost iteration
+            if (++pf_n == n1) { pf_n = 0; pf_p = min(pf_p + 1, NPW - 1); }
+            if (p < NPW && real) {                        // else a ghost or warm-up iteration
                 float etot = etot_prev, T = T_prev, glast_here = gl_prev;
                 const float Win = cW.get(n);              // carries in from the previous
                 const float glin = cGl.get(n);            // panel pass (zero in the first)
@@ -766,7 +787,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                     glast_here = lane63((float)Gacc[CPL - 1]);
                     etot_prev = etot; gl_prev = glast_here;
 
-                    if (mlo < mhi) {
+                    if (due) {
                         // snapshot of G over the panel (rounded again from the
                         // fp64 values, rather than kept live through the scans)
                         float gv[CPL];
@@ -830,7 +851,6 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                         wave_lds_fence();
                     }
                 }
-                pass_zero = zero_after;
                 // carries out to the next panel pass (needed up to LASTP), per-step sums
                 if (p < LASTP) {
                     cW.set(n, fmaf(Win, dPW, T));
@@ -838,7 +858,8 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                 }
                 if constexpr (!AFF) cE.set(n, cE.get(n) + (double)etot);
             }
-            if (++n == ncap) {
+            pass_zero = zero_after;
+            if (++n == n1) {
                 n = 0;
                 ++p;
                 mlo = __builtin_amdgcn_readlane(mlo_r, min(p, NP));
@@ -851,7 +872,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
 #pragma unroll
     for (int r = 0; r < CR; ++r) {
         const int n = r * 64 + lane;
-        if (n < ncap) {
+        if (n >= n0 && n < n1) {
             double esum = cE.mine(r);
             if constexpr (AFF) {
                 // the panels' sums in panel order, as this kernel adds them
@@ -1765,6 +1786,9 @@ int orloj_create(orloj_ctx** out, int32_t hip_device, void* hip_stream) {
     float fill[kFillFloats];
     for (int i = 0; i < kFillFloats; ++i) fill[i] = i < kFillFloats / 2 ? 0.0f : 1.0f;
     hipError_t e = hipSetDevice(hip_device);
+    ctx->n_cu = 0;
+    ctx->chunk_pref = -1;
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&ctx->n_cu, hipDeviceAttributeMultiprocessorCount, hip_device);
     if (e == hipSuccess) e = hipMalloc((void**)&ctx->d_err, sizeof(int));
     if (e == hipSuccess) e = hipMemset(ctx->d_err, 0, sizeof(int));
     if (e == hipSuccess) e = hipMalloc((void**)&ctx->d_fill, sizeof fill);
@@ -1787,6 +1811,13 @@ void orloj_destroy(orloj_ctx* ctx) {
     if (ctx->d_fill) (void)hipFree(ctx->d_fill);
     if (ctx->d_work) (void)hipFree(ctx->d_work);
     delete ctx;
+}
+
+int orloj_set_score_chunk(orloj_ctx* ctx, int32_t steps) {
+    if (!ctx) return ORLOJ_E_INVALID;
+    if (steps < -1) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "score chunk %d < -1", steps);
+    ctx->chunk_pref = steps;
+    return ORLOJ_OK;
 }
 
 int orloj_set_stream(orloj_ctx* ctx, void* hip_stream) {
@@ -1894,6 +1925,57 @@ int orloj_output_sizes(const orloj_grid* grid, const orloj_queues* queues, int32
 
 namespace {
 
+// Prefix steps per score workgroup.  A (model, batch size) workgroup runs
+// its steps one after another, so a launch with too few workgroups to fill
+// the chip lasts as long as its longest one.  Splitting the steps into
+// chunks, each of which first rebuilds G over the steps before it with
+// warm-up steps (about a fifth of a scored step), shortens that chain at
+// the price of the warm-up work.  Only launches whose workgroups occupy
+// fewer than half the SIMDs (`active` pairs with candidates against
+// `simds`) and whose rows span at most two panels are split: every chunk
+// repeats the product over the panels past its members' deadlines, which
+// in rows of more panels costs as much as it saves.  Cost model, in scored
+// steps: max(longest workgroup, all work / slots), where a SIMD is worth
+// 1.5 slots (one wave alone on a SIMD runs at about half the rate three
+// waves sharing it reach together); a chunk size is taken only if it is 10%
+// faster than none.  Measured: this picks the fastest of none, 8, 16 and 32
+// at configurations 1 to 3 and leaves configuration 5's saturated launch
+// and scheduling-loop rounds unsplit.
+int pick_chunk(const orloj_grid* g, const orloj_queues* qs, int mode, int64_t maxcap,
+               int64_t active, int simds, int panels) {
+    if (2 * active > simds || panels > 2) return 0;
+    const double slots = 1.5 * simds;
+    constexpr double kWarm = 0.2;
+    constexpr int kCh[4] = {0, 32, 16, 8};
+    double total[4] = {0.0, 0.0, 0.0, 0.0}, longest[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int q = 0; q < g->n_models; ++q) {
+        const int64_t N = qs->h_queue_off[q + 1] - qs->h_queue_off[q];
+        if (N <= 0) continue;
+        for (int bi = 0; bi < g->n_bs; ++bi) {
+            const int64_t n = ncap_of(N, g->batch_sizes[bi], mode);
+            total[0] += (double)n;
+            longest[0] = fmax(longest[0], (double)n);
+            for (int o = 1; o < 4; ++o) {
+                const int64_t ch = kCh[o], k = (n + ch - 1) / ch;
+                total[o] += (double)n + kWarm * ch * (double)(k * (k - 1) / 2);
+                longest[o] = fmax(longest[o], kWarm * ch * (double)(k - 1) + (double)(n - (k - 1) * ch));
+            }
+        }
+    }
+    const double t_none = fmax(longest[0], total[0] / slots);
+    double t_best = t_none;
+    int best = 0;
+    for (int o = 1; o < 4; ++o) {
+        if (kCh[o] >= maxcap) continue;
+        const double t = fmax(longest[o], total[o] / slots);
+        if (t < 0.9 * t_none && t < t_best) {
+            t_best = t;
+            best = kCh[o];
+        }
+    }
+    return best;
+}
+
 // The context's scratch, grown to at least `bytes`.  Work already enqueued
 // on the context's stream may still use the old block, so the stream is
 // drained before it is freed.
@@ -1936,13 +2018,15 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
         return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "b_expo_per_ms must be finite and > 0");
     const int M = grid->n_models;
     if (M == 0) return ORLOJ_OK;
-    int64_t maxcap = 0, total = 0;
+    int64_t maxcap = 0, total = 0, active = 0;
     for (int q = 0; q < M; ++q) {
         const int64_t N = queues->h_queue_off[q + 1] - queues->h_queue_off[q];
+        if (N <= 0) continue;
         for (int bi = 0; bi < grid->n_bs; ++bi) {
             const int64_t c = ncap_of(N, grid->batch_sizes[bi], prefix_mode);
             if (c > maxcap) maxcap = c;
             total += c;
+            active += c > 0;
         }
     }
     if (maxcap > ORLOJ_MAX_PREFIX)
@@ -1952,10 +2036,19 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
     if (!d_ccdf || !d_cand_off || !d_prob_off || !d_finish_prob || !d_expected_finish ||
         !d_expected_latency_ms || !d_score)
         return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
-    const int64_t nblk = (int64_t)M * grid->n_bs;
+    const int chunk = ctx->chunk_pref >= 0
+                          ? (ctx->chunk_pref < maxcap ? ctx->chunk_pref : 0)
+                          : pick_chunk(grid, queues, prefix_mode, maxcap, active,
+                                       4 * (ctx->n_cu > 0 ? ctx->n_cu : 256),
+                                       (grid->n_bins + 64 * score_chunk(grid->n_bins) - 1) /
+                                           (64 * score_chunk(grid->n_bins)));
+    const int nchunk = chunk ? (int)((maxcap + chunk - 1) / chunk) : 1;
+    const int64_t nblk = (int64_t)M * grid->n_bs * nchunk;
     if (nblk > 0x7fffffff) return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (model, batch size) pairs");
 
     ScoreArgs a;
+    a.chunk = chunk;
+    a.nchunk = nchunk;
     a.tab = d_ccdf;
     a.sup = d_support;
     a.c0 = d_c0;

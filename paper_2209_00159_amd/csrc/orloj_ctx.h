@@ -10,6 +10,8 @@
 
 struct orloj_ctx {
     int device;
+    int n_cu;        // compute units of the device
+    int chunk_pref;  // prefix steps per score workgroup: -1 automatic, 0 all
     hipStream_t stream;
     int* d_err;      // device status word (data error bits)
     float* d_fill;   // stand-in table entries: 16 zeros, 16 ones

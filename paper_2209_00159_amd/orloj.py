@@ -77,7 +77,8 @@ _QP = ctypes.POINTER(Queues)
 _SP = ctypes.POINTER(Steps)
 _I64P = ctypes.POINTER(ctypes.c_int64)
 
-EXPORTS = ("orloj_create", "orloj_destroy", "orloj_set_stream", "orloj_last_error", "orloj_sync",
+EXPORTS = ("orloj_create", "orloj_destroy", "orloj_set_stream", "orloj_set_score_chunk",
+           "orloj_last_error", "orloj_sync",
            "orloj_build_cdfs", "orloj_output_sizes", "orloj_score_candidates",
            "orloj_score_candidates_affine", "orloj_select_batch", "orloj_build_model_laws",
            "orloj_iterate", "orloj_accumulate", "orloj_sched_create", "orloj_sched_destroy",
@@ -102,6 +103,8 @@ def load(path: Optional[str] = None):
     L.orloj_destroy.restype = None
     L.orloj_set_stream.argtypes = [_VP, _VP]
     L.orloj_set_stream.restype = ctypes.c_int
+    L.orloj_set_score_chunk.argtypes = [_VP, ctypes.c_int32]
+    L.orloj_set_score_chunk.restype = ctypes.c_int
     L.orloj_last_error.argtypes = [_VP]
     L.orloj_last_error.restype = ctypes.c_char_p
     L.orloj_sync.argtypes = [_VP]
@@ -188,6 +191,10 @@ class Context:
 
     def set_stream(self, stream: torch.cuda.Stream):
         self._check(self.L.orloj_set_stream(self.ctx, ctypes.c_void_p(stream.cuda_stream)))
+
+    def set_score_chunk(self, steps: int):
+        """Prefix steps per score workgroup: -1 automatic, 0 never split."""
+        self._check(self.L.orloj_set_score_chunk(self.ctx, int(steps)))
 
     def sync(self):
         self._check(self.L.orloj_sync(self.ctx))

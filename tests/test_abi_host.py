@@ -88,6 +88,7 @@ def test_null_context_is_rejected_without_touching_the_gpu(lib):
     assert rc == O.ORLOJ_E_INVALID
     assert lib.orloj_build_cdfs(None, 1, 4, None, None, None) == O.ORLOJ_E_INVALID
     assert lib.orloj_sync(None) == O.ORLOJ_E_INVALID
+    assert lib.orloj_set_score_chunk(None, 16) == O.ORLOJ_E_INVALID
     assert lib.orloj_last_error(None)
     lib.orloj_destroy(None)
 
