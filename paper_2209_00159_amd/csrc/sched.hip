@@ -71,8 +71,8 @@ struct orloj_sched {
     double* d_E = nullptr;
     float* d_EL = nullptr;
     float* d_S = nullptr;
-    int32_t* d_sel = nullptr;      // [3M]: n, batch size, score bits
-    int32_t* h_sel = nullptr;      // pinned [2M]
+    int32_t* h_sel = nullptr;      // pinned, mapped [3M]: n, batch size, score bits
+    int32_t* d_sel = nullptr;      // the device's address of h_sel
     double device_s = 0.0;         // time spent in upload + launches + download
 
     int64_t* off() { return reinterpret_cast<int64_t*>(h_stage); }
@@ -91,7 +91,7 @@ void sched_free(orloj_sched* s) {
     if (s->h_stage) (void)hipHostFree(s->h_stage);
     if (s->h_sel) (void)hipHostFree(s->h_sel);
     for (void* p : {(void*)s->d_stage, (void*)s->d_P, (void*)s->d_E, (void*)s->d_EL,
-                    (void*)s->d_S, (void*)s->d_sel})
+                    (void*)s->d_S})
         if (p) (void)hipFree(p);
     delete s;
 }
@@ -164,9 +164,9 @@ int decide(orloj_sched* s, double now, const uint8_t* idle, int32_t* sel_n, int3
         rc = orloj_select_batch(ctx, &s->grid, &dq, ORLOJ_PREFIX_TRIANGLE, d_coff, s->d_S, s->d_sel,
                                 s->d_sel + M, reinterpret_cast<float*>(s->d_sel + 2 * M));
         if (rc) return rc;
-        e = hipMemcpyAsync(s->h_sel, s->d_sel, sizeof(int32_t) * 2 * (size_t)M,
-                           hipMemcpyDeviceToHost, ctx->stream);
-        if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+        // the select kernel writes the selections straight into mapped
+        // host memory: no copy, the stream's completion makes them visible
+        e = hipStreamSynchronize(ctx->stream);
         if (e != hipSuccess) return hip_err(ctx, e, "orloj_sched_decide: reading the selections");
         s->device_s += std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
         for (int q = 0; q < M; ++q) {
@@ -259,13 +259,13 @@ int orloj_sched_create(orloj_sched** out, orloj_ctx* ctx, const orloj_grid* grid
     n_p *= M;
     hipError_t e = hipSetDevice(ctx->device);
     if (e == hipSuccess) e = hipHostMalloc((void**)&s->h_stage, s->stage_bytes, hipHostMallocDefault);
-    if (e == hipSuccess) e = hipHostMalloc((void**)&s->h_sel, sizeof(int32_t) * 2 * M, hipHostMallocDefault);
+    if (e == hipSuccess) e = hipHostMalloc((void**)&s->h_sel, sizeof(int32_t) * 3 * M, hipHostMallocMapped);
+    if (e == hipSuccess) e = hipHostGetDevicePointer((void**)&s->d_sel, s->h_sel, 0);
     if (e == hipSuccess) e = hipMalloc((void**)&s->d_stage, s->stage_bytes);
     if (e == hipSuccess) e = hipMalloc((void**)&s->d_P, sizeof(float) * n_p);
     if (e == hipSuccess) e = hipMalloc((void**)&s->d_E, sizeof(double) * n_c);
     if (e == hipSuccess) e = hipMalloc((void**)&s->d_EL, sizeof(float) * n_c);
     if (e == hipSuccess) e = hipMalloc((void**)&s->d_S, sizeof(float) * n_c);
-    if (e == hipSuccess) e = hipMalloc((void**)&s->d_sel, sizeof(int32_t) * 3 * M);
     if (e != hipSuccess) {
         const int rc = hip_err(ctx, e, "orloj_sched_create");
         sched_free(s);
