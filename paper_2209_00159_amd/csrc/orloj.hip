@@ -30,6 +30,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 
 #include "../../include/orloj.h"
@@ -250,7 +251,8 @@ struct ScoreArgs {
     const double* c0;          // affine mode: [M] fixed batch overhead (ms); else NULL
     const double* c1;          // affine mode: [M] per-member slope; NULL = tabulated mode
     const float* fill;         // [2][16] zeros, ones (the context's stand-in rows)
-    float* psum;               // affine mode: [M][panels][maxcap] panel sums of 1 - G
+    float* psum;               // affine mode: [M][np_e][maxcap] panel sums of 1 - G
+    int np_e;                  // panels of those sums (emax_kernel's panel width)
     int* err;
     int chunk;                 // prefix lengths scored per workgroup (0: all of them)
     int nchunk;                // workgroups per (model, batch size)
@@ -877,8 +879,8 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             if constexpr (AFF) {
                 // the panels' sums in panel order, as this kernel adds them
                 esum = 0.0;
-                const float* ps = a.psum + (size_t)q * (size_t)NP * (size_t)maxcap + n;
-                for (int pp = 0; pp < NP; ++pp) esum += (double)ps[(size_t)pp * (size_t)maxcap];
+                const float* ps = a.psum + (size_t)q * (size_t)a.np_e * (size_t)maxcap + n;
+                for (int pp = 0; pp < a.np_e; ++pp) esum += (double)ps[(size_t)pp * (size_t)maxcap];
             }
             const double el = c0q + w * (0.5 + esum);
             a.E[cand + n] = cP.mine(r);
@@ -1709,13 +1711,6 @@ hipError_t launch_score_v(const ScoreArgs& a, unsigned grid, hipStream_t st) {
         if (e != hipSuccess) return e;
         attr_bytes = sm;
     }
-    if constexpr (AFF) {
-        // the E[max] panel sums first, on the same stream
-        const unsigned np = (unsigned)((a.K + 64 * CPL - 1) / (64 * CPL));
-        hipLaunchKernelGGL((emax_kernel<CPL, EXACT, CR>), dim3((unsigned)a.M * np), dim3(64), 0, st, a);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
     hipLaunchKernelGGL((score_kernel<CPL, PF, EXACT, CR, AFF>), dim3(grid), dim3(64), sm, st, a);
     return hipGetLastError();
 }
@@ -1728,11 +1723,27 @@ hipError_t launch_score_v(const ScoreArgs& a, unsigned grid, hipStream_t st) {
 // waves per SIMD) balances the two on gfx950.
 constexpr int kMaxChunk = 16;
 
-int score_chunk(int K) {
+int score_chunk_of(int K) {
     int c = 1;
     while (c < kMaxChunk && 64 * c < K) c <<= 1;
     return c;
 }
+// The affine mode's score waves read only the bins up to their members'
+// deadlines (E[L_B] comes from emax_kernel), which at large batch sizes
+// are a few hundred: narrower panels there mean less work per step and
+// fewer registers.
+#ifndef ORLOJ_AFFINE_CHUNK
+#define ORLOJ_AFFINE_CHUNK 4
+#endif
+constexpr int kAffineChunk = ORLOJ_AFFINE_CHUNK;
+
+int affine_chunk(int K) {
+    int c = std::min(score_chunk_of(K), kAffineChunk);
+    while ((K + 64 * c - 1) / (64 * c) > kMaxPanels) c <<= 1;   // a lane per panel's first member
+    return c;
+}
+
+int score_chunk(int K) { return score_chunk_of(K); }
 
 // Step carries: one register per 64 steps (longest prefix up to 64, or up to
 // the compiled limit).
@@ -1751,6 +1762,23 @@ hipError_t launch_score_m(const ScoreArgs& a, unsigned grid, hipStream_t st) {
 template <int CPL>
 hipError_t launch_score(const ScoreArgs& a, unsigned grid, hipStream_t st) {
     return a.c1 ? launch_score_m<CPL, true>(a, grid, st) : launch_score_m<CPL, false>(a, grid, st);
+}
+
+// emax_kernel (affine mode): its own panel width, the tabulated kernel's, so
+// that its per-panel sums round as that kernel's do.
+template <int CPL>
+hipError_t launch_emax(const ScoreArgs& a, hipStream_t st) {
+    const unsigned g = (unsigned)a.M * (unsigned)a.np_e;
+    const bool exact = a.K % (64 * CPL) == 0;
+    if (a.maxcap <= 64) {
+        if (exact) hipLaunchKernelGGL((emax_kernel<CPL, true, 1>), dim3(g), dim3(64), 0, st, a);
+        else hipLaunchKernelGGL((emax_kernel<CPL, false, 1>), dim3(g), dim3(64), 0, st, a);
+    } else {
+        constexpr int CR = (ORLOJ_MAX_PREFIX + 63) / 64;
+        if (exact) hipLaunchKernelGGL((emax_kernel<CPL, true, CR>), dim3(g), dim3(64), 0, st, a);
+        else hipLaunchKernelGGL((emax_kernel<CPL, false, CR>), dim3(g), dim3(64), 0, st, a);
+    }
+    return hipGetLastError();
 }
 
 template <int VPT>
@@ -2036,12 +2064,14 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
     if (!d_ccdf || !d_cand_off || !d_prob_off || !d_finish_prob || !d_expected_finish ||
         !d_expected_latency_ms || !d_score)
         return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
+    // bins per lane of the score kernel (the affine mode reads only its
+    // members' bins, in narrower panels)
+    const int cpl = d_c1 ? affine_chunk(grid->n_bins) : score_chunk(grid->n_bins);
     const int chunk = ctx->chunk_pref >= 0
                           ? (ctx->chunk_pref < maxcap ? ctx->chunk_pref : 0)
                           : pick_chunk(grid, queues, prefix_mode, maxcap, active,
                                        4 * (ctx->n_cu > 0 ? ctx->n_cu : 256),
-                                       (grid->n_bins + 64 * score_chunk(grid->n_bins) - 1) /
-                                           (64 * score_chunk(grid->n_bins)));
+                                       (grid->n_bins + 64 * cpl - 1) / (64 * cpl));
     const int nchunk = chunk ? (int)((maxcap + chunk - 1) / chunk) : 1;
     const int64_t nblk = (int64_t)M * grid->n_bs * nchunk;
     if (nblk > 0x7fffffff) return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (model, batch size) pairs");
@@ -2080,19 +2110,30 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
     a.psum = nullptr;
+    a.np_e = 0;
+    const int cple = score_chunk(grid->n_bins);
     if (d_c1) {
-        // emax_kernel's panel sums: [M][panels][maxcap] floats
-        const int64_t np = (grid->n_bins + 64 * score_chunk(grid->n_bins) - 1) / (64 * score_chunk(grid->n_bins));
+        // emax_kernel's panel sums: [M][panels][maxcap] floats, formed first
+        const int64_t np = (grid->n_bins + 64 * cple - 1) / (64 * cple);
         if ((int64_t)M * np > 0x7fffffff)
             return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (model, panel) pairs");
         rc = ensure_work(ctx, (size_t)M * (size_t)np * (size_t)maxcap * sizeof(float));
         if (rc) return rc;
         a.psum = (float*)ctx->d_work;
+        a.np_e = (int)np;
+        switch (cple) {
+            case 1: e = launch_emax<1>(a, ctx->stream); break;
+            case 2: e = launch_emax<2>(a, ctx->stream); break;
+            case 4: e = launch_emax<4>(a, ctx->stream); break;
+            case 8: e = launch_emax<8>(a, ctx->stream); break;
+            default: e = launch_emax<16>(a, ctx->stream); break;
+        }
+        if (e != hipSuccess) return hip_fail(ctx, e, "emax_kernel launch");
     }
     const unsigned g = (unsigned)nblk;
     static_assert(kMaxChunk == 16, "launch table below");
     static_assert((ORLOJ_MAX_BINS + 64 * kMaxChunk - 1) / (64 * kMaxChunk) <= kMaxPanels, "panels");
-    switch (score_chunk(grid->n_bins)) {
+    switch (cpl) {
         case 1: e = launch_score<1>(a, g, ctx->stream); break;
         case 2: e = launch_score<2>(a, g, ctx->stream); break;
         case 4: e = launch_score<4>(a, g, ctx->stream); break;

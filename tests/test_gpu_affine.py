@@ -123,18 +123,30 @@ def test_cost_weighted_scores(ctx, case):
     parity.compare(wl, got, run_oracle(wl))
 
 
+def same_but_scores(tab, aff):
+    # P, the expected finish counts and E[L_B] come from the same products
+    # and sums: the same bits.  The affine score waves read their bins in
+    # narrower panels, so a priority's discounted prefix is summed in another
+    # order: the scores agree to rounding.
+    for k in ("finish_prob", "expected_finish", "expected_latency_ms"):
+        assert np.array_equal(tab[k].view(np.uint8), aff[k].view(np.uint8)), k
+    assert np.allclose(aff["score"], tab["score"], rtol=2e-6, atol=1e-12)
+    assert np.array_equal(aff["sel_n"], tab["sel_n"]) and np.array_equal(aff["sel_bs"], tab["sel_bs"])
+
+
 def test_reduces_to_tabulated_path(ctx):
     # c0 = 0 and c1 s = 1 at every batch size: the affine path must give the
-    # tabulated path's bits on the same tables (one batch size, s = 1)
+    # tabulated path's results on the same tables (one batch size, s = 1)
     base = W.random_case(50, n_models=2, queue_lens=[1, 1], batch_sizes=(1,), n_bins=700)
     tab = dataclasses.replace(base, counts=np.ascontiguousarray(base.counts[:, :1]))
     aff = dataclasses.replace(base, counts=np.ascontiguousarray(base.counts[:, 0]),
                               c0_ms=np.zeros(2), c1=np.ones(2))
     _, g_tab = run_gpu(tab, ctx)
     _, g_aff = run_gpu(aff, ctx)
-    assert_same_bits(g_tab, g_aff)
-    # and with s = 4, c1 = 1/4 the bin width c1 s w equals w exactly
-    base = W.random_case(51, n_models=1, queue_lens=[4], batch_sizes=(4,), n_bins=300)
+    same_but_scores(g_tab, g_aff)
+    # and with s = 4, c1 = 1/4 the bin width c1 s w equals w exactly; at 256
+    # bins or fewer both paths read 4 bins per lane: every bit agrees
+    base = W.random_case(51, n_models=1, queue_lens=[4], batch_sizes=(4,), n_bins=250)
     tab = dataclasses.replace(base, counts=np.ascontiguousarray(base.counts[:, :1]))
     aff = dataclasses.replace(base, counts=np.ascontiguousarray(base.counts[:, 0]),
                               c0_ms=np.zeros(1), c1=np.full(1, 0.25))
@@ -152,7 +164,7 @@ def test_reduces_to_tabulated_path(ctx):
                                   c0_ms=np.zeros(2), c1=np.full(2, c1))
         _, g_tab = run_gpu(tab, ctx)
         _, g_aff = run_gpu(aff, ctx)
-        assert_same_bits(g_tab, g_aff)
+        same_but_scores(g_tab, g_aff)
 
 
 def test_scratch_grows_and_is_reused(ctx):
