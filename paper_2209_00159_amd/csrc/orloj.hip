@@ -648,7 +648,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     // The wave walks every panel when it sums E[L_B] itself (those past
     // LASTP are E-only steps), else only panels up to LASTP.
     const int LASTP = __builtin_amdgcn_readfirstlane((int)s_mem[n1 - 1].hp);
-    const int NPW = AFF ? LASTP + 1 : NP;
+    const int NPW = LASTP + 1;
     // Load the lane chunk starting at bin c0 of member n's row; chunks wholly
     // outside the row's support, and every chunk when `none` (the row's
     // values cannot change G), read a constant row instead.
@@ -866,6 +866,78 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                 ++p;
                 mlo = __builtin_amdgcn_readlane(mlo_r, min(p, NP));
                 mend = __builtin_amdgcn_readlane(mlo_r, min(p + 1, NP));
+            }
+        }
+    }
+
+    // ---- E-only panels (tabulated mode): past LASTP no member reads G, so
+    // these panels only add their sums of 1 - G to E[L_B], in a loop of its
+    // own: the product and the sum, no discounted prefix, snapshot or
+    // carries.  Its ring is primed afresh; the panels' sums are added in
+    // panel order after those of the member panels, as before.
+    if constexpr (!AFF) {
+        if (LASTP + 1 < NP) {
+            const int totalB = (NP - LASTP - 1) * n1;
+            const int itersB = (totalB + PF - 1) / PF * PF;
+            int qf_p = LASTP + 1, qf_n = 0;
+#pragma unroll
+            for (int i = 0; i < PF; ++i) {
+                load_step(buf[i], qf_n, qf_p * PW + base, false);
+                __builtin_amdgcn_sched_barrier(0);
+                if (++qf_n == n1) { qf_n = 0; qf_p = min(qf_p + 1, NP - 1); }
+            }
+            int pb = LASTP + 1, nb = 0;
+            bool zero_b = false;
+            float eprev = 0.0f;
+            for (int it0 = 0; it0 < itersB; it0 += PF) {
+#pragma unroll
+                for (int i = 0; i < PF; ++i) {
+                    if (nb == 0) {
+                        asm volatile("" ::: "memory");
+#pragma unroll
+                        for (int j = 0; j < CPL; ++j) Gacc[j] = 1.0;
+                        zero_b = false;
+                    }
+                    const int p0 = pb * PW;
+                    const int pbase = p0 + base;
+                    const int hi_n = __builtin_bit_cast(int, hi_r.get(nb));
+                    const int lo_n = __builtin_bit_cast(int, lo_r.get(nb));
+                    const bool real = nb >= n0;
+                    const bool unchanged = zero_b || p0 >= hi_n;
+                    const bool skip = pb >= NP || (real ? (nb > n0 && unchanged) : unchanged);
+                    double gs[Q::QW];
+                    if (!skip) {
+#pragma unroll
+                        for (int qq = 0; qq < Q::NQ; ++qq) {
+#pragma unroll
+                            for (int r = 0; r < Q::QW; ++r) {
+                                const int j = qq * Q::QW + r;
+                                const float t = (EXACT || pbase + j < K) ? buf[i][j] : 0.0f;
+                                Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
+                                gs[r] = qq == 0 ? Gacc[j] : gs[r] + Gacc[j];
+                            }
+                        }
+                    }
+#pragma unroll
+                    for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(Gacc[j])::"memory");
+                    const bool zero_after = zero_b || min(p0 + PW, K) <= lo_n;
+                    load_step(buf[i], qf_n, qf_p * PW + base, zero_after && qf_p == pb);
+                    if (++qf_n == n1) { qf_n = 0; qf_p = min(qf_p + 1, NP - 1); }
+                    if (pb < NP && real) {
+                        float etot = eprev;
+                        if (!skip) {
+                            double gsum = gs[0];
+#pragma unroll
+                            for (int r = 1; r < Q::QW; ++r) gsum += gs[r];
+                            const float e = (float)((double)CPL - gsum);
+                            etot = lane63(wave_scan_sum(e));
+                            eprev = etot;
+                        }
+                        cE.set(nb, cE.get(nb) + (double)etot);
+                    }
+                    zero_b = zero_after;
+                    if (++nb == n1) { nb = 0; ++pb; }
+                }
             }
         }
     }
