@@ -448,6 +448,9 @@ struct LaneCarry64 {
 // some member's deadline falls in this panel, a snapshot in LDS that the
 // same wave then reads to score those members.  Rows are prefetched PF
 // iterations ahead through a register ring.
+#ifndef ORLOJ_EONLY_PREFETCH
+#define ORLOJ_EONLY_PREFETCH 3   // iterations ahead in the E-only panels' loop
+#endif
 template <int CPL, int PF, bool EXACT, int CR, bool AFF>
 __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     using Q = Quarters<CPL>;
@@ -877,21 +880,23 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     // panel order after those of the member panels, as before.
     if constexpr (!AFF) {
         if (LASTP + 1 < NP) {
+            constexpr int PFB = ORLOJ_EONLY_PREFETCH;   // its ring is deeper: fewer registers live here
+            float bufb[PFB][CPL];
             const int totalB = (NP - LASTP - 1) * n1;
-            const int itersB = (totalB + PF - 1) / PF * PF;
+            const int itersB = (totalB + PFB - 1) / PFB * PFB;
             int qf_p = LASTP + 1, qf_n = 0;
 #pragma unroll
-            for (int i = 0; i < PF; ++i) {
-                load_step(buf[i], qf_n, qf_p * PW + base, false);
+            for (int i = 0; i < PFB; ++i) {
+                load_step(bufb[i], qf_n, qf_p * PW + base, false);
                 __builtin_amdgcn_sched_barrier(0);
                 if (++qf_n == n1) { qf_n = 0; qf_p = min(qf_p + 1, NP - 1); }
             }
             int pb = LASTP + 1, nb = 0;
             bool zero_b = false;
             float eprev = 0.0f;
-            for (int it0 = 0; it0 < itersB; it0 += PF) {
+            for (int it0 = 0; it0 < itersB; it0 += PFB) {
 #pragma unroll
-                for (int i = 0; i < PF; ++i) {
+                for (int i = 0; i < PFB; ++i) {
                     if (nb == 0) {
                         asm volatile("" ::: "memory");
 #pragma unroll
@@ -912,7 +917,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
 #pragma unroll
                             for (int r = 0; r < Q::QW; ++r) {
                                 const int j = qq * Q::QW + r;
-                                const float t = (EXACT || pbase + j < K) ? buf[i][j] : 0.0f;
+                                const float t = (EXACT || pbase + j < K) ? bufb[i][j] : 0.0f;
                                 Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
                                 gs[r] = qq == 0 ? Gacc[j] : gs[r] + Gacc[j];
                             }
@@ -921,7 +926,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
 #pragma unroll
                     for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(Gacc[j])::"memory");
                     const bool zero_after = zero_b || min(p0 + PW, K) <= lo_n;
-                    load_step(buf[i], qf_n, qf_p * PW + base, zero_after && qf_p == pb);
+                    load_step(bufb[i], qf_n, qf_p * PW + base, zero_after && qf_p == pb);
                     if (++qf_n == n1) { qf_n = 0; qf_p = min(qf_p + 1, NP - 1); }
                     if (pb < NP && real) {
                         float etot = eprev;
