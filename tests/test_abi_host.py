@@ -126,3 +126,21 @@ def test_affine_workloads():
     assert np.all((r.c0_ms >= 0) & (r.c0_ms <= 3.0)) and np.all((r.c1 >= 0.05) & (r.c1 <= 1.0))
     sub = r.subset([2, 0])
     assert np.array_equal(sub.c0_ms, r.c0_ms[[2, 0]]) and np.array_equal(sub.c1, r.c1[[2, 0]])
+
+
+def test_runtime_rejects_null_handles_without_touching_the_gpu(lib):
+    g, qs, _ = _grid_queues([1, 4], [3, 2])
+    out = ctypes.c_void_p(123)
+    rc = lib.orloj_sched_create(ctypes.byref(out), None, ctypes.byref(g), None, None, None, 1e-4)
+    assert rc == O.ORLOJ_E_INVALID and out.value is None
+    assert lib.orloj_sched_create(None, None, ctypes.byref(g), None, None, None, 1e-4) == \
+        O.ORLOJ_E_INVALID
+    assert lib.orloj_sched_admit(None, 0, None, None, None) == O.ORLOJ_E_INVALID
+    sel = (ctypes.c_int32 * 2)()
+    assert lib.orloj_sched_decide(None, 0.0, None, sel, sel, None, None, None, None) == \
+        O.ORLOJ_E_INVALID
+    assert lib.orloj_sched_queue_length(None, 0) == -1
+    lib.orloj_sched_destroy(None)
+    st = O.SimStats()
+    assert lib.orloj_simulate_trace(None, None, 0.5, None, None, None, 1, 0, None,
+                                    ctypes.byref(st)) == O.ORLOJ_E_INVALID
