@@ -188,8 +188,8 @@ def _oracle_over_models(wl, affine, budget_s, threads):
 
 def cpu_baseline(config_id, max_models, budget_s=10.0, affine=False, threads=16):
     """The oracle, as it stands, on the models of the same state: once on
-    one host thread and once on `threads` host threads (the GPU machine's CPU
-    share), each for about budget_s seconds.  value = the all-threads
+    one host thread and once on `threads` host threads (the host CPU share
+    of one GPU), each for about budget_s seconds.  value = the all-threads
     evals/s; the one-thread figure is kept beside it."""
     from paper_2209_00159_amd import workloads as W
 
