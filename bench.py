@@ -487,7 +487,7 @@ def main():
         print(f"[bench] scheduling loop over {args.trace_arrivals} arrivals", file=sys.stderr,
               flush=True)
         loop = schedsim.NativeTraceLoop(wl, schedsim.config5_trace(args.trace_arrivals), ctx=ctx,
-                                        record_every=250, record_limit=400,
+                                        record_every=45, record_limit=2000,
                                         tables=(sc.ccdf, sc.support if not args.no_trim else None))
         st = loop.run()
         recorded = st.recorded

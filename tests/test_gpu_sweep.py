@@ -3,8 +3,11 @@ derandomised): bin counts 1..3000 (one or more panels, ragged tails), 1..6
 classes, sparse and dense histograms, irregular batch-size sets, queues of
 0..130 requests spanning dead, in-grid and beyond-grid deadlines, delay
 rates 1e-6..1e-1, both prefix modes, optional miss costs, and both batch
-laws (per-batch-size tables and the affine law c0 + c1 s l)."""
+laws (per-batch-size tables and the affine law c0 + c1 s l), with the
+launch split into step chunks or not.  ORLOJ_SWEEP_EXAMPLES sets the number
+of cases (default 80)."""
 import dataclasses
+import os
 import sys
 
 import numpy as np
@@ -19,7 +22,8 @@ from paper_2209_00159_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
 
-SETTINGS = dict(max_examples=80, deadline=None, derandomize=True, database=None,
+SETTINGS = dict(max_examples=int(os.environ.get("ORLOJ_SWEEP_EXAMPLES", "80")), deadline=None,
+                derandomize=True, database=None,
                 suppress_health_check=[HealthCheck.too_slow, HealthCheck.function_scoped_fixture])
 
 
@@ -42,15 +46,21 @@ def shapes(draw):
 
 
 @settings(**SETTINGS)
-@given(case=shapes(), mode=st.sampled_from([0, 1]), costs=st.booleans(), affine=st.booleans())
-def test_random_shapes_match_oracle(ctx, case, mode, costs, affine):
-    print("sweep", case, "mode", mode, "costs", costs, "affine", affine, flush=True)
+@given(case=shapes(), mode=st.sampled_from([0, 1]), costs=st.booleans(), affine=st.booleans(),
+       chunk=st.sampled_from([-1, 0, 5]))
+def test_random_shapes_match_oracle(ctx, case, mode, costs, affine, chunk):
+    print("sweep", case, "mode", mode, "costs", costs, "affine", affine, "chunk", chunk,
+          flush=True)
     sys.stdout.flush()
     wl = W.random_affine(**case) if affine else W.random_case(**case)
     if costs:
         r = np.random.default_rng(case["seed"])
         wl = dataclasses.replace(wl, cost=r.uniform(0.0, 3.0, size=wl.cls.size))
-    got = O.Scorer(wl, ctx, prefix_mode=mode).run()
+    ctx.set_score_chunk(chunk)
+    try:
+        got = O.Scorer(wl, ctx, prefix_mode=mode).run()
+    finally:
+        ctx.set_score_chunk(-1)
     ora = (oracle.score_workload_affine(wl, wl.c0_ms, wl.c1, prefix_mode=mode) if affine
            else oracle.score_workload(wl, prefix_mode=mode))
     parity.compare(wl, got, ora, mode=mode)
