@@ -447,7 +447,10 @@ struct LaneCarry64 {
 // a DPP scan joins the lanes), the carries into the next panel, and, if
 // some member's deadline falls in this panel, a snapshot in LDS that the
 // same wave then reads to score those members.  Rows are prefetched PF
-// iterations ahead through a register ring.
+// iterations ahead through a register ring.  Panels past the last member's
+// deadline need only the sums of 1 - G: a second, lean loop takes them
+// (tabulated mode).  A workgroup may take a chunk of the steps only, after
+// warm-up steps that rebuild G over the steps before it.
 #ifndef ORLOJ_EONLY_PREFETCH
 #define ORLOJ_EONLY_PREFETCH 3   // iterations ahead in the E-only panels' loop
 #endif
@@ -648,8 +651,9 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     const int mlo_r = s_mlo[min(lane, NP)];
     // Home panel of the last member (the latest deadline): past it no member
     // needs G or the discounted prefix, only E[L_B] needs the sums of 1 - G.
-    // The wave walks every panel when it sums E[L_B] itself (those past
-    // LASTP are E-only steps), else only panels up to LASTP.
+    // The main loop walks the panels up to LASTP; the tabulated mode then
+    // sums the rest (E-only panels) in a loop of its own, the affine mode
+    // takes them from emax_kernel.
     const int LASTP = __builtin_amdgcn_readfirstlane((int)s_mem[n1 - 1].hp);
     const int NPW = LASTP + 1;
     // Load the lane chunk starting at bin c0 of member n's row; chunks wholly
@@ -735,7 +739,6 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             // step after the chunk's first reuses the previous step's sums
             const bool unchanged = pass_zero || p0 >= hi_n;
             const bool skip = p >= NPW || (real ? (n > n0 && unchanged && !due) : unchanged);
-            const bool needz = p <= LASTP;                // else an E-only step
             // G <- G * F = G - G (1 - F), in fp64; per-quarter sums
             double gs[Q::QW];
             float zqv[Q::NQ];
@@ -768,7 +771,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                 const float Win = cW.get(n);              // carries in from the previous
                 const float glin = cGl.get(n);            // panel pass (zero in the first)
                 float A = 0.0f;
-                if (!skip && needz) {
+                if (!skip) {
                     // quarter ends of the in-chunk discounted prefix, and its total
                     float zc = zqv[0];
 #pragma unroll
@@ -856,7 +859,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                         wave_lds_fence();
                     }
                 }
-                // carries out to the next panel pass (needed up to LASTP), per-step sums
+                // carries out to the next panel pass, per-step sums
                 if (p < LASTP) {
                     cW.set(n, fmaf(Win, dPW, T));
                     cGl.set(n, glast_here);
