@@ -193,7 +193,8 @@ def cpu_baseline(config_id, max_models, budget_s=10.0, affine=False, threads=16)
     evals/s; the one-thread figure is kept beside it."""
     from paper_2209_00159_amd import workloads as W
 
-    wl = W.make(config_id, models=list(range(max_models)) if config_id in (4, 5) else None,
+    n_cfg = W.CONFIG_MODELS.get(config_id)
+    wl = W.make(config_id, models=list(range(min(max_models, n_cfg))) if n_cfg else None,
                 workers=threads)
     if affine:
         wl = W.affine(wl)

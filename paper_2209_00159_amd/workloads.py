@@ -418,6 +418,9 @@ def config4(models: Optional[Sequence[int]] = None, workers: int = 1,
 
 CFG5_BACKLOG = 256
 
+# models of the multi-model configurations
+CONFIG_MODELS = {4: 64, 5: 128}
+
 
 def config5(models: Optional[Sequence[int]] = None, workers: int = 1,
             slo_scale: float = 1.0) -> Workload:
