@@ -1346,8 +1346,9 @@ __global__ __launch_bounds__(kThreads) void laws_kernel(const LawArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// iterate_kernel: one workgroup per model.  Requests are strided over the
-// threads (request i on thread i mod 256).  For every batch size the drop
+// iterate_kernel: one workgroup per model, of TH threads (256, or 1024 when
+// a queue is longer than 1024 requests).  Requests are strided over the
+// threads (request i on thread i mod TH).  For every batch size the drop
 // phase keeps a request iff its deadline lies past the left edge of its
 // class's first bin with mass at that batch size (then it could finish run
 // alone); counts and the earliest kept request come from wave ballots.
@@ -1387,17 +1388,20 @@ struct IterArgs {
 
 constexpr int kIterMaxBatch = 1024;      // largest batch size PopBatch orders in LDS
 constexpr int kIterMaxQueue = 4096;      // longest queue one workgroup ranks
+constexpr int kIterWideQueue = 1024;     // longer queues get 1024-thread workgroups
 
-__global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
+template <int TH>
+__global__ __launch_bounds__(TH) void iterate_kernel(const IterArgs a) {
+    constexpr int kW = TH / 64;                    // waves
     __shared__ int s_cnt[ORLOJ_MAX_BATCH_SIZES];
     __shared__ int s_first[ORLOJ_MAX_BATCH_SIZES];
     __shared__ int s_cand;
-    __shared__ double s_cd[kWaves];
-    __shared__ int s_cb[kWaves];
+    __shared__ double s_cd[kW];
+    __shared__ int s_cb[kW];
     __shared__ unsigned s_hist[2][256];
-    __shared__ int s_wcnt[kWaves][ORLOJ_MAX_BATCH_SIZES];
-    __shared__ int s_wfirst[kWaves][ORLOJ_MAX_BATCH_SIZES];
-    __shared__ unsigned s_wsum[kWaves];
+    __shared__ int s_wcnt[kW][ORLOJ_MAX_BATCH_SIZES];
+    __shared__ int s_wfirst[kW][ORLOJ_MAX_BATCH_SIZES];
+    __shared__ unsigned s_wsum[4];
     __shared__ int s_digit, s_need;
     __shared__ unsigned long long s_sel[kIterMaxBatch];
     __shared__ int s_nsel;
@@ -1410,8 +1414,10 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
     const double nowq = a.now[q];
     const bool wok = w > 0.0 && w < HUGE_VAL;
     if (tid == 0) { s_cand = -1; s_nsel = 0; }
-    s_hist[0][tid] = 0u;
-    s_hist[1][tid] = 0u;
+    if (tid < 256) {
+        s_hist[0][tid] = 0u;
+        s_hist[1][tid] = 0u;
+    }
     const int32_t* sup_q = a.sup + (size_t)q * (size_t)nbs * (size_t)C * 2;
     // first bin with mass of class c at batch size index bi
     auto first_bin = [&](int bi, int c) { return sup_q[((size_t)bi * C + c) * 2]; };
@@ -1424,7 +1430,7 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
     int cntv[kBR], firstv[kBR];
 #pragma unroll
     for (int r = 0; r < kBR; ++r) { cntv[r] = 0; firstv[r] = 0x7fffffff; }
-    for (int i0 = 0; i0 < N; i0 += kThreads) {
+    for (int i0 = 0; i0 < N; i0 += TH) {
         const int i = i0 + tid;
         const bool live = i < N;
         int c = 0;
@@ -1480,10 +1486,10 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
         s_wfirst[wv][64 * r + lane] = firstv[r];
     }
     __syncthreads();
-    for (int bi = tid; bi < nbs; bi += kThreads) {
+    for (int bi = tid; bi < nbs; bi += TH) {
         int cnt = 0, first = 0x7fffffff;
 #pragma unroll
-        for (int v = 0; v < kWaves; ++v) {
+        for (int v = 0; v < kW; ++v) {
             cnt += s_wcnt[v][bi];
             first = min(first, s_wfirst[v][bi]);
         }
@@ -1498,7 +1504,7 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
     {
         double dc = 0.0;
         int cb = -1;
-        for (int bi = tid; bi < nbs; bi += kThreads) {
+        for (int bi = tid; bi < nbs; bi += TH) {
             if (s_cnt[bi] < a.bs[bi]) continue;
             const double D = a.deadline[q0 + s_first[bi]];
             if (cb < 0 || D > dc || (D == dc && bi > cb)) { dc = D; cb = bi; }
@@ -1514,7 +1520,7 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
         if (lane == 0) { s_cd[wv] = dc; s_cb[wv] = cb; }
         __syncthreads();
         if (tid == 0) {
-            for (int i = 0; i < kWaves; ++i) take(s_cd[i], s_cb[i]);
+            for (int i = 0; i < kW; ++i) take(s_cd[i], s_cb[i]);
             s_cand = cb;
             a.cand_bs[q] = cb >= 0 ? a.bs[cb] : 0;
         }
@@ -1523,7 +1529,7 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
     const int cand = s_cand;
     int32_t* bq = a.batch + (size_t)q * (size_t)a.bs_max;
     if (cand < 0) {
-        for (int j = tid; j < a.bs_max; j += kThreads) bq[j] = -1;
+        for (int j = tid; j < a.bs_max; j += TH) bq[j] = -1;
         return;
     }
     const int s = a.bs[cand];
@@ -1534,13 +1540,13 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
     const double omd = -expm1(-bw);
     const float el = a.model_el[(size_t)q * nbs + cand];
     const size_t lrow0 = ((size_t)q * nbs + cand) * (size_t)C;
-    constexpr int kPer = kIterMaxQueue / kThreads;   // keys per thread, in registers
+    constexpr int kPer = kIterMaxQueue / TH;         // keys per thread, in registers
     unsigned long long key[kPer];
 #pragma unroll
     for (int j = 0; j < kPer; ++j) key[j] = 0ull;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
-        const int i = j * kThreads + tid;
+        const int i = j * TH + tid;
         if (i < N) {
             int c = a.cls[q0 + i];
             c = (c < 0 || c >= C) ? 0 : c;
@@ -1603,24 +1609,25 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
     // (keys are unique), counted over the keys staged in LDS; the s keys of
     // rank < s are the batch, in rank order.
     constexpr int kRankQueue = 512;
-    static_assert(kRankQueue <= kIterMaxBatch && kRankQueue % kThreads == 0, "s_sel holds the keys");
+    constexpr int kRankSlots = (kRankQueue + TH - 1) / TH;
+    static_assert(kRankQueue <= kIterMaxBatch && kRankSlots <= kPer, "s_sel holds the keys");
     if (N <= kRankQueue) {
 #pragma unroll
-        for (int j = 0; j < kRankQueue / kThreads; ++j) {
-            const int i = j * kThreads + tid;
+        for (int j = 0; j < kRankSlots; ++j) {
+            const int i = j * TH + tid;
             if (i < N) s_sel[i] = key[j];
         }
         __syncthreads();
 #pragma unroll
-        for (int j = 0; j < kRankQueue / kThreads; ++j) {
-            const int i = j * kThreads + tid;
+        for (int j = 0; j < kRankSlots; ++j) {
+            const int i = j * TH + tid;
             if (i < N && key[j] != 0ull) {
                 int rank = 0;
                 for (int t = 0; t < N; ++t) rank += s_sel[t] > key[j];
                 if (rank < s) bq[rank] = i;
             }
         }
-        for (int j = s + tid; j < a.bs_max; j += kThreads) bq[j] = -1;
+        for (int j = s + tid; j < a.bs_max; j += TH) bq[j] = -1;
         return;
     }
     // Longer queues: the s-th largest key (at least s are non-zero, since
@@ -1629,34 +1636,40 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
     // per next digit; the digit is the largest whose suffix count reaches
     // the number of keys still needed, which then drops by the count of the
     // larger digits.
-    static_assert(kThreads == 256, "one histogram bin per thread");
     unsigned long long prefix = 0ull, pmask = 0ull;
     int need = s;
     for (int shift = 56; shift >= 0; shift -= 8) {
         unsigned* hist = s_hist[(shift >> 3) & 1];    // two buffers: the other one is cleared here
-        s_hist[((shift >> 3) & 1) ^ 1][tid] = 0u;
+        if (tid < 256) s_hist[((shift >> 3) & 1) ^ 1][tid] = 0u;
 #pragma unroll
         for (int j = 0; j < kPer; ++j)
             if (key[j] != 0ull && (key[j] & pmask) == prefix)
                 atomicAdd(&hist[(unsigned)(key[j] >> shift) & 255u], 1u);
         __syncthreads();
-        // suffix sums over the digits: thread t holds digit 255 - t, so an
-        // inclusive prefix scan over t counts the keys with digit >= 255 - t
-        const unsigned mine = hist[255 - tid];
-        unsigned incl = mine;
-        for (int o = 1; o < 64; o <<= 1) {
-            const unsigned up = __shfl_up(incl, o, 64);
-            if (lane >= o) incl += up;
+        // suffix sums over the digits: thread t < 256 holds digit 255 - t,
+        // so an inclusive prefix scan over t counts the keys with digit
+        // >= 255 - t (the first four waves, whole)
+        const bool hw = tid < 256;
+        unsigned mine = 0u, incl = 0u;
+        if (hw) {
+            mine = hist[255 - tid];
+            incl = mine;
+            for (int o = 1; o < 64; o <<= 1) {
+                const unsigned up = __shfl_up(incl, o, 64);
+                if (lane >= o) incl += up;
+            }
+            if (lane == 63) s_wsum[wv] = incl;
         }
-        if (lane == 63) s_wsum[wv] = incl;
         __syncthreads();
-        for (int i = 0; i < wv; ++i) incl += s_wsum[i];
-        const unsigned excl = incl - mine;
-        // exactly one thread sees the crossing: keys with larger digits are
-        // fewer than `need`, with this digit included they are enough
-        if (excl < (unsigned)need && incl >= (unsigned)need) {
-            s_digit = 255 - tid;
-            s_need = need - (int)excl;
+        if (hw) {
+            for (int i = 0; i < wv; ++i) incl += s_wsum[i];
+            const unsigned excl = incl - mine;
+            // exactly one thread sees the crossing: keys with larger digits
+            // are fewer than `need`, with this digit included they are enough
+            if (excl < (unsigned)need && incl >= (unsigned)need) {
+                s_digit = 255 - tid;
+                s_need = need - (int)excl;
+            }
         }
         __syncthreads();
         prefix |= (unsigned long long)s_digit << shift;
@@ -1673,13 +1686,13 @@ __global__ __launch_bounds__(kThreads) void iterate_kernel(const IterArgs a) {
         }
     __syncthreads();
     const int nsel = min(s_nsel, min(s, kIterMaxBatch));
-    for (int j = tid; j < nsel; j += kThreads) {
+    for (int j = tid; j < nsel; j += TH) {
         const unsigned long long kj = s_sel[j];
         int rank = 0;
         for (int i = 0; i < nsel; ++i) rank += s_sel[i] > kj;
         bq[rank] = (int32_t)(0xffffffffu - (unsigned)(kj & 0xffffffffull));
     }
-    for (int j = nsel + tid; j < a.bs_max; j += kThreads) bq[j] = -1;
+    for (int j = nsel + tid; j < a.bs_max; j += TH) bq[j] = -1;
 }
 
 // ---------------------------------------------------------------------------
@@ -2313,8 +2326,10 @@ int orloj_iterate(orloj_ctx* ctx, const orloj_grid* grid, const int32_t* d_suppo
     const int bs_max = grid->batch_sizes[grid->n_bs - 1];
     if (bs_max > kIterMaxBatch)
         return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "batch size %d > %d", bs_max, kIterMaxBatch);
+    int64_t longest = 0;
     for (int q = 0; q < M; ++q) {
         const int64_t N = queues->h_queue_off[q + 1] - queues->h_queue_off[q];
+        longest = std::max(longest, N);
         if (N > kIterMaxQueue)
             return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "queue of model %d holds %lld > %d requests", q,
                         (long long)N, kIterMaxQueue);
@@ -2361,7 +2376,10 @@ int orloj_iterate(orloj_ctx* ctx, const orloj_grid* grid, const int32_t* d_suppo
     for (int i = 0; i < grid->n_bs; ++i) a.bs[i] = grid->batch_sizes[i];
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-    hipLaunchKernelGGL(iterate_kernel, dim3(M), dim3(kThreads), 0, ctx->stream, a);
+    if (longest > kIterWideQueue)
+        hipLaunchKernelGGL(iterate_kernel<1024>, dim3(M), dim3(1024), 0, ctx->stream, a);
+    else
+        hipLaunchKernelGGL(iterate_kernel<kThreads>, dim3(M), dim3(kThreads), 0, ctx->stream, a);
     e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(ctx, e, "iterate_kernel launch");
     return ORLOJ_OK;

@@ -89,11 +89,15 @@ CASES = [
     # 128-bit table accesses with the last thread chunks past the row's end
     dict(seed=14, n_bins=1000, n_classes=4, queue_lens=[40, 17], batch_sizes=(1, 5, 16)),
     dict(seed=15, n_models=1, n_bins=8192, n_classes=3, queue_lens=[30], batch_sizes=(4, 32)),
-    # (batch size, class) pairs: 8192 (first bins staged in LDS) and 8320
-    # (read from the support table)
+    # 128 batch sizes (two ballot rows per wave) with 64 and 65 classes
     dict(seed=16, n_models=2, n_bins=40, n_classes=64, queue_lens=[200, 90],
          batch_sizes=tuple(range(1, 129))),
     dict(seed=17, n_models=2, n_bins=40, n_classes=65, queue_lens=[200, 90],
+         batch_sizes=tuple(range(1, 129))),
+    # a queue past 1024 requests (1024-thread workgroups) beside a short one
+    # (rank counting) and an empty one, in the same launch
+    dict(seed=18, n_models=3, n_bins=200, queue_lens=[1025, 3, 0], batch_sizes=(1, 7, 64, 512)),
+    dict(seed=19, n_models=2, n_bins=60, n_classes=9, queue_lens=[2000, 600],
          batch_sizes=tuple(range(1, 129))),
 ]
 
