@@ -32,6 +32,7 @@
 
 #include <algorithm>
 #include <new>
+#include <type_traits>
 
 #include "../../include/orloj.h"
 #include "orloj_ctx.h"
@@ -1351,7 +1352,11 @@ __global__ __launch_bounds__(kThreads) void laws_kernel(const LawArgs a) {
 // threads (request i on thread i mod TH).  For every batch size the drop
 // phase keeps a request iff its deadline lies past the left edge of its
 // class's first bin with mass at that batch size (then it could finish run
-// alone); counts and the earliest kept request come from wave ballots.
+// alone).  Over 32 batch sizes the model's first-bin table sits in LDS and
+// each wave walks its 64 requests with the batch sizes across its lanes (one
+// integer compare per pair against the request's keep edge); otherwise each
+// lane takes a request and the counts and the earliest kept request come
+// from wave ballots.
 // Thread 0 picks the candidate batch size ((D_{Q_s}, s) descending, first
 // with |Q_s| >= s).  Requests kept at the candidate size get their
 // priority from the model-law tables (Eq. (2) in the scan form:
@@ -1389,8 +1394,21 @@ struct IterArgs {
 constexpr int kIterMaxBatch = 1024;      // largest batch size PopBatch orders in LDS
 constexpr int kIterMaxQueue = 4096;      // longest queue one workgroup ranks
 constexpr int kIterWideQueue = 1024;     // longer queues get 1024-thread workgroups
+constexpr int kIterStage = 8448;         // LDS words for a model's first-bin table
 
-template <int TH>
+// The largest k in [0, K] with (double)k * w < tau, or -1 when there is
+// none (tau <= 0 or NaN); w is finite and > 0.  Products k * w rise with k,
+// so for any first bin lo in [0, K]: tau > lo * w iff lo <= keep_edge.
+__device__ inline int keep_edge(double tau, double w, int K) {
+    if (!(tau > 0.0)) return -1;
+    const double t = tau / w;
+    int k = t >= (double)K ? K : (int)t;
+    while (k > 0 && (double)k * w >= tau) --k;
+    while (k < K && (double)(k + 1) * w < tau) ++k;
+    return k;
+}
+
+template <int TH, bool STAGE>
 __global__ __launch_bounds__(TH) void iterate_kernel(const IterArgs a) {
     constexpr int kW = TH / 64;                    // waves
     __shared__ int s_cnt[ORLOJ_MAX_BATCH_SIZES];
@@ -1405,7 +1423,8 @@ __global__ __launch_bounds__(TH) void iterate_kernel(const IterArgs a) {
     __shared__ int s_digit, s_need;
     __shared__ unsigned long long s_sel[kIterMaxBatch];
     __shared__ int s_nsel;
-    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    __shared__ int s_lo[STAGE ? kIterStage + 64 : 1];   // [C][nbs + 1] first bins, 64 words of tail
+    const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int q = blockIdx.x;
     const int64_t q0 = a.queue_off[q];
     const int N = (int)(a.queue_off[q + 1] - q0);
@@ -1419,17 +1438,37 @@ __global__ __launch_bounds__(TH) void iterate_kernel(const IterArgs a) {
         s_hist[1][tid] = 0u;
     }
     const int32_t* sup_q = a.sup + (size_t)q * (size_t)nbs * (size_t)C * 2;
-    // first bin with mass of class c at batch size index bi
+    // first bin with mass of class c at batch size index bi, in [0, K) in
+    // a support that orloj_build_cdfs wrote (the LDS copy below is clamped
+    // to [0, K], which changes nothing there)
     auto first_bin = [&](int bi, int c) { return sup_q[((size_t)bi * C + c) * 2]; };
+    // STAGE (more than 32 batch sizes, and C (nbs + 1) <= kIterStage): the
+    // model's table is staged in LDS class-major (rows of nbs + 1 words, so
+    // the transposing writes spread over the banks) and the drop phase runs
+    // across the batch sizes in the lanes.  Fewer batch sizes would leave
+    // most lanes idle that way, so there each lane takes a request instead.
+    const int ldo = nbs + 1;
+    constexpr bool staged = STAGE;
+    if constexpr (staged)
+        for (int j = tid; j < nbs * C; j += TH) {
+            const int bi = j / C, c = j - bi * C;
+            s_lo[c * ldo + bi] = min(max(sup_q[2 * j], 0), K);
+        }
     __syncthreads();
 
     // drop phase: per wave, the count of kept requests and the first kept
     // position of batch size index 64 r + l sit in lane l of cntv[r] and
-    // firstv[r] (ballots, no atomics); the waves are combined afterwards
+    // firstv[r] (no atomics); the waves are combined afterwards
     constexpr int kBR = ORLOJ_MAX_BATCH_SIZES / 64;
     int cntv[kBR], firstv[kBR];
+    unsigned long long vmask[kBR];   // lanes that hold a batch size, per row
+    const int nrows = (nbs + 63) / 64;
 #pragma unroll
-    for (int r = 0; r < kBR; ++r) { cntv[r] = 0; firstv[r] = 0x7fffffff; }
+    for (int r = 0; r < kBR; ++r) {
+        cntv[r] = 0;
+        firstv[r] = 0x7fffffff;
+        vmask[r] = __ballot(64 * r + lane < nbs);
+    }
     for (int i0 = 0; i0 < N; i0 += TH) {
         const int i = i0 + tid;
         const bool live = i < N;
@@ -1448,6 +1487,55 @@ __global__ __launch_bounds__(TH) void iterate_kernel(const IterArgs a) {
             if (i == 0 && !wok) flag |= kErrWidth;
             if (flag) atomicOr(a.err, flag);
             tau = Dlast - nowq;
+        }
+        if constexpr (staged) {
+            // the wave's 64 requests one at a time, its lanes over the batch
+            // sizes: request j is kept at batch size 64 r + l iff that
+            // batch size's first bin of its class is <= its keep edge (no
+            // first bin is below 0, so a request with edge -1, dead lanes
+            // included, is kept nowhere).  Eight requests' rows are read
+            // before any is compared.
+            const int kk = live && wok ? keep_edge(tau, w, K) : -1;
+            const int base = i0 + wv * 64;
+            const int nj = __builtin_amdgcn_readfirstlane(min(64, N - base));
+            unsigned long long anyb = 0ull;   // bit j: request base + j kept somewhere
+            auto sweep = [&](auto rows) {
+                constexpr int NR = decltype(rows)::value;
+                for (int j0 = 0; j0 < nj; j0 += 8) {
+                    int kj[8], lo[8][NR];
+#pragma unroll
+                    for (int jj = 0; jj < 8; ++jj) {
+                        kj[jj] = __builtin_amdgcn_readlane(kk, j0 + jj);
+                        const int* row = s_lo + __builtin_amdgcn_readlane(c, j0 + jj) * ldo + lane;
+#pragma unroll
+                        for (int r = 0; r < NR; ++r) lo[jj][r] = row[64 * r];
+                    }
+#pragma unroll
+                    for (int jj = 0; jj < 8; ++jj) {
+                        const int ij = base + j0 + jj;
+                        unsigned long long hit = 0ull;
+#pragma unroll
+                        for (int r = 0; r < NR; ++r) {
+                            const bool keep = lo[jj][r] <= kj[jj];
+                            hit |= __ballot(keep) & vmask[r];
+                            cntv[r] += keep ? 1 : 0;
+                            firstv[r] = min(firstv[r], keep ? ij : 0x7fffffff);
+                        }
+                        if (hit) anyb |= 1ull << (j0 + jj);
+                    }
+                }
+            };
+            switch (nrows) {
+                case 1: sweep(std::integral_constant<int, 1>{}); break;
+                case 2: sweep(std::integral_constant<int, 2>{}); break;
+                case 3: sweep(std::integral_constant<int, 3>{}); break;
+                default: sweep(std::integral_constant<int, 4>{}); break;
+            }
+            if (live) {
+                a.timed_out[q0 + i] = (anyb >> lane) & 1ull ? 0 : 1;
+                a.score[q0 + i] = 0.0f;
+            }
+            continue;
         }
         bool any = false;
         // the support's first bins of a group of batch sizes are loaded
@@ -2376,10 +2464,17 @@ int orloj_iterate(orloj_ctx* ctx, const orloj_grid* grid, const int32_t* d_suppo
     for (int i = 0; i < grid->n_bs; ++i) a.bs[i] = grid->batch_sizes[i];
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-    if (longest > kIterWideQueue)
-        hipLaunchKernelGGL(iterate_kernel<1024>, dim3(M), dim3(1024), 0, ctx->stream, a);
-    else
-        hipLaunchKernelGGL(iterate_kernel<kThreads>, dim3(M), dim3(kThreads), 0, ctx->stream, a);
+    const bool stage = a.nbs > 32 && (int64_t)a.C * (a.nbs + 1) <= kIterStage;
+    if (longest > kIterWideQueue) {
+        if (stage)
+            hipLaunchKernelGGL((iterate_kernel<1024, true>), dim3(M), dim3(1024), 0, ctx->stream, a);
+        else
+            hipLaunchKernelGGL((iterate_kernel<1024, false>), dim3(M), dim3(1024), 0, ctx->stream, a);
+    } else if (stage) {
+        hipLaunchKernelGGL((iterate_kernel<kThreads, true>), dim3(M), dim3(kThreads), 0, ctx->stream, a);
+    } else {
+        hipLaunchKernelGGL((iterate_kernel<kThreads, false>), dim3(M), dim3(kThreads), 0, ctx->stream, a);
+    }
     e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(ctx, e, "iterate_kernel launch");
     return ORLOJ_OK;

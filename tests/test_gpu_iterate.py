@@ -89,16 +89,33 @@ CASES = [
     # 128-bit table accesses with the last thread chunks past the row's end
     dict(seed=14, n_bins=1000, n_classes=4, queue_lens=[40, 17], batch_sizes=(1, 5, 16)),
     dict(seed=15, n_models=1, n_bins=8192, n_classes=3, queue_lens=[30], batch_sizes=(4, 32)),
-    # 128 batch sizes (two ballot rows per wave) with 64 and 65 classes
+    # 128 batch sizes (two rows of lanes) with 64 classes (first-bin table
+    # of 64 x 129 words, staged in LDS) and 66 classes (66 x 129 = 8514
+    # words, past the 8448 staged: read from the support table)
     dict(seed=16, n_models=2, n_bins=40, n_classes=64, queue_lens=[200, 90],
          batch_sizes=tuple(range(1, 129))),
-    dict(seed=17, n_models=2, n_bins=40, n_classes=65, queue_lens=[200, 90],
+    dict(seed=17, n_models=2, n_bins=40, n_classes=66, queue_lens=[200, 90],
          batch_sizes=tuple(range(1, 129))),
     # a queue past 1024 requests (1024-thread workgroups) beside a short one
     # (rank counting) and an empty one, in the same launch
     dict(seed=18, n_models=3, n_bins=200, queue_lens=[1025, 3, 0], batch_sizes=(1, 7, 64, 512)),
     dict(seed=19, n_models=2, n_bins=60, n_classes=9, queue_lens=[2000, 600],
          batch_sizes=tuple(range(1, 129))),
+    # many classes over 40 batch sizes: 200 x 41 words staged, 210 x 41 not
+    dict(seed=22, n_models=2, n_bins=30, n_classes=200, queue_lens=[1500, 70],
+         batch_sizes=tuple(range(1, 41))),
+    dict(seed=23, n_models=1, n_bins=30, n_classes=210, queue_lens=[700],
+         batch_sizes=tuple(range(1, 41))),
+    # 256 batch sizes: four rows of lanes
+    dict(seed=24, n_models=2, n_bins=50, n_classes=6, queue_lens=[1100, 300],
+         batch_sizes=tuple(range(1, 257))),
+    # batch sizes across the lanes at the edges of the keep test: one and
+    # two bins, deadlines all past or all before, 33 / 65 / 129 batch sizes
+    dict(seed=25, n_bins=1, queue_lens=[90, 33], batch_sizes=tuple(range(1, 34))),
+    dict(seed=26, n_models=1, n_bins=2, n_classes=1, queue_lens=[70], batch_sizes=tuple(range(2, 67))),
+    dict(seed=27, n_bins=64, tau_range=(-50.0, -1.0), queue_lens=[300, 70], batch_sizes=tuple(range(1, 130))),
+    dict(seed=28, n_bins=64, tau_range=(500.0, 900.0), queue_lens=[300, 70], batch_sizes=tuple(range(1, 130))),
+    dict(seed=29, n_bins=300, sparsity=0.9, total=3, queue_lens=[1200, 5], batch_sizes=tuple(range(1, 66))),
 ]
 
 
