@@ -1421,7 +1421,7 @@ __global__ __launch_bounds__(TH) void iterate_kernel(const IterArgs a) {
     __shared__ int s_wfirst[kW][ORLOJ_MAX_BATCH_SIZES];
     __shared__ unsigned s_wsum[4];
     __shared__ int s_digit, s_need;
-    __shared__ unsigned long long s_sel[kIterMaxBatch];
+    __shared__ __align__(16) unsigned long long s_sel[kIterMaxBatch];
     __shared__ int s_nsel;
     __shared__ int s_lo[STAGE ? kIterStage + 64 : 1];   // [C][nbs + 1] first bins, 64 words of tail
     const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1700,18 +1700,29 @@ __global__ __launch_bounds__(TH) void iterate_kernel(const IterArgs a) {
     constexpr int kRankSlots = (kRankQueue + TH - 1) / TH;
     static_assert(kRankQueue <= kIterMaxBatch && kRankSlots <= kPer, "s_sel holds the keys");
     if (N <= kRankQueue) {
+        // staged up to a multiple of 8 with zero keys (never larger than a
+        // kept key), read 16 bytes at a time
+        const int N8 = (N + 7) & ~7;
 #pragma unroll
         for (int j = 0; j < kRankSlots; ++j) {
             const int i = j * TH + tid;
-            if (i < N) s_sel[i] = key[j];
+            if (i < N8) s_sel[i] = i < N ? key[j] : 0ull;
         }
         __syncthreads();
+        const ulonglong2* sel2 = reinterpret_cast<const ulonglong2*>(s_sel);
 #pragma unroll
         for (int j = 0; j < kRankSlots; ++j) {
             const int i = j * TH + tid;
             if (i < N && key[j] != 0ull) {
+                const unsigned long long kj = key[j];
                 int rank = 0;
-                for (int t = 0; t < N; ++t) rank += s_sel[t] > key[j];
+                for (int t = 0; t < N8 / 2; t += 4) {
+                    ulonglong2 v[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) v[u] = sel2[t + u];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) rank += (v[u].x > kj) + (v[u].y > kj);
+                }
                 if (rank < s) bq[rank] = i;
             }
         }
