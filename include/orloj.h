@@ -76,8 +76,9 @@ int orloj_create(orloj_ctx **out, int32_t hip_device, void *hip_stream);
 void orloj_destroy(orloj_ctx *ctx);
 
 /* Switch the stream later calls enqueue on.  If the context holds a
- * scratch block (orloj_score_candidates_affine), work already enqueued on
- * the previous stream is waited for first. */
+ * scratch block (orloj_score_candidates_affine, or orloj_iterate on long
+ * queues), work already enqueued on the previous stream is waited for
+ * first. */
 int orloj_set_stream(orloj_ctx *ctx, void *hip_stream);
 
 /* Prefix steps one score workgroup takes (orloj_score_candidates and
@@ -289,7 +290,12 @@ int orloj_select_batch(orloj_ctx *ctx, const orloj_grid *grid, const orloj_queue
  * batch size.  b_expo_per_ms must be the value the laws were built with.
  * ORLOJ_E_UNSUPPORTED for a queue longer than 4096 requests or a batch size
  * above 1024.  Queue data errors are reported by orloj_sync as for
- * orloj_score_candidates.
+ * orloj_score_candidates.  A queue longer than 1024 requests, when there are
+ * few enough models (4 M <= the GPU's compute units), has its drop phase run
+ * in parts of 256 requests: the per-part counts (M x parts x |S| x 8 bytes)
+ * go to the context's scratch block, grown on demand as for the affine
+ * scorer (ORLOJ_E_NOMEM if that fails).  d_support entries are taken to lie
+ * in [0, K), as orloj_build_cdfs writes them.
  */
 /*
  * Piecewise-step cost functions (App. B) for orloj_iterate: request r's cost

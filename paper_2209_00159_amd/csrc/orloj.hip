@@ -1349,7 +1349,10 @@ __global__ __launch_bounds__(kThreads) void laws_kernel(const LawArgs a) {
 // ---------------------------------------------------------------------------
 // iterate_kernel: one workgroup per model, of TH threads (256, or 1024 when
 // a queue is longer than 1024 requests).  Requests are strided over the
-// threads (request i on thread i mod TH).  For every batch size the drop
+// threads (request i on thread i mod TH).  Long queues on few models split
+// the iteration in two launches: the drop phase in parts of kDropPart
+// requests, one workgroup each, writing per-part counts, then the rest per
+// model from those counts.  For every batch size the drop
 // phase keeps a request iff its deadline lies past the left edge of its
 // class's first bin with mass at that batch size (then it could finish run
 // alone).  Over 32 batch sizes the model's first-bin table sits in LDS and
@@ -1386,10 +1389,20 @@ struct IterArgs {
     int32_t* cand_bs;          // [M]
     int32_t* batch;            // [M][bs_max]
     int* err;
+    int32_t* part_cnt;         // [M][parts][nbs] drop-phase counts of a split launch
+    int32_t* part_first;       // [M][parts][nbs] and first kept positions
+    int parts;
     double b;
     int M, C, K, nbs, bs_max;
     int bs[ORLOJ_MAX_BATCH_SIZES];
 };
+
+// What one iterate_kernel launch does: the whole iteration per model, or
+// the iteration split in two launches for long queues on few models: the
+// drop phase over parts of kDropPart requests (one workgroup each), then
+// the rest per model from the parts' counts.
+constexpr int kIterWhole = 0, kIterDropPart = 1, kIterFromParts = 2;
+constexpr int kDropPart = 256;
 
 constexpr int kIterMaxBatch = 1024;      // largest batch size PopBatch orders in LDS
 constexpr int kIterMaxQueue = 4096;      // longest queue one workgroup ranks
@@ -1408,7 +1421,7 @@ __device__ inline int keep_edge(double tau, double w, int K) {
     return k;
 }
 
-template <int TH, bool STAGE>
+template <int TH, bool STAGE, int PH>
 __global__ __launch_bounds__(TH) void iterate_kernel(const IterArgs a) {
     constexpr int kW = TH / 64;                    // waves
     __shared__ int s_cnt[ORLOJ_MAX_BATCH_SIZES];
@@ -1425,9 +1438,16 @@ __global__ __launch_bounds__(TH) void iterate_kernel(const IterArgs a) {
     __shared__ int s_nsel;
     __shared__ int s_lo[STAGE ? kIterStage + 64 : 1];   // [C][nbs + 1] first bins, 64 words of tail
     const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int q = blockIdx.x;
+    const int q = PH == kIterDropPart ? (int)blockIdx.x / a.parts : (int)blockIdx.x;
     const int64_t q0 = a.queue_off[q];
     const int N = (int)(a.queue_off[q + 1] - q0);
+    // the requests whose drop phase this workgroup runs
+    int ib = 0, ie = N;
+    if constexpr (PH == kIterDropPart) {
+        ib = ((int)blockIdx.x - q * a.parts) * kDropPart;
+        ie = min(N, ib + kDropPart);
+        if (ib >= ie) return;
+    }
     const int nbs = a.nbs, C = a.C, K = a.K;
     const double w = a.width[q];
     const double nowq = a.now[q];
@@ -1469,9 +1489,9 @@ __global__ __launch_bounds__(TH) void iterate_kernel(const IterArgs a) {
         firstv[r] = 0x7fffffff;
         vmask[r] = __ballot(64 * r + lane < nbs);
     }
-    for (int i0 = 0; i0 < N; i0 += TH) {
+    for (int i0 = ib; i0 < (PH == kIterFromParts ? ib : ie); i0 += TH) {
         const int i = i0 + tid;
-        const bool live = i < N;
+        const bool live = i < ie;
         int c = 0;
         double tau = 0.0;
         if (live) {
@@ -1497,7 +1517,7 @@ __global__ __launch_bounds__(TH) void iterate_kernel(const IterArgs a) {
             // before any is compared.
             const int kk = live && wok ? keep_edge(tau, w, K) : -1;
             const int base = i0 + wv * 64;
-            const int nj = __builtin_amdgcn_readfirstlane(min(64, N - base));
+            const int nj = __builtin_amdgcn_readfirstlane(min(64, ie - base));
             unsigned long long anyb = 0ull;   // bit j: request base + j kept somewhere
             auto sweep = [&](auto rows) {
                 constexpr int NR = decltype(rows)::value;
@@ -1568,22 +1588,39 @@ __global__ __launch_bounds__(TH) void iterate_kernel(const IterArgs a) {
             a.score[q0 + i] = 0.0f;
         }
     }
+    if constexpr (PH != kIterFromParts) {
 #pragma unroll
-    for (int r = 0; r < kBR; ++r) {
-        s_wcnt[wv][64 * r + lane] = cntv[r];
-        s_wfirst[wv][64 * r + lane] = firstv[r];
+        for (int r = 0; r < kBR; ++r) {
+            s_wcnt[wv][64 * r + lane] = cntv[r];
+            s_wfirst[wv][64 * r + lane] = firstv[r];
+        }
+        __syncthreads();
     }
-    __syncthreads();
     for (int bi = tid; bi < nbs; bi += TH) {
         int cnt = 0, first = 0x7fffffff;
+        if constexpr (PH == kIterFromParts) {
+            const size_t p0 = (size_t)q * a.parts * nbs + bi;
+            for (int p = 0; p * kDropPart < N; ++p) {
+                cnt += a.part_cnt[p0 + (size_t)p * nbs];
+                first = min(first, a.part_first[p0 + (size_t)p * nbs]);
+            }
+        } else {
 #pragma unroll
-        for (int v = 0; v < kW; ++v) {
-            cnt += s_wcnt[v][bi];
-            first = min(first, s_wfirst[v][bi]);
+            for (int v = 0; v < kW; ++v) {
+                cnt += s_wcnt[v][bi];
+                first = min(first, s_wfirst[v][bi]);
+            }
         }
-        s_cnt[bi] = cnt;
-        s_first[bi] = first;
+        if constexpr (PH == kIterDropPart) {
+            const size_t o = ((size_t)blockIdx.x) * nbs + bi;   // (q parts + part) nbs + bi
+            a.part_cnt[o] = cnt;
+            a.part_first[o] = first;
+        } else {
+            s_cnt[bi] = cnt;
+            s_first[bi] = first;
+        }
     }
+    if constexpr (PH == kIterDropPart) return;
     __syncthreads();
     // Candidate batch size: among batch sizes whose kept set holds at least
     // s requests, the largest earliest-kept deadline D_{Q_s}, ties to the
@@ -2475,16 +2512,38 @@ int orloj_iterate(orloj_ctx* ctx, const orloj_grid* grid, const int32_t* d_suppo
     for (int i = 0; i < grid->n_bs; ++i) a.bs[i] = grid->batch_sizes[i];
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    a.part_cnt = a.part_first = nullptr;
+    a.parts = 0;
     const bool stage = a.nbs > 32 && (int64_t)a.C * (a.nbs + 1) <= kIterStage;
-    if (longest > kIterWideQueue) {
+    // A long queue on few models leaves most of the chip idle while one
+    // workgroup per model walks it: the drop phase then runs in parts of
+    // kDropPart requests, one workgroup each, before the rest per model.
+    const int n_cu = ctx->n_cu > 0 ? ctx->n_cu : 256;
+    if (longest > kIterWideQueue && 4 * (int64_t)M <= n_cu) {
+        const int P = (int)((longest + kDropPart - 1) / kDropPart);
+        const size_t n = (size_t)M * (size_t)P * (size_t)a.nbs;
+        int rc2 = ensure_work(ctx, 2 * n * sizeof(int32_t));
+        if (rc2) return rc2;
+        a.part_cnt = static_cast<int32_t*>(ctx->d_work);
+        a.part_first = a.part_cnt + n;
+        a.parts = P;
+        const dim3 g((unsigned)(M * P));
         if (stage)
-            hipLaunchKernelGGL((iterate_kernel<1024, true>), dim3(M), dim3(1024), 0, ctx->stream, a);
+            hipLaunchKernelGGL((iterate_kernel<kThreads, true, kIterDropPart>), g, dim3(kThreads), 0, ctx->stream, a);
         else
-            hipLaunchKernelGGL((iterate_kernel<1024, false>), dim3(M), dim3(1024), 0, ctx->stream, a);
+            hipLaunchKernelGGL((iterate_kernel<kThreads, false, kIterDropPart>), g, dim3(kThreads), 0, ctx->stream, a);
+        e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(ctx, e, "iterate_kernel launch");
+        hipLaunchKernelGGL((iterate_kernel<1024, false, kIterFromParts>), dim3(M), dim3(1024), 0, ctx->stream, a);
+    } else if (longest > kIterWideQueue) {
+        if (stage)
+            hipLaunchKernelGGL((iterate_kernel<1024, true, kIterWhole>), dim3(M), dim3(1024), 0, ctx->stream, a);
+        else
+            hipLaunchKernelGGL((iterate_kernel<1024, false, kIterWhole>), dim3(M), dim3(1024), 0, ctx->stream, a);
     } else if (stage) {
-        hipLaunchKernelGGL((iterate_kernel<kThreads, true>), dim3(M), dim3(kThreads), 0, ctx->stream, a);
+        hipLaunchKernelGGL((iterate_kernel<kThreads, true, kIterWhole>), dim3(M), dim3(kThreads), 0, ctx->stream, a);
     } else {
-        hipLaunchKernelGGL((iterate_kernel<kThreads, false>), dim3(M), dim3(kThreads), 0, ctx->stream, a);
+        hipLaunchKernelGGL((iterate_kernel<kThreads, false, kIterWhole>), dim3(M), dim3(kThreads), 0, ctx->stream, a);
     }
     e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(ctx, e, "iterate_kernel launch");

@@ -116,6 +116,15 @@ CASES = [
     dict(seed=27, n_bins=64, tau_range=(-50.0, -1.0), queue_lens=[300, 70], batch_sizes=tuple(range(1, 130))),
     dict(seed=28, n_bins=64, tau_range=(500.0, 900.0), queue_lens=[300, 70], batch_sizes=tuple(range(1, 130))),
     dict(seed=29, n_bins=300, sparsity=0.9, total=3, queue_lens=[1200, 5], batch_sizes=tuple(range(1, 66))),
+    # long queues on few models run the drop phase in parts of 256 requests
+    # (the cases above with a queue past 1024); on 70 models the same
+    # queues stay whole, one 1024-thread workgroup per model
+    dict(seed=30, n_models=70, n_bins=40, n_classes=5, queue_lens=[1500] + [3] * 68 + [1025],
+         batch_sizes=tuple(range(1, 41))),
+    dict(seed=31, n_models=70, n_bins=40, n_classes=5, queue_lens=[0] * 69 + [2049],
+         batch_sizes=(1, 4, 9, 30)),
+    dict(seed=32, n_models=3, n_bins=70, n_classes=4, queue_lens=[1536, 1537, 0],
+         batch_sizes=(2, 16, 500)),
 ]
 
 
