@@ -473,7 +473,8 @@ def main():
         n_batches = int((res["cand_bs"] > 0).sum())
         line["iterate"] = dict(
             what="orloj_iterate: one Algorithm 1 iteration (drop phase, candidate batch size, "
-                 "priority of every kept request, PopBatch) for every model, one launch",
+                 "priority of every kept request, PopBatch) for every model, one launch "
+                 "(two for long queues on few models)",
             ms_per_iteration=round(it_ms, 5), models_with_batch=n_batches,
             decisions_per_s=round(n_batches / (it_ms * 1e-3), 1),
             requests=int(wl.queue_off[-1]),
