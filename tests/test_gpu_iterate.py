@@ -214,6 +214,25 @@ def test_iterate_costs_and_steps(ctx, seed):
     check(wl, got, ora)
 
 
+@pytest.mark.parametrize("seed,lens", [(54, [300, 9, 40]), (55, [1300, 9, 700])],
+                         ids=["lanes-over-batch-sizes", "drop-in-parts"])
+def test_iterate_costs_and_steps_wide(ctx, seed, lens):
+    """Step cost functions where the drop phase runs across the batch sizes
+    in the lanes (40 batch sizes), and split into parts (a 1300-request
+    queue): the keep edge comes from each request's last step."""
+    import dataclasses
+    wl = W.random_case(seed, n_models=3, queue_lens=lens, n_classes=6, n_bins=200,
+                       batch_sizes=tuple(range(1, 41)), tau_range=(-5.0, 150.0))
+    r = np.random.default_rng(seed)
+    wl = dataclasses.replace(wl, cost=r.uniform(0.0, 3.0, size=wl.cls.size))
+    steps = random_steps(wl, seed)
+    it = O.Iterator(wl, ctx)
+    it.set_queues(wl.queue_off, wl.cls, wl.deadline_ms, wl.now_ms, steps=steps)
+    got = it.run()
+    ora = oracle.iterate_workload(wl, steps=steps)
+    check(wl, got, ora)
+
+
 def test_iterate_bad_steps_are_a_data_error(ctx):
     wl = W.random_case(53, n_models=1, queue_lens=[4], tau_range=(10.0, 40.0))
     off = np.array([0, 1, 3, 4, 5], np.int64)
