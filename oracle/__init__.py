@@ -118,6 +118,16 @@ def _opt64(a):
     return None if a is None else np.ascontiguousarray(a, dtype=np.float64)
 
 
+def _map_models(fn, models, threads):
+    """fn(q) over the models, in order; with threads > 1 on a pool of host
+    threads (each call is one C function, which releases Python's lock)."""
+    if threads is None or threads <= 1 or len(models) <= 1:
+        return [fn(q) for q in models]
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(min(int(threads), len(models))) as ex:
+        return list(ex.map(fn, models))
+
+
 def score_model(counts, batch_sizes, bin_width_ms, cls, deadline_ms, now_ms, b_expo,
                 prefix_mode: int = 0, want_priority: bool = False, L=None, cost=None) -> dict:
     """All candidates of one model (see orloj_oracle_score_model)."""
@@ -155,16 +165,19 @@ def score_model(counts, batch_sizes, bin_width_ms, cls, deadline_ms, now_ms, b_e
 
 
 def score_workload(wl, prefix_mode: int = 0, models: Optional[Sequence[int]] = None,
-                   want_priority: bool = False, L=None) -> dict:
+                   want_priority: bool = False, L=None, threads: int = 1) -> dict:
     """Score every model of a workload (or the listed ones); outputs are
-    concatenated in model order, as the HIP library lays them out."""
+    concatenated in model order, as the HIP library lays them out.
+    ``threads`` > 1 scores the models on that many host threads."""
     models = list(range(wl.n_models)) if models is None else list(models)
-    parts = []
-    for q in models:
+
+    def one(q):
         m = wl.model(q)
-        parts.append(score_model(m["counts"], wl.batch_sizes, m["bin_width_ms"], m["cls"],
-                                 m["deadline_ms"], m["now_ms"], wl.b_expo, prefix_mode,
-                                 want_priority, L, cost=m["cost"]))
+        return score_model(m["counts"], wl.batch_sizes, m["bin_width_ms"], m["cls"],
+                           m["deadline_ms"], m["now_ms"], wl.b_expo, prefix_mode,
+                           want_priority, L, cost=m["cost"])
+
+    parts = _map_models(one, models, threads)
     cat = lambda k: (np.concatenate([p[k] for p in parts]) if parts else np.zeros(0))
     out = {k: cat(k) for k in ("finish_prob", "expected_finish", "expected_latency_ms", "score")}
     if want_priority:
@@ -214,13 +227,14 @@ def iterate_model(counts, batch_sizes, bin_width_ms, cls, deadline_ms, now_ms, b
 
 
 def iterate_workload(wl, weights=None, models: Optional[Sequence[int]] = None, L=None,
-                     steps=None) -> dict:
+                     steps=None, threads: int = 1) -> dict:
     """Algorithm 1 for every model of a workload (or the listed ones);
     per-request outputs concatenated in model order.  steps = (step_off over
-    the whole queue array, step_deadline_ms, step_cost) or None."""
+    the whole queue array, step_deadline_ms, step_cost) or None.
+    ``threads`` > 1 runs the models on that many host threads."""
     models = list(range(wl.n_models)) if models is None else list(models)
-    parts = []
-    for q in models:
+
+    def one(q):
         m = wl.model(q)
         st = None
         if steps is not None:
@@ -228,10 +242,12 @@ def iterate_workload(wl, weights=None, models: Optional[Sequence[int]] = None, L
             off = np.asarray(steps[0], np.int64)
             lo, hi = int(off[a]), int(off[b])
             st = (off[a:b + 1] - lo, np.asarray(steps[1])[lo:hi], np.asarray(steps[2])[lo:hi])
-        parts.append(iterate_model(m["counts"], wl.batch_sizes, m["bin_width_ms"], m["cls"],
-                                   m["deadline_ms"], m["now_ms"], wl.b_expo,
-                                   None if weights is None else weights[q], L, cost=m["cost"],
-                                   steps=st))
+        return iterate_model(m["counts"], wl.batch_sizes, m["bin_width_ms"], m["cls"],
+                             m["deadline_ms"], m["now_ms"], wl.b_expo,
+                             None if weights is None else weights[q], L, cost=m["cost"],
+                             steps=st)
+
+    parts = _map_models(one, models, threads)
     cat = lambda k: (np.concatenate([p[k] for p in parts]) if parts else np.zeros(0))
     return dict(timed_out=cat("timed_out").astype(np.int32), score=cat("score"),
                 cand_bs=np.array([p["cand_bs"] for p in parts], np.int32),
@@ -297,16 +313,20 @@ def score_model_affine(counts_ck, batch_sizes, bin_width_ms, c0_ms, c1, cls, dea
     return out
 
 
-def score_workload_affine(wl, c0_ms, c1, prefix_mode: int = 0, models=None, L=None) -> dict:
+def score_workload_affine(wl, c0_ms, c1, prefix_mode: int = 0, models=None, L=None,
+                          threads: int = 1) -> dict:
     """Affine mode over a workload whose counts are [M][C][K] (batch-size
-    independent); outputs concatenated in model order."""
+    independent); outputs concatenated in model order.  ``threads`` > 1
+    scores the models on that many host threads."""
     models = list(range(wl.n_models)) if models is None else list(models)
-    parts = []
-    for q in models:
+
+    def one(q):
         m = wl.model(q)
-        parts.append(score_model_affine(m["counts"], wl.batch_sizes, m["bin_width_ms"], c0_ms[q],
-                                        c1[q], m["cls"], m["deadline_ms"], m["now_ms"], wl.b_expo,
-                                        prefix_mode, L=L, cost=m["cost"]))
+        return score_model_affine(m["counts"], wl.batch_sizes, m["bin_width_ms"], c0_ms[q],
+                                  c1[q], m["cls"], m["deadline_ms"], m["now_ms"], wl.b_expo,
+                                  prefix_mode, L=L, cost=m["cost"])
+
+    parts = _map_models(one, models, threads)
     cat = lambda k: (np.concatenate([p[k] for p in parts]) if parts else np.zeros(0))
     out = {k: cat(k) for k in ("finish_prob", "expected_finish", "expected_latency_ms", "score")}
     out["sel_n"] = np.array([p["sel_n"] for p in parts], np.int32)

@@ -270,8 +270,7 @@ struct ScoreArgs {
 // stay in cache, and keep every row load a plain global load.
 constexpr int kFillFloats = 32;
 
-// Per-member lookup plan, built once per workgroup in LDS (it depends on
-// the deadline only, not on the step).
+// Per-member lookup plan (it depends on the deadline only, not on the step).
 //
 // The bins are swept in panels of 64 CPL bins (one chunk of CPL
 // consecutive bins per lane); a member with deadline bin k is handled in the
@@ -282,26 +281,31 @@ constexpr int kFillFloats = 32;
 //   W     = Z at the last bin of panel hp-1   (discounted prefix carried in)
 //   gl    = G at the last bin of panel hp-1
 //   A[]   = in-panel discounted scan of the lane chunk totals
-//   g[], zq[]  snapshot of G and of each chunk's quarter-end prefixes
+//   g[], zq[]  snapshot of G (fp64) and of each chunk's quarter-end prefixes
 // and assembles
-//   G(x_k)     = f[o0]
-//   G(x_{k+1}) = f[o1]
-//   Z(k-2) = cW W + cG gl + cA f[oa] + fq f[oz] + sum_r wq[r] f[o4 + r]
-//   P   = G(x_k) + theta (G(x_{k+1}) - G(x_k))
+//   G(x_k)     = g[o0]
+//   G(x_{k+1}) = g[o1]
+//   Z(k-2) = cW W + cG gl + cA f[oa] + fq f[oz] + z4
+//   z4     = the in-quarter discounted prefix of g[o4 + 0 .. rq] (Horner)
+//   P   = G(x_k) + theta (G(x_{k+1}) - G(x_k))          (fp64)
 //   num = cg (G(x_k) - (1 - d) Z(k-2)) + psi (G(x_{k+1}) - G(x_k))
-// where f is the float area of the workgroup's LDS (g, zq, A and three
-// constant slots: 0, 1 and gl, the last written at every scoring step).  The
-// plan resolves every case into an offset: G(x_k) is gl when bin k-1 lies
-// in the previous panel, 0 when k = 0; both G values are 0 when the deadline
-// has passed and 1 when it lies beyond the grid; a term the member does not
-// need has weight 0 and reads any finite slot.  So the lookup takes no
-// branch and no select.
+// where g is the fp64 area of the workgroup's LDS (the snapshot and three
+// constant slots: 0, 1 and gl, the last written at every scoring step) and
+// f its float area (zq, A and a zero).  The plan resolves every case into an
+// offset: G(x_k) is gl when bin k-1 lies in the previous panel, 0 when
+// k = 0; both G values are 0 when the deadline has passed and 1 when it lies
+// beyond the grid; a term the member does not need has weight 0 and reads a
+// finite slot.  So the lookup takes no branch.  P and the expected finish
+// count are formed in fp64 from the fp64 snapshot and an fp64 theta (a
+// float pair); the priority's terms are fp32.  A plan is 48 bytes, so that
+// 64 of them and the fp64 snapshot of a 1024-bin panel leave room for
+// twelve waves per compute unit.
 constexpr int kMaxPanels = 63;   // panels per row (their first members sit in one lane each)
 
 struct Member {
-    int cls;        // class id (clamped into range)
-    int16_t hp;     // home panel
-    uint16_t o0;    // LDS byte offsets (into the float area) of G(x_k),
+    uint8_t hp;     // home panel
+    uint8_t rq;     // bin k-2's place in its quarter (kNoQuarter: no quarter term)
+    uint16_t o0;    // LDS byte offsets of G(x_k),
     uint16_t o1;    //   G(x_{k+1}),
     uint16_t o4;    //   the quarter holding bin k-2,
     uint16_t oz;    //   the quarter-end prefix before that quarter,
@@ -310,12 +314,14 @@ struct Member {
     float cG;       // weight of gl
     float cA;       // weight of f[oa]
     float fq;       // weight of f[oz]
-    float wq[4];    // weights of the quarter's G values
-    float theta;    // position inside bin k
+    float theta;    // position inside bin k (rounded to fp32) ...
+    float thlo;     //   ... and the rest of the fp64 position
     float cg;       // gamma exp(-b theta w), or gamma exp(-b (tau - K w))
     float psi;      // (1 - exp(-b theta w)) / (b w)
     float cost;     // the request's miss cost (weights its priority)
 };
+static_assert(sizeof(Member) == 48, "member plan size");
+constexpr int kNoQuarter = 0xff;
 
 template <int CPL>
 struct Quarters {
@@ -323,30 +329,37 @@ struct Quarters {
     static constexpr int NQ = CPL / QW;            // quarters per lane chunk
 };
 
-// LDS layout of one workgroup (one wave):
-//   g[64 CPL]   snapshot of G over the current panel (float4-interleaved)
-//   zq[64 NQ]   quarter-end discounted prefixes of each lane chunk
-//   A[64]       in-panel discounted scan of the lane chunk totals
-//   k[4]        constant slots: 0, 1, gl (G carried in), unused
-//   mlo[]       first member of each panel
-//   mem[maxcap] Member
+// LDS layout of one workgroup (one wave), byte offsets:
+//   GD  g[64 CPL]   snapshot of G over the current panel, fp64; pairs of
+//                   bins interleaved (bins j, j+1 of lane l at pair
+//                   (j/2) 64 + l), so each lane writes 16 consecutive bytes
+//   KD  k[4]        constant slots (fp64): 0, 1, gl (G carried in), unused
+//   ZQ  zq[64 NQ]   quarter-end discounted prefixes of each lane chunk (f32)
+//   AA  A[64]       in-panel discounted scan of the lane chunk totals (f32)
+//   FZ  4 zeros     (f32) what a weight-0 float term reads
+//   MEM mem[maxcap] Member plans
 template <int CPL>
-__host__ __device__ constexpr int score_const_slot() {   // float index of k[0]
-    return 64 * CPL + 64 * Quarters<CPL>::NQ + 64;
-}
+struct ScoreLds {
+    static constexpr int GD = 0;
+    static constexpr int KD = 8 * 64 * CPL;
+    static constexpr int ZQ = KD + 32;
+    static constexpr int AA = ZQ + 4 * 64 * Quarters<CPL>::NQ;
+    static constexpr int FZ = AA + 4 * 64;
+    static constexpr int MEM = FZ + 16;
+    static_assert(MEM % 16 == 0 && MEM < 65536, "LDS layout");
+};
 template <int CPL>
-__host__ __device__ constexpr size_t score_fixed_bytes() {
-    return 4 * ((size_t)score_const_slot<CPL>() + 4 + kMaxPanels + 1);
-}
+__host__ __device__ constexpr size_t score_fixed_bytes() { return (size_t)ScoreLds<CPL>::MEM; }
 __host__ __device__ constexpr size_t score_bytes_per_member() { return sizeof(Member); }
 
+// Byte offset of the snapshot's bin r (bin offset inside the panel).
 template <int CPL>
-__device__ __forceinline__ int snap_index(int r) {   // r: bin offset inside the panel
-    if constexpr (CPL >= 4) {
+__device__ __forceinline__ int snap_byte(int r) {
+    if constexpr (CPL >= 2) {
         const int l = r / CPL, j = r - l * CPL;
-        return ((j >> 2) * 64 + l) * 4 + (j & 3);
+        return 8 * (((j >> 1) * 64 + l) * 2 + (j & 1));
     } else {
-        return r;
+        return 8 * r;
     }
 }
 
@@ -460,12 +473,12 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     using Q = Quarters<CPL>;
     constexpr int PW = 64 * CPL;                   // bins per panel
     extern __shared__ __align__(16) unsigned char smem_raw[];
-    float* s_g = reinterpret_cast<float*>(smem_raw);
-    float* s_zq = s_g + 64 * CPL;
-    float* s_A = s_zq + 64 * Q::NQ;
-    float* s_k = s_A + 64;                                  // constant slots
-    int* s_mlo = reinterpret_cast<int*>(s_k + 4);           // kMaxPanels + 1 ints
-    Member* s_mem = reinterpret_cast<Member*>(s_mlo + kMaxPanels + 1);
+    using L = ScoreLds<CPL>;
+    double* s_kd = reinterpret_cast<double*>(smem_raw + L::KD);   // constant slots
+    float* s_zq = reinterpret_cast<float*>(smem_raw + L::ZQ);
+    float* s_A = reinterpret_cast<float*>(smem_raw + L::AA);
+    float* s_fz = reinterpret_cast<float*>(smem_raw + L::FZ);
+    Member* s_mem = reinterpret_cast<Member*>(smem_raw + L::MEM);   // CR > 1 only
     const int maxcap = a.maxcap;
 
     const int lane = threadIdx.x;
@@ -522,37 +535,39 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     const float gamma = (float)(-expm1(-bw) / bw);   // (1 - d) / (b w)
     const float omd = (float)(-expm1(-bw));          // 1 - d
 
-    // ---- member lookup plans (fp64 time relative to now); the last chunk
-    // checks every member
-    for (int m = lane; m < n1; m += 64) {
+    // ---- member lookup plans (fp64 time relative to now).  `check` flags
+    // the member's data errors (once per member and workgroup).
+    auto make_plan = [&](int m, bool check) -> Member {
         int c = a.cls[q0 + m];
         const double D = a.deadline[q0 + m];
-        int flag = 0;
-        if (c < 0 || c >= a.C) { flag |= kErrClassRange; c = 0; }
-        if (isnan(D)) flag |= kErrDeadlineNaN;
-        if (m > 0 && D < a.deadline[q0 + m - 1]) flag |= kErrUnsorted;
-        if (m == 0 && isnan(nowq)) flag |= kErrNowNaN;
-        if (m == 0 && !(wq > 0.0 && wq < HUGE_VAL)) flag |= kErrWidth;
-        if (m == 0 && !aok) flag |= kErrAffine;
         double cm = a.cost ? a.cost[q0 + m] : 1.0;
-        if (!(cm >= 0.0 && cm < HUGE_VAL)) { flag |= kErrCost; cm = 0.0; }
-        if (flag) atomicOr(a.err, flag);
+        if (check) {
+            int flag = 0;
+            if (c < 0 || c >= a.C) flag |= kErrClassRange;
+            if (isnan(D)) flag |= kErrDeadlineNaN;
+            if (m > 0 && D < a.deadline[q0 + m - 1]) flag |= kErrUnsorted;
+            if (m == 0 && isnan(nowq)) flag |= kErrNowNaN;
+            if (m == 0 && !(wq > 0.0 && wq < HUGE_VAL)) flag |= kErrWidth;
+            if (m == 0 && !aok) flag |= kErrAffine;
+            if (!(cm >= 0.0 && cm < HUGE_VAL)) flag |= kErrCost;
+            if (flag) atomicOr(a.err, flag);
+        }
+        if (c < 0 || c >= a.C) c = 0;
+        if (!(cm >= 0.0 && cm < HUGE_VAL)) cm = 0.0;
         Member mb;
-        mb.cls = c;
         mb.cost = (float)cm;
-        // float indices into the LDS float area; kZ reads 0, kZ + 1 reads 1,
-        // kZ + 2 reads gl
-        constexpr int kZ = score_const_slot<CPL>();
-        int hp = 0, o0 = kZ, o1 = kZ, o4 = 0, oz = kZ, oa = kZ;
+        mb.rq = (uint8_t)kNoQuarter;
+        // byte offsets: KD reads 0, KD + 8 reads 1, KD + 16 reads gl; FZ
+        // reads a float 0
+        int hp = 0, o0 = L::KD, o1 = L::KD, o4 = 0, oz = L::FZ, oa = L::FZ;
         mb.cW = mb.cG = mb.cA = mb.fq = 0.0f;
-        mb.wq[0] = mb.wq[1] = mb.wq[2] = mb.wq[3] = 0.0f;
-        mb.theta = mb.cg = mb.psi = 0.0f;
+        mb.theta = mb.thlo = mb.cg = mb.psi = 0.0f;
         const double tau = D - nowq - c0q;
         int kz = -1;   // bin whose discounted prefix Z the priority needs
         if (tau > 0.0 && wok) {
             const double u = tau / w;
             if (u >= (double)K) {                  // beyond the grid: P = 1
-                o0 = o1 = kZ + 1;
+                o0 = o1 = L::KD + 8;
                 mb.cg = gamma * (float)exp(-b * (tau - (double)K * w));
                 hp = NP - 1;
                 kz = K - 2;
@@ -562,10 +577,11 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                 const int k = (int)kf;
                 hp = k / PW;
                 mb.theta = (float)th;
+                mb.thlo = (float)(th - (double)mb.theta);
                 mb.cg = gamma * (float)exp(-b * th * w);
                 mb.psi = (float)(-expm1(-b * th * w) / bw);
-                o1 = snap_index<CPL>(k - hp * PW);
-                if (k >= 1) o0 = k - 1 >= hp * PW ? snap_index<CPL>(k - 1 - hp * PW) : kZ + 2;
+                o1 = snap_byte<CPL>(k - hp * PW);
+                if (k >= 1) o0 = k - 1 >= hp * PW ? snap_byte<CPL>(k - 1 - hp * PW) : L::KD + 16;
                 kz = k - 2;
             }
         }
@@ -576,17 +592,15 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                 const int qq = j / Q::QW, rq = j - qq * Q::QW;
                 mb.cW = hp > 0 ? exp2f(log2d * (float)(kz - p0 + 1)) : 0.0f;
                 if (l > 0) {
-                    oa = 64 * CPL + 64 * Q::NQ + l - 1;
+                    oa = L::AA + 4 * (l - 1);
                     mb.cA = exp2f(log2d * (float)(j + 1));
                 }
                 if (qq > 0) {
-                    oz = 64 * CPL + l * Q::NQ + qq - 1;
+                    oz = L::ZQ + 4 * (l * Q::NQ + qq - 1);
                     mb.fq = exp2f(log2d * (float)(rq + 1));
                 }
-                o4 = snap_index<CPL>(r - rq);      // first bin of the quarter
-#pragma unroll
-                for (int rr = 0; rr < 4; ++rr)
-                    mb.wq[rr] = rr <= rq ? exp2f(log2d * (float)(rq - rr)) : 0.0f;
+                o4 = snap_byte<CPL>(r - rq);       // first bin of the quarter
+                mb.rq = (uint8_t)rq;
             } else if (kz == p0 - 1) {             // last bin of the previous panel
                 mb.cW = 1.0f;
             } else {                               // kz = p0 - 2: step back one bin
@@ -594,19 +608,23 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                 mb.cG = -(float)exp(bw);
             }
         }
-        mb.hp = (int16_t)hp;
-        mb.o0 = (uint16_t)(4 * o0); mb.o1 = (uint16_t)(4 * o1); mb.o4 = (uint16_t)(4 * o4);
-        mb.oz = (uint16_t)(4 * oz); mb.oa = (uint16_t)(4 * oa);
-        s_mem[m] = mb;
-    }
+        mb.hp = (uint8_t)hp;
+        mb.o0 = (uint16_t)o0; mb.o1 = (uint16_t)o1; mb.o4 = (uint16_t)o4;
+        mb.oz = (uint16_t)oz; mb.oa = (uint16_t)oa;
+        return mb;
+    };
+    for (int m = lane; m < n1; m += 64) s_mem[m] = make_plan(m, true);
     if (lane == 0) {
-        s_k[0] = 0.0f;
-        s_k[1] = 1.0f;
-        s_k[2] = 0.0f;
-        s_k[3] = 0.0f;
+        s_kd[0] = 0.0;
+        s_kd[1] = 1.0;
+        s_kd[2] = 0.0;
+        s_kd[3] = 0.0;
     }
+    if (lane < 4) s_fz[lane] = 0.0f;
     wave_lds_fence();
-    // first member of each panel (home panels are non-decreasing in m)
+    // first member of each panel p <= NP in lane p (home panels are
+    // non-decreasing in m); lanes past NP hold n1
+    int mlo_r = n1;
     for (int p = 0; p <= NP; ++p) {
         int cnt = 0;
         for (int m0 = 0; m0 < n1; m0 += 64) {
@@ -614,7 +632,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             const bool below = m < n1 && s_mem[m].hp < p;
             cnt += __builtin_popcountll(__ballot(below));
         }
-        if (lane == 0) s_mlo[p] = cnt;
+        mlo_r = lane == p ? cnt : mlo_r;
     }
 
     // ---- scan constants
@@ -624,6 +642,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     const float w15 = exp2_hw(log2d * (float)(CPL * ((lane & 15) + 1)));
     const float w31 = exp2_hw(log2d * (float)(CPL * (lane >= 32 ? lane - 31 : 0)));
     const float dQ = exp2_hw(log2d * (float)Q::QW);
+    const float dq1 = exp2f(log2d);                   // d in fp32
     const float dPW = exp2_hw(log2d * (float)PW);
 
     int64_t cand = a.cand_off[q], prob = a.prob_off[q];
@@ -635,7 +654,6 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     // rows of this (model, batch size); affine mode has one set per model
     const size_t qb = AFF ? (size_t)q : (size_t)q * (size_t)a.nbs + (size_t)bi;
     const float* tab_qb = a.tab + qb * (size_t)a.C * (size_t)K;
-    wave_lds_fence();
 
     // class and support of member n in lane n % 64 of register n / 64;
     // first member of each panel in lane p
@@ -643,13 +661,12 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     const int32_t* sup_qb = a.sup ? a.sup + qb * (size_t)a.C * 2 : nullptr;
 #pragma unroll
     for (int r = 0; r < CR; ++r) {
-        const int m = min(r * 64 + lane, n1 - 1);
-        const int c = s_mem[m].cls;
+        int c = a.cls[q0 + min(r * 64 + lane, n1 - 1)];
+        if (c < 0 || c >= a.C) c = 0;                     // flagged by its plan
         cls_r.v[r] = __builtin_bit_cast(float, c);
         lo_r.v[r] = __builtin_bit_cast(float, sup_qb ? sup_qb[2 * c] : 0);
         hi_r.v[r] = __builtin_bit_cast(float, sup_qb ? sup_qb[2 * c + 1] : K);
     }
-    const int mlo_r = s_mlo[min(lane, NP)];
     // Home panel of the last member (the latest deadline): past it no member
     // needs G or the discounted prefix, only E[L_B] needs the sums of 1 - G.
     // The main loop walks the panels up to LASTP; the tabulated mode then
@@ -674,8 +691,8 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         load_chunk<CPL, EXACT>(v, src, lim);
     };
 
-    LaneCarry<CR> cW, cGl, cN;
-    LaneCarry64<CR> cE, cP;
+    LaneCarry<CR> cW, cN;
+    LaneCarry64<CR> cE, cP, cGl;
     cW.zero(); cGl.zero(); cN.zero(); cE.zero(); cP.zero();
 
     // One flat loop over (panel p, step n), n fastest, padded at the end to a
@@ -710,7 +727,8 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     bool pass_zero = false;                  // G == 0 on every bin of this pass's panel
     Member pass_mb;                          // CR == 1: this lane's member of the pass
     bool pass_valid = false;
-    float etot_prev = 0.0f, T_prev = 0.0f, gl_prev = 0.0f;
+    float etot_prev = 0.0f, T_prev = 0.0f;
+    double gl_prev = 0.0;
 
     for (int it0 = 0; it0 < iters; it0 += PF) {
 #pragma unroll
@@ -768,9 +786,11 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             load_step(buf[i], pf_n, pf_p * PW + base, zero_after && pf_p == p);
             if (++pf_n == n1) { pf_n = 0; pf_p = min(pf_p + 1, NPW - 1); }
             if (p < NPW && real) {                        // else a ghost or warm-up iteration
-                float etot = etot_prev, T = T_prev, glast_here = gl_prev;
+                float etot = etot_prev, T = T_prev;
+                double glast_here = gl_prev;
                 const float Win = cW.get(n);              // carries in from the previous
-                const float glin = cGl.get(n);            // panel pass (zero in the first)
+                const double glin64 = cGl.get(n);         // panel pass (zero in the first)
+                const float glin = (float)glin64;
                 float A = 0.0f;
                 if (!skip) {
                     // quarter ends of the in-chunk discounted prefix, and its total
@@ -793,58 +813,69 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                         const float e = (float)((double)CPL - gsum);
                         etot = lane63(wave_scan_sum(e));
                     }
-                    glast_here = lane63((float)Gacc[CPL - 1]);
+                    glast_here = lane63(Gacc[CPL - 1]);
                     etot_prev = etot; gl_prev = glast_here;
 
                     if (due) {
-                        // snapshot of G over the panel (rounded again from the
-                        // fp64 values, rather than kept live through the scans)
-                        float gv[CPL];
+                        // snapshot of G over the panel, fp64, pairs of bins
+                        // interleaved over the lanes (16-byte writes)
+                        if constexpr (CPL >= 2) {
 #pragma unroll
-                        for (int j = 0; j < CPL; ++j) gv[j] = (float)Gacc[j];
-                        if constexpr (CPL >= 4) {
-#pragma unroll
-                            for (int j = 0; j < CPL; j += 4) {
-                                const int slot = ((j >> 2) * 64 + lane) * 4;
-                                *reinterpret_cast<float4*>(s_g + slot) =
-                                    make_float4(gv[j], gv[j + 1], gv[j + 2], gv[j + 3]);
+                            for (int j = 0; j < CPL; j += 2) {
+                                const int pair = (j >> 1) * 64 + lane;
+                                *reinterpret_cast<double2*>(smem_raw + L::GD + 16 * pair) =
+                                    make_double2(Gacc[j], Gacc[j + 1]);
                             }
                         } else {
-#pragma unroll
-                            for (int j = 0; j < CPL; ++j) s_g[base + j] = gv[j];
+                            *reinterpret_cast<double*>(smem_raw + L::GD + 8 * lane) = Gacc[0];
                         }
 #pragma unroll
                         for (int qq = 0; qq < Q::NQ; ++qq) s_zq[lane * Q::NQ + qq] = zqv[qq];
                         s_A[lane] = A;
-                        if (lane == 0) s_k[2] = glin;
+                        if (lane == 0) s_kd[2] = glin64;
                         wave_lds_fence();
                         double pP = 0.0;
                         float pN = 0.0f;
                         const int nn = n + 1;
                         auto score_member = [&](const Member& mb, int m) {
-                            const unsigned char* f = reinterpret_cast<const unsigned char*>(s_g);
-                            auto at = [&](int off) { return *reinterpret_cast<const float*>(f + off); };
-                            const float gk = at(mb.o0);
-                            const float gk1 = at(mb.o1);
-                            const float al0 = at(mb.oa);
-                            const float zq0 = at(mb.oz);
+                            const unsigned char* f = smem_raw;
+                            auto atf = [&](int off) { return *reinterpret_cast<const float*>(f + off); };
+                            auto atd = [&](int off) { return *reinterpret_cast<const double*>(f + off); };
+                            const double gk64 = atd(mb.o0);
+                            const double gk164 = atd(mb.o1);
+                            const float al0 = atf(mb.oa);
+                            const float zq0 = atf(mb.oz);
+                            // the quarter's G values (fp32 terms of the priority)
                             float g4[4];
                             if constexpr (Q::QW == 4) {
-                                const float4 t4 = *reinterpret_cast<const float4*>(f + mb.o4);
-                                g4[0] = t4.x; g4[1] = t4.y; g4[2] = t4.z; g4[3] = t4.w;
+                                const double2 t0 = *reinterpret_cast<const double2*>(f + mb.o4);
+                                const double2 t1 = *reinterpret_cast<const double2*>(f + mb.o4 + 16 * 64);
+                                g4[0] = (float)t0.x; g4[1] = (float)t0.y;
+                                g4[2] = (float)t1.x; g4[3] = (float)t1.y;
+                            } else if constexpr (Q::QW == 2) {
+                                const double2 t0 = *reinterpret_cast<const double2*>(f + mb.o4);
+                                g4[0] = (float)t0.x; g4[1] = (float)t0.y;
+                                g4[2] = g4[3] = 0.0f;
                             } else {
-#pragma unroll
-                                for (int r = 0; r < 4; ++r) g4[r] = r < Q::QW ? at(mb.o4 + 4 * r) : 0.0f;
+                                g4[0] = (float)atd(mb.o4);
+                                g4[1] = g4[2] = g4[3] = 0.0f;
                             }
-                            float zin = mb.fq * zq0;
+                            // discounted prefix of the quarter up to bin k-2
+                            // (0 when the member needs no quarter term)
+                            const int rq = mb.rq;
+                            float z4 = rq <= 3 ? g4[0] : 0.0f;
 #pragma unroll
-                            for (int r = 0; r < 4; ++r) zin = fmaf(mb.wq[r], g4[r], zin);
+                            for (int r = 1; r < 4; ++r) z4 = r <= rq && rq <= 3 ? fmaf(z4, dq1, g4[r]) : z4;
+                            const float zin = fmaf(mb.fq, zq0, z4);
                             const float Zv = fmaf(mb.cW, Win, fmaf(mb.cG, glin, fmaf(mb.cA, al0, zin)));
+                            const float gk = (float)gk64, gk1 = (float)gk164;
                             const float h = gk1 - gk;
-                            const float P = fmaf(mb.theta, h, gk);
+                            // P in fp64: the expected finish count sums it
+                            const double th = (double)mb.theta + (double)mb.thlo;
+                            const double P64 = fma(th, gk164 - gk64, gk64);
                             const float num = mb.cost * fmaf(mb.cg, fmaf(-omd, Zv, gk), h * mb.psi);
-                            a.P[prob + (int64_t)n * nn / 2 + m] = P;
-                            pP += (double)P;
+                            a.P[prob + (int64_t)n * nn / 2 + m] = (float)P64;
+                            pP += P64;
                             pN += num;
                         };
                         if constexpr (CR == 1) {

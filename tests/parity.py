@@ -94,3 +94,17 @@ def compare(wl, gpu: dict, ora: dict, mode: int = 0, models=None, cand_off=None,
         check_selection(wl, q, mode, po["score"],
                         (int(gpu["sel_n"][q]), int(gpu["sel_bs"][q])))
     return err
+
+
+_MADE = {}
+
+
+def make_cached(config_id: int, slo_scale: float = 1.0, workers: int = 16):
+    """workloads.make(config_id, slo_scale=...), generated once per test
+    session (configurations 4 and 5 take seconds).  Callers must not modify
+    the returned workload."""
+    from paper_2209_00159_amd import workloads as W
+    key = (config_id, float(slo_scale))
+    if key not in _MADE:
+        _MADE[key] = W.make(config_id, workers=workers, slo_scale=slo_scale)
+    return _MADE[key]

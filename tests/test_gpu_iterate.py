@@ -2,12 +2,14 @@
 through the C ABI against the oracle: timed-out flags and candidate batch
 sizes bit-exact, priorities within the score bar, and the popped batch a
 valid top-s under the oracle's priorities (ties within the bar aside)."""
+import os
 import sys
 
 import numpy as np
 import pytest
 
 import oracle
+import parity
 from paper_2209_00159_amd import orloj as O
 from paper_2209_00159_amd import workloads as W
 
@@ -60,10 +62,14 @@ def check(wl, got, ora):
     return err
 
 
+ORACLE_THREADS = max(1, min(16, len(os.sched_getaffinity(0))))
+
+
 def run(wl, ctx, weights=None, b_expo=None):
     it = O.Iterator(wl, ctx, class_weights=weights)
     got = it.run(b_expo=b_expo)
-    ora = oracle.iterate_workload(wl if b_expo is None else _with_b(wl, b_expo), weights=weights)
+    ora = oracle.iterate_workload(wl if b_expo is None else _with_b(wl, b_expo), weights=weights,
+                                  threads=ORACLE_THREADS)
     return got, ora
 
 
@@ -155,11 +161,11 @@ def test_iterate_delay_rate(ctx, b):
     check(wl, got, ora)
 
 
-@pytest.mark.parametrize("cid,scale", [(1, 1.0), (1, 4.0), (2, 1.0), (2, 3.0), (3, 1.0), (4, 1.0),
-                                       (4, 3.0)])
+@pytest.mark.parametrize("cid,scale", [(1, 1.0), (1, 4.0), (2, 1.0), (2, 3.0), (3, 1.0), (3, 5.0),
+                                       (4, 1.0), (4, 3.0), (5, 1.0), (5, 4.0)])
 def test_iterate_configs(ctx, cid, scale):
     say(f"iterate config {cid} slo x{scale}")
-    wl = W.make(cid, workers=8, slo_scale=scale)
+    wl = parity.make_cached(cid, scale)
     got, ora = run(wl, ctx)
     say("  candidates", np.unique(got["cand_bs"]), "max |d score|", check(wl, got, ora))
 

@@ -5,7 +5,7 @@ Covers the CDF-table builder, scoring and selection on random ragged cases
 histograms, non-contiguous batch sizes, both prefix modes, a sweep of the
 delay rate b), on configurations 1-4 at full size (as specified and with
 relaxed SLOs), and on configuration 5 at full size in the launch the
-benchmark times, checked on sampled models.
+benchmark times, every model compared.
 """
 import os
 import sys
@@ -178,7 +178,7 @@ def test_delay_rate_sweep(ctx, b):
                                        (3, 5.0), (4, 1.0), (4, 3.0)])
 def test_config_full_size(ctx, cid, scale):
     say(f"config {cid} slo x{scale}")
-    wl = W.make(cid, workers=8, slo_scale=scale)
+    wl = parity.make_cached(cid, scale)
     sc, got = run_gpu(wl, ctx)
     ora = oracle.score_workload(wl)
     err = parity.compare(wl, got, ora)
@@ -188,31 +188,33 @@ def test_config_full_size(ctx, cid, scale):
         assert int((P > 0).sum()) >= min(1000, P.size // 2) and np.all(got["sel_n"] > 0)
 
 
+ORACLE_THREADS = max(1, min(16, len(os.sched_getaffinity(0))))
+
+
 @pytest.fixture(scope="module")
 def cfg5():
     say("generating config 5 (128 models x 64 batch sizes x 32 classes x 4096 bins)")
-    return W.make(5, workers=16)
+    return parity.make_cached(5)
 
 
-def test_config5_full_launch_sampled_models(ctx, cfg5):
-    wl = cfg5
-    say("config 5 full launch")
+# Configuration 5 at full size, in the launch the benchmark times, compared
+# with the oracle on every one of its 128 models: as specified, and at x4
+# SLOs, where most member slots have 0 < P < 1.
+@pytest.mark.parametrize("scale", [1.0, 4.0])
+def test_config5_full_launch_all_models(ctx, cfg5, scale):
+    wl = parity.make_cached(5, scale)
+    say(f"config 5 full launch, slo x{scale}, all {wl.n_models} models")
     sc, got = run_gpu(wl, ctx)
-    models = [0, 57, 127]
-    sub = wl.subset(models)
-    ora = oracle.score_workload(sub)
-    err = parity.compare(wl, got, ora, models=models, cand_off=sc.h_cand_off,
-                         prob_off=sc.h_prob_off)
+    ora = oracle.score_workload(wl, threads=ORACLE_THREADS)
+    err = parity.compare(wl, got, ora)
     say("  max errors", err)
-    # properties that hold at any size, over every model
     P = got["finish_prob"]
     assert np.all((P >= 0) & (P <= 1))
-    # the timed state is not a trivial one: members can finish, models pick batches
+    # the state is not a trivial one: members can finish, models pick batches
     assert (P > 0).mean() > 0.1 and (got["sel_n"] > 0).mean() > 0.9
     assert np.all(got["expected_latency_ms"] >= 0.5 * wl.bin_width_ms[0] * (1 - 1e-6))
-    for q in range(wl.n_models):
-        E = got["expected_finish"][sc.h_cand_off[q]:sc.h_cand_off[q + 1]]
-        assert np.all(E >= -1e-6) and np.all(E <= 64 + 1e-6)
+    if scale > 1.0:
+        assert ((P > 0) & (P < 1)).mean() > 0.3
 
 
 def test_config5_trimmed_and_full_reads_agree(ctx, cfg5):
@@ -221,13 +223,6 @@ def test_config5_trimmed_and_full_reads_agree(ctx, cfg5):
     _, on = run_gpu(wl, ctx, trim=True)
     _, off = run_gpu(wl, ctx, trim=False)
     assert_same_bits(on, off)
-
-
-def test_config5_relaxed_slo_sampled(ctx):
-    wl = W.make(5, models=[3, 99], slo_scale=4.0)
-    say("config 5 relaxed SLO, 2 models")
-    sc, got = run_gpu(wl, ctx)
-    parity.compare(wl, got, oracle.score_workload(wl))
 
 
 # ---------------------------------------------------------------- errors and plumbing
