@@ -12,6 +12,7 @@
  *                           expected finish count, priority score
  *   orloj_score_candidates_affine  the same with the affine batch-latency
  *                           law c0 + c1 s l of §4.2.1 (one table per class)
+ *   orloj_score_candidates_affine_noalloc  the same, allocating nothing
  *   orloj_select_batch      highest-scoring candidate per model
  *   orloj_build_model_laws  model-wide batch laws for the scheduler iteration
  *   orloj_iterate           one Algorithm 1 iteration per model (drop phase,
@@ -64,6 +65,9 @@ enum orloj_prefix_mode { ORLOJ_PREFIX_TRIANGLE = 0, ORLOJ_PREFIX_RECT = 1 };
 #define ORLOJ_MAX_BINS 8192       /* histogram bins per table */
 #define ORLOJ_MAX_BATCH_SIZES 256 /* entries of the batch-size set */
 #define ORLOJ_MAX_PREFIX 256      /* longest prefix scored per batch size */
+/* Floats of the fixed scratch of orloj_score_candidates_affine_noalloc
+ * (4 MiB per device). */
+#define ORLOJ_NOALLOC_SCRATCH_FLOATS (1 << 20)
 
 typedef struct orloj_ctx orloj_ctx;
 
@@ -234,6 +238,34 @@ int orloj_score_candidates_affine(orloj_ctx *ctx, const orloj_grid *grid, const 
                                   const int64_t *d_cand_off, const int64_t *d_prob_off,
                                   float *d_finish_prob, double *d_expected_finish,
                                   float *d_expected_latency_ms, float *d_score);
+
+/*
+ * orloj_score_candidates_affine without any allocation, for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  Arguments, outputs and
+ * errors are those of orloj_score_candidates_affine, with the same kernels
+ * and the same bits; the per-(model, panel, prefix length) sums behind E[X]
+ * go to a fixed device array of ORLOJ_NOALLOC_SCRATCH_FLOATS floats instead
+ * of the context's grown block.  The library looks up that array's address
+ * on a device once (the first orloj_create on it) and each device keeps
+ * its array until the process ends.  A call needing more than
+ * M x ceil(K / 1024) x (the longest prefix) floats of it returns
+ * ORLOJ_E_UNSUPPORTED before any launch (configuration 5, 128 x 4 x 64,
+ * needs 32 768).  ORLOJ_E_HIP if the array is unavailable on the context's
+ * device.  Every entry a call reads is written earlier in the same call, so
+ * nothing needs clearing; but all calls on one device share the one array,
+ * so calls that may overlap on a device (other contexts, other streams,
+ * other threads) race and must be ordered by the caller.  The call itself
+ * makes no hipMalloc, hipFree or host-synchronising call.
+ */
+int orloj_score_candidates_affine_noalloc(orloj_ctx *ctx, const orloj_grid *grid,
+                                          const float *d_ccdf, const int32_t *d_support,
+                                          const double *d_c0_ms, const double *d_c1,
+                                          const orloj_queues *queues, double b_expo_per_ms,
+                                          int32_t prefix_mode, const int64_t *d_cand_off,
+                                          const int64_t *d_prob_off, float *d_finish_prob,
+                                          double *d_expected_finish,
+                                          float *d_expected_latency_ms, float *d_score);
 
 /*
  * Pick one batch per model (the scheduler pops the top batch, §3.2

@@ -31,6 +31,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 #include <type_traits>
 
@@ -2052,6 +2053,44 @@ hipError_t launch_cdf(const uint32_t* c, float* o, int32_t* sup, int64_t rows, i
 
 }  // namespace
 
+// Scratch of orloj_score_candidates_affine_noalloc: the per-(model, panel,
+// prefix length) sums of 1 - G that emax_kernel writes and score_kernel
+// reads, in a fixed device array instead of the context's grown block.  Each
+// device the library runs on holds its own copy until the process ends.  In
+// host code `scratch` names a host-side stand-in: kernels are given the
+// device address that hipGetSymbolAddress returns for the current device.
+constexpr size_t kNoAllocScratchFloats = ORLOJ_NOALLOC_SCRATCH_FLOATS;
+static __device__ __align__(256) float scratch[kNoAllocScratchFloats];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+bool g_scratch_done[kMaxScratchDevices];
+hipError_t g_scratch_err[kMaxScratchDevices];
+float* g_scratch_ptr[kMaxScratchDevices];
+
+// Device address of `scratch` on `device`, looked up once per device with
+// that device current (the caller has made it current).
+float* scratch_address(int device, hipError_t* err) {
+    if (device < 0 || device >= kMaxScratchDevices) {
+        *err = hipErrorInvalidDevice;
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_done[device]) {
+        void* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        g_scratch_err[device] = e;
+        g_scratch_ptr[device] = e == hipSuccess ? static_cast<float*>(ptr) : nullptr;
+        g_scratch_done[device] = true;
+    }
+    *err = g_scratch_err[device];
+    return g_scratch_ptr[device];
+}
+
+}  // namespace
+
 extern "C" {
 
 int orloj_create(orloj_ctx** out, int32_t hip_device, void* hip_stream) {
@@ -2065,6 +2104,8 @@ int orloj_create(orloj_ctx** out, int32_t hip_device, void* hip_stream) {
     ctx->d_fill = nullptr;
     ctx->d_work = nullptr;
     ctx->work_bytes = 0;
+    ctx->noalloc_scratch = nullptr;
+    ctx->noalloc_err = hipSuccess;
     ctx->msg[0] = 0;
     int n = 0;
     if (hipGetDeviceCount(&n) != hipSuccess || hip_device < 0 || hip_device >= n) {
@@ -2081,6 +2122,9 @@ int orloj_create(orloj_ctx** out, int32_t hip_device, void* hip_stream) {
     if (e == hipSuccess) e = hipMemset(ctx->d_err, 0, sizeof(int));
     if (e == hipSuccess) e = hipMalloc((void**)&ctx->d_fill, sizeof fill);
     if (e == hipSuccess) e = hipMemcpy(ctx->d_fill, fill, sizeof fill, hipMemcpyHostToDevice);
+    // the allocation-free scorer's scratch on this device (its failure only
+    // disables that entry point)
+    if (e == hipSuccess) ctx->noalloc_scratch = scratch_address(hip_device, &ctx->noalloc_err);
     if (e != hipSuccess) {
         if (ctx->d_err) (void)hipFree(ctx->d_err);
         if (ctx->d_fill) (void)hipFree(ctx->d_fill);
@@ -2290,11 +2334,15 @@ int ensure_work(orloj_ctx* ctx, size_t bytes) {
 
 // Validation and launch shared by the tabulated and the affine scorer
 // (d_c0 / d_c1 NULL: tabulated).
+// fixed_psum (affine mode only): a caller-fixed block of fixed_floats
+// floats for the panel sums instead of the context's grown one (no
+// allocation; ORLOJ_E_UNSUPPORTED when the call needs more).
 int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
                  const int32_t* d_support, const double* d_c0, const double* d_c1,
                  const orloj_queues* queues, double b_expo_per_ms, int32_t prefix_mode,
                  const int64_t* d_cand_off, const int64_t* d_prob_off, float* d_finish_prob,
-                 double* d_expected_finish, float* d_expected_latency_ms, float* d_score) {
+                 double* d_expected_finish, float* d_expected_latency_ms, float* d_score,
+                 float* fixed_psum = nullptr, size_t fixed_floats = 0) {
     if (!ctx) return ORLOJ_E_INVALID;
     int rc = check_grid(ctx, grid);
     if (rc) return rc;
@@ -2377,9 +2425,19 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
         const int64_t np = (grid->n_bins + 64 * cple - 1) / (64 * cple);
         if ((int64_t)M * np > 0x7fffffff)
             return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (model, panel) pairs");
-        rc = ensure_work(ctx, (size_t)M * (size_t)np * (size_t)maxcap * sizeof(float));
-        if (rc) return rc;
-        a.psum = (float*)ctx->d_work;
+        const size_t need = (size_t)M * (size_t)np * (size_t)maxcap;
+        if (fixed_psum) {
+            if (need > fixed_floats)
+                return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED,
+                                      "the call needs %zu scratch floats (models x panels x longest "
+                                      "prefix), the fixed scratch holds %zu",
+                                      need, fixed_floats);
+            a.psum = fixed_psum;
+        } else {
+            rc = ensure_work(ctx, need * sizeof(float));
+            if (rc) return rc;
+            a.psum = (float*)ctx->d_work;
+        }
         a.np_e = (int)np;
         switch (cple) {
             case 1: e = launch_emax<1>(a, ctx->stream); break;
@@ -2431,6 +2489,26 @@ int orloj_score_candidates_affine(orloj_ctx* ctx, const orloj_grid* grid, const 
     return score_common(ctx, grid, d_ccdf, d_support, d_c0_ms, d_c1, queues, b_expo_per_ms,
                         prefix_mode, d_cand_off, d_prob_off, d_finish_prob, d_expected_finish,
                         d_expected_latency_ms, d_score);
+}
+
+int orloj_score_candidates_affine_noalloc(orloj_ctx* ctx, const orloj_grid* grid,
+                                          const float* d_ccdf, const int32_t* d_support,
+                                          const double* d_c0_ms, const double* d_c1,
+                                          const orloj_queues* queues, double b_expo_per_ms,
+                                          int32_t prefix_mode, const int64_t* d_cand_off,
+                                          const int64_t* d_prob_off, float* d_finish_prob,
+                                          double* d_expected_finish,
+                                          float* d_expected_latency_ms, float* d_score) {
+    if (!ctx) return ORLOJ_E_INVALID;
+    if (grid && grid->n_models > 0 && (!d_c0_ms || !d_c1))
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "d_c0_ms / d_c1 is NULL");
+    if (!ctx->noalloc_scratch)
+        return orloj_ctx_fail(ctx, ORLOJ_E_HIP, "fixed scratch unavailable on device %d: %s",
+                              ctx->device, hipGetErrorString(ctx->noalloc_err));
+    return score_common(ctx, grid, d_ccdf, d_support, d_c0_ms, d_c1, queues, b_expo_per_ms,
+                        prefix_mode, d_cand_off, d_prob_off, d_finish_prob, d_expected_finish,
+                        d_expected_latency_ms, d_score, ctx->noalloc_scratch,
+                        kNoAllocScratchFloats);
 }
 
 int orloj_build_model_laws(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,

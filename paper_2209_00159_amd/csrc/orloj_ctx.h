@@ -17,6 +17,8 @@ struct orloj_ctx {
     float* d_fill;   // stand-in table entries: 16 zeros, 16 ones
     void* d_work;    // scratch of the affine scorer (grown on demand), or NULL
     size_t work_bytes;
+    float* noalloc_scratch;   // this device's fixed scratch array (NULL: unavailable)
+    hipError_t noalloc_err;   // why it is unavailable
     char msg[512];
 };
 

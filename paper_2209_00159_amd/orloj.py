@@ -80,7 +80,8 @@ _I64P = ctypes.POINTER(ctypes.c_int64)
 EXPORTS = ("orloj_create", "orloj_destroy", "orloj_set_stream", "orloj_set_score_chunk",
            "orloj_last_error", "orloj_sync",
            "orloj_build_cdfs", "orloj_output_sizes", "orloj_score_candidates",
-           "orloj_score_candidates_affine", "orloj_select_batch", "orloj_build_model_laws",
+           "orloj_score_candidates_affine", "orloj_score_candidates_affine_noalloc",
+           "orloj_select_batch", "orloj_build_model_laws",
            "orloj_iterate", "orloj_accumulate", "orloj_sched_create", "orloj_sched_destroy",
            "orloj_sched_admit", "orloj_sched_decide", "orloj_sched_queue_length",
            "orloj_simulate_trace")
@@ -119,6 +120,8 @@ def load(path: Optional[str] = None):
     L.orloj_score_candidates_affine.argtypes = [_VP, _GP, _VP, _VP, _VP, _VP, _QP, ctypes.c_double,
                                                 ctypes.c_int32, _VP, _VP, _VP, _VP, _VP, _VP]
     L.orloj_score_candidates_affine.restype = ctypes.c_int
+    L.orloj_score_candidates_affine_noalloc.argtypes = L.orloj_score_candidates_affine.argtypes
+    L.orloj_score_candidates_affine_noalloc.restype = ctypes.c_int
     L.orloj_select_batch.argtypes = [_VP, _GP, _QP, ctypes.c_int32, _VP, _VP, _VP, _VP, _VP]
     L.orloj_select_batch.restype = ctypes.c_int
     L.orloj_build_model_laws.argtypes = [_VP, _GP, _VP, _VP, ctypes.c_double, _VP, _VP, _VP]
@@ -313,14 +316,20 @@ class Scorer:
     def build(self):
         self.ctx.build_cdfs(self.counts, self.ccdf, self.support)
 
-    def score(self, b_expo: Optional[float] = None):
+    def score(self, b_expo: Optional[float] = None, noalloc: bool = False):
+        """Enqueue the scoring call; ``noalloc`` (affine workloads only) calls
+        orloj_score_candidates_affine_noalloc, which allocates nothing."""
         b = self.wl.b_expo if b_expo is None else b_expo
         c = self.ctx
         sup = _ptr(self.support) if self.trim else None
         outs = (_ptr(self.d_cand_off), _ptr(self.d_prob_off), _ptr(self.finish_prob),
                 _ptr(self.expected_finish), _ptr(self.expected_latency), _ptr(self.score_out))
+        if noalloc and not self.affine:
+            raise ValueError("the allocation-free entry point scores affine workloads")
         if self.affine:
-            c._check(c.L.orloj_score_candidates_affine(
+            fn = (c.L.orloj_score_candidates_affine_noalloc if noalloc
+                  else c.L.orloj_score_candidates_affine)
+            c._check(fn(
                 c.ctx, ctypes.byref(self.grid), _ptr(self.ccdf), sup, _ptr(self.c0), _ptr(self.c1),
                 ctypes.byref(self.queues), float(b), self.mode, *outs))
         else:
