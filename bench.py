@@ -150,10 +150,11 @@ def valid_candidates(wl):
     return sum(min(int(s), wl.queue_len(q)) for q in range(wl.n_models) for s in wl.batch_sizes)
 
 
-def _oracle_over_models(wl, affine, budget_s, threads):
-    """The oracle on the workload's models, `threads` host threads at a
-    time (the C oracle releases the GIL), each thread taking the next model
-    until about budget_s seconds have passed.  Returns (models, evals, s)."""
+def _oracle_leg(wl, affine, budget_s, threads):
+    """One timed leg of the oracle on the workload's models: `threads` host
+    threads at a time (the C oracle releases the GIL; threads = 1 runs in
+    the calling thread), each taking the next model until about budget_s
+    seconds have passed.  Returns (models, evals, seconds)."""
     import threading
     from concurrent.futures import ThreadPoolExecutor
 
@@ -180,37 +181,66 @@ def _oracle_over_models(wl, affine, budget_s, threads):
                 state["done"] += 1
                 state["evals"] += ev
 
-    with ThreadPoolExecutor(threads) as ex:
-        for f in [ex.submit(worker) for _ in range(threads)]:
-            f.result()
+    if threads == 1:
+        worker()
+    else:
+        with ThreadPoolExecutor(threads) as ex:
+            for f in [ex.submit(worker) for _ in range(threads)]:
+                f.result()
     return state["done"], state["evals"], time.perf_counter() - t0
 
 
-def cpu_baseline(config_id, max_models, budget_s=10.0, affine=False, threads=16):
-    """The oracle, as it stands, on the models of the same state: once on
-    one host thread and once on `threads` host threads (the host CPU share
-    of one GPU), each for about budget_s seconds.  value = the all-threads
-    evals/s; the one-thread figure is kept beside it."""
+def host_cores():
+    """The host CPUs this process may run on (the GPU's CPU share)."""
+    return len(os.sched_getaffinity(0))
+
+
+def cpu_baseline(config_id, max_models, budget_s=10.0, affine=False, legs=3):
+    """The oracle, as it stands, on the models of the same state, timed in
+    `legs` legs of each kind, the median leg reported:
+      - on every host core this process may use (one model per thread at a
+        time); value = its evals/s, cores = that count;
+      - on one core: the calling thread pinned to one CPU with
+        os.sched_setaffinity for the leg, then restored.
+    The whole run takes about 2 x budget_s seconds."""
     from paper_2209_00159_amd import workloads as W
 
+    cores = host_cores()
     n_cfg = W.CONFIG_MODELS.get(config_id)
     wl = W.make(config_id, models=list(range(min(max_models, n_cfg))) if n_cfg else None,
-                workers=threads)
+                workers=cores)
     if affine:
         wl = W.affine(wl)
-    d1, e1, t1 = _oracle_over_models(wl, affine, budget_s, 1)
-    dn, en, tn = _oracle_over_models(wl, affine, budget_s, threads)
+    per_leg = budget_s / legs
+
+    def median_leg(runs):
+        runs = sorted(runs, key=lambda r: r[1] / r[2])
+        return runs[len(runs) // 2], [round(r[1] / r[2], 1) for r in runs]
+
+    many, many_rates = median_leg([_oracle_leg(wl, affine, per_leg, cores) for _ in range(legs)])
+    mask = os.sched_getaffinity(0)
+    pin = min(mask)
+    os.sched_setaffinity(0, {pin})
+    try:
+        one, one_rates = median_leg([_oracle_leg(wl, affine, per_leg, 1) for _ in range(legs)])
+    finally:
+        os.sched_setaffinity(0, mask)
+    dn, en, tn = many
+    d1, e1, t1 = one
     whole = dn == wl.n_models
-    return dict(value=en / tn, unit="evals/s", cores=threads, kind="oracle",
+    return dict(value=en / tn, unit="evals/s", cores=cores, kind="oracle",
                 sample=(f"{wl.name}: {'all ' if whole else 'the first '}{dn} model(s) of the same "
-                        f"state, full triangles, fp64 C oracle, {tn:.1f} s on {threads} host "
-                        f"threads (one model per thread at a time)"),
-                seconds=round(tn, 2), decisions_per_s=dn / tn,
-                single_thread=dict(value=e1 / t1, unit="evals/s", cores=1, models=d1,
-                                   seconds=round(t1, 2), decisions_per_s=d1 / t1))
+                        f"state, full triangles, fp64 C oracle, median of {legs} legs on "
+                        f"{cores} host threads (every core this process may use, one model per "
+                        f"thread at a time), {tn:.2f} s for the median leg"),
+                nproc=os.cpu_count(), legs=legs, seconds=round(tn, 2), decisions_per_s=dn / tn,
+                leg_rates=many_rates,
+                single_core=dict(value=e1 / t1, unit="evals/s", cores=1, pinned_cpu=pin,
+                                 models=d1, seconds=round(t1, 2), decisions_per_s=d1 / t1,
+                                 leg_rates=one_rates))
 
 
-def oracle_on_states(wl, recorded, budget_s=10.0, threads=16):
+def oracle_on_states(wl, recorded, budget_s=10.0, threads=None):
     """The oracle on decision states recorded by the scheduling loop, on
     `threads` host threads, for about budget_s seconds: decisions/s, and how
     many of its selections equal the GPU's."""
@@ -219,6 +249,7 @@ def oracle_on_states(wl, recorded, budget_s=10.0, threads=16):
 
     import oracle
 
+    threads = host_cores() if threads is None else threads
     lock = threading.Lock()
     state = dict(next=0, done=0, same=0)
     t0 = time.perf_counter()
@@ -320,9 +351,31 @@ def bench_affine(wl, ctx, args, torch, O, W):
         what="orloj_score_candidates_affine + orloj_select_batch: batch latency c0 + c1 s l "
              "(one solo-latency table per class), same queues, grid and batch sizes",
         workload=aw.name, c1=float(aw.c1[0]), ms_per_step=round(ms, 5),
-        evals_per_s=evals / (ms * 1e-3), decisions_per_s=aw.n_models / (ms * 1e-3),
+        evals_per_s=evals / (ms * 1e-3),
+        saturated_pass_selections_per_s=aw.n_models / (ms * 1e-3),
         table_bytes=int(aw.counts.size * 4),
         roofline=dict(affine_roofline(aw, kms), kernel_ms_median=round(float(np.median(times)), 5)))
+
+
+def copy_reference(torch, dev, nbytes=1 << 30, reps=10):
+    """Measured HBM rate of a plain device copy (torch's copy kernel, 1 GiB
+    read + 1 GiB written per launch), HIP events on the current stream: the
+    attainable stream rate beside the 8 TB/s peak."""
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    return (round(2 * nbytes / (ms * 1e-3) / 1e9, 1),
+            f"device copy of {nbytes >> 20} MiB (read + write), mean of {reps} launches")
 
 
 def main():
@@ -334,7 +387,8 @@ def main():
     ap.add_argument("--cpu-models", type=int, default=128,
                     help="most models the CPU oracle sample may take (each leg stops after ~10 s)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workers", type=int, default=16)
+    ap.add_argument("--workers", type=int, default=None,
+                    help="host threads for the workload generator (default: every host core)")
     ap.add_argument("--trace-arrivals", type=int, default=1_000_000,
                     help="arrivals of the configuration-5 trace replayed by the native "
                          "scheduling loop after the timed steps (0 = skip)")
@@ -348,6 +402,8 @@ def main():
                     help="batch-latency law of the timed step: per-batch-size tables "
                          "(default) or the affine law c0 + c1 s l (then the affine, iteration "
                          "and scheduling-loop legs are skipped)")
+    ap.add_argument("--no-copy-ref", action="store_true",
+                    help="skip timing the plain device copy reported as roofline.copy_gbs")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after timing, copy a 1 GiB buffer once (a plain copy kernel of "
                          "known size, for scaling HBM traffic counters)")
@@ -369,7 +425,8 @@ def main():
     torch.cuda.set_device(dev)
 
     t0 = time.perf_counter()
-    wl = W.make(args.config, workers=args.workers)
+    workers = args.workers or len(os.sched_getaffinity(0))
+    wl = W.make(args.config, workers=workers)
     print(f"[bench] generated {wl.name} in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
           flush=True)
     affine = args.mode == "affine"
@@ -432,7 +489,12 @@ def main():
                     candidates=valid_candidates(wl), evals_per_step=evals,
                     prefix_mode="triangle", b_expo_per_ms=wl.b_expo,
                     batch_law="affine c0 + c1 s l" if affine else "per-batch-size tables"),
-        decisions_per_s=wl.n_models / (ms_per_step * 1e-3),
+        decisions_per_s=None,
+        saturated_pass_selections_per_s=wl.n_models / (ms_per_step * 1e-3),
+        saturated_pass_note=("one selection per model per timed step (every model scored at "
+                             "once, all 64-deep prefixes present); configuration 5's scheduling "
+                             "decisions/s, with the queue re-scored at every dispatch decision, "
+                             "is decisions_per_s from the trace-driven loop"),
         build_cdfs_ms=round(build_ms, 4),
         build_cdfs_gbs=round(wl.counts.nbytes * 2 / (build_ms * 1e-3) / 1e9, 1),
         roofline=roof,
@@ -445,6 +507,8 @@ def main():
         torch.cuda.synchronize()
         line["calibration_copy_bytes"] = src.numel() * 4
         del src, dst
+    if not args.no_copy_ref:
+        roof["copy_gbs"], roof["copy_note"] = copy_reference(torch, dev)
     if not args.no_affine:
         line["affine"] = bench_affine(wl, ctx, args, torch, O, W)
     if not args.no_iterate:
@@ -504,15 +568,14 @@ def main():
             note="decisions_per_s: wall clock of the whole loop (queues, drop phase, "
                  "simulated workers and the rounds); decisions_per_device_s: queue upload + "
                  "score + select + selection download of the rounds only")
+        line["decisions_per_s"] = line["trace"]["decisions_per_s"]
         print(f"[bench] loop: {d['decisions']} decisions in {d['wall_s']:.2f} s wall "
               f"({d['device_s']:.2f} s on device)", file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = cpu_baseline(args.config, args.cpu_models, affine=affine,
-                                            threads=args.workers)
+        line["cpu_baseline"] = cpu_baseline(args.config, args.cpu_models, affine=affine)
         if recorded:
-            line["cpu_baseline"]["trace"] = oracle_on_states(wl, recorded, budget_s=10.0,
-                                                             threads=args.workers)
+            line["cpu_baseline"]["trace"] = oracle_on_states(wl, recorded, budget_s=10.0)
     print(json.dumps(line), flush=True)
 
 

@@ -143,10 +143,18 @@ int decide(orloj_sched* s, double now, const uint8_t* idle, int32_t* sel_n, int3
                                     s->prob_off());
         if (rc) return orloj_ctx_fail(ctx, rc, "orloj_sched_decide: sizing the outputs failed");
         hipError_t e = hipSetDevice(ctx->device);
-        if (e == hipSuccess)
-            e = hipMemcpyAsync(s->d_stage, s->h_stage, s->fixed + 12 * (size_t)n,
-                               hipMemcpyHostToDevice, ctx->stream);
-        if (e != hipSuccess) return hip_err(ctx, e, "orloj_sched_decide: uploading the queues");
+        if (e != hipSuccess) return hip_err(ctx, e, "orloj_sched_decide: hipSetDevice");
+        // Once the upload is enqueued, every return waits for the stream
+        // first: the copy reads the pinned staging block, which the next
+        // round rewrites.
+        auto drained = [&](int code) {
+            (void)hipStreamSynchronize(ctx->stream);
+            return code;
+        };
+        e = hipMemcpyAsync(s->d_stage, s->h_stage, s->fixed + 12 * (size_t)n,
+                           hipMemcpyHostToDevice, ctx->stream);
+        if (e != hipSuccess)
+            return drained(hip_err(ctx, e, "orloj_sched_decide: uploading the queues"));
         const size_t o1 = 8 * (size_t)(M + 1);
         orloj_queues dq;
         dq.h_queue_off = off;
@@ -160,10 +168,10 @@ int decide(orloj_sched* s, double now, const uint8_t* idle, int32_t* sel_n, int3
         rc = orloj_score_candidates(ctx, &s->grid, s->d_ccdf, s->d_support, &dq, s->b,
                                     ORLOJ_PREFIX_TRIANGLE, d_coff, d_poff, s->d_P, s->d_E, s->d_EL,
                                     s->d_S);
-        if (rc) return rc;
+        if (rc) return drained(rc);
         rc = orloj_select_batch(ctx, &s->grid, &dq, ORLOJ_PREFIX_TRIANGLE, d_coff, s->d_S, s->d_sel,
                                 s->d_sel + M, reinterpret_cast<float*>(s->d_sel + 2 * M));
-        if (rc) return rc;
+        if (rc) return drained(rc);
         // the select kernel writes the selections straight into mapped
         // host memory: no copy, the stream's completion makes them visible
         e = hipStreamSynchronize(ctx->stream);
