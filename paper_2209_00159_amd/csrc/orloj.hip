@@ -66,6 +66,14 @@ __device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t x, int lane) {
     return x;
 }
 
+// Sum over the wave, in every lane.
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x, int lane) {
+    const uint64_t s = wave_incl_scan_u64(x, lane);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)s, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(s >> 32), 63);
+    return ((uint64_t)hi << 32) | lo;
+}
+
 // ---------------------------------------------------------------------------
 // cdf_kernel: one workgroup per histogram row.  Thread t owns the VPT
 // consecutive bins [t*VPT, t*VPT + VPT): it loads them once, the workgroup
@@ -235,6 +243,13 @@ __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2
 // ---------------------------------------------------------------------------
 // score_kernel
 // ---------------------------------------------------------------------------
+// Launches over many models of which only a few have a queue (a scheduling
+// round scores the idle models only) list those models in their arguments
+// and launch workgroups for them alone: workgroups that only find an empty
+// queue and exit would still hold the dispatch slots for a memory round
+// trip each.
+constexpr int kMaxActive = 256;
+
 struct ScoreArgs {
     const float* tab;          // [M][nbs][C][K] 1 - F(x_{k+1})
     const int64_t* queue_off;  // [M+1]
@@ -260,8 +275,15 @@ struct ScoreArgs {
     int nchunk;                // workgroups per (model, batch size)
     double b;
     int M, C, K, nbs, rect, maxcap;
+    int Mg;                    // models the grid covers: M, or the listed ones
+    int compact;               // 1: grid model i is act[i]
     int bs[ORLOJ_MAX_BATCH_SIZES];
+    int act[kMaxActive];       // the models with a non-empty queue (compact)
 };
+
+__device__ __forceinline__ int grid_model(const ScoreArgs& a, unsigned i) {
+    return a.compact ? a.act[i] : (int)i;
+}
 
 // Stand-in rows for lane chunks that lie wholly outside a row's support:
 // there every entry of 1 - F is exactly 0 (past the last bin with mass) or
@@ -469,8 +491,12 @@ struct LaneCarry64 {
 #ifndef ORLOJ_EONLY_PREFETCH
 #define ORLOJ_EONLY_PREFETCH 3   // iterations ahead in the E-only panels' loop
 #endif
-template <int CPL, int PF, bool EXACT, int CR, bool AFF>
+#ifndef ORLOJ_WARMUP_PREFETCH
+#define ORLOJ_WARMUP_PREFETCH 4  // steps ahead in a chunk's warm-up loop
+#endif
+template <int CPL, int PF, bool EXACT, int CR, bool AFF, bool ESPLIT>
 __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
+    static_assert(ESPLIT || !AFF, "the affine mode takes its E sums from emax_kernel");
     using Q = Quarters<CPL>;
     constexpr int PW = 64 * CPL;                   // bins per panel
     extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -486,11 +512,11 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
 
     // Largest batch sizes first, and their last chunks first: those
     // workgroups run longest.
-    const unsigned per_bs = (unsigned)a.M * (unsigned)a.nchunk;
+    const unsigned per_bs = (unsigned)a.Mg * (unsigned)a.nchunk;
     const int bi = a.nbs - 1 - (int)(blockIdx.x / per_bs);
     const unsigned rem = blockIdx.x % per_bs;
-    const int kc = a.nchunk - 1 - (int)(rem / (unsigned)a.M);
-    const int q = (int)(rem % (unsigned)a.M);
+    const int kc = a.nchunk - 1 - (int)(rem / (unsigned)a.Mg);
+    const int q = grid_model(a, rem % (unsigned)a.Mg);
     const int64_t q0 = a.queue_off[q];
     const int64_t N = a.queue_off[q + 1] - q0;
     const int bsz = a.bs[bi];
@@ -614,7 +640,43 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         mb.oz = (uint16_t)oz; mb.oa = (uint16_t)oa;
         return mb;
     };
-    for (int m = lane; m < n1; m += 64) s_mem[m] = make_plan(m, true);
+    // The prologue is a chain of memory round trips, which the launches too
+    // small to fill the chip wait on: the loads that do not depend on each
+    // other are issued together.  This batch size's block of candidates and
+    // member slots starts after those of the batch sizes before it (one per
+    // lane, summed across the wave).
+    int64_t cand = a.cand_off[q], prob = a.prob_off[q];
+    {
+        uint64_t dc = 0, dp = 0;
+        for (int j0 = 0; j0 < bi; j0 += 64) {
+            const int j = j0 + lane;
+            if (j < bi) {
+                const int64_t c = a.rect ? N : (N < a.bs[j] ? N : (int64_t)a.bs[j]);
+                dc += (uint64_t)c;
+                dp += (uint64_t)(c * (c + 1) / 2);
+            }
+        }
+        cand += (int64_t)wave_sum_u64(dc, lane);
+        prob += (int64_t)wave_sum_u64(dp, lane);
+    }
+    // rows of this (model, batch size); affine mode has one set per model
+    const size_t qb = AFF ? (size_t)q : (size_t)q * (size_t)a.nbs + (size_t)bi;
+    const float* tab_qb = a.tab + qb * (size_t)a.C * (size_t)K;
+
+    // class and support of member n in lane n % 64 of register n / 64, and
+    // the members' plans, in one pass
+    LaneCarry<CR> cls_r, lo_r, hi_r;
+    const int32_t* sup_qb = a.sup ? a.sup + qb * (size_t)a.C * 2 : nullptr;
+#pragma unroll
+    for (int r = 0; r < CR; ++r) {
+        const int m = r * 64 + lane;
+        int c = a.cls[q0 + min(m, n1 - 1)];
+        if (c < 0 || c >= a.C) c = 0;                     // flagged by its plan
+        cls_r.v[r] = __builtin_bit_cast(float, c);
+        lo_r.v[r] = __builtin_bit_cast(float, sup_qb ? sup_qb[2 * c] : 0);
+        hi_r.v[r] = __builtin_bit_cast(float, sup_qb ? sup_qb[2 * c + 1] : K);
+        if (m < n1) s_mem[m] = make_plan(m, true);
+    }
     if (lane == 0) {
         s_kd[0] = 0.0;
         s_kd[1] = 1.0;
@@ -646,28 +708,6 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     const float dq1 = exp2f(log2d);                   // d in fp32
     const float dPW = exp2_hw(log2d * (float)PW);
 
-    int64_t cand = a.cand_off[q], prob = a.prob_off[q];
-    for (int j = 0; j < bi; ++j) {
-        const int64_t c = a.rect ? N : (N < a.bs[j] ? N : (int64_t)a.bs[j]);
-        cand += c;
-        prob += c * (c + 1) / 2;
-    }
-    // rows of this (model, batch size); affine mode has one set per model
-    const size_t qb = AFF ? (size_t)q : (size_t)q * (size_t)a.nbs + (size_t)bi;
-    const float* tab_qb = a.tab + qb * (size_t)a.C * (size_t)K;
-
-    // class and support of member n in lane n % 64 of register n / 64;
-    // first member of each panel in lane p
-    LaneCarry<CR> cls_r, lo_r, hi_r;
-    const int32_t* sup_qb = a.sup ? a.sup + qb * (size_t)a.C * 2 : nullptr;
-#pragma unroll
-    for (int r = 0; r < CR; ++r) {
-        int c = a.cls[q0 + min(r * 64 + lane, n1 - 1)];
-        if (c < 0 || c >= a.C) c = 0;                     // flagged by its plan
-        cls_r.v[r] = __builtin_bit_cast(float, c);
-        lo_r.v[r] = __builtin_bit_cast(float, sup_qb ? sup_qb[2 * c] : 0);
-        hi_r.v[r] = __builtin_bit_cast(float, sup_qb ? sup_qb[2 * c + 1] : K);
-    }
     // Home panel of the last member (the latest deadline): past it no member
     // needs G or the discounted prefix, only E[L_B] needs the sums of 1 - G.
     // The main loop walks the panels up to LASTP; the tabulated mode then
@@ -696,26 +736,32 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     LaneCarry64<CR> cE, cP, cGl;
     cW.zero(); cGl.zero(); cN.zero(); cE.zero(); cP.zero();
 
-    // One flat loop over (panel p, step n), n fastest, padded at the end to a
-    // multiple of PF with ghost iterations (p == NP) so that ring slot i
-    // always holds iteration it0 + i.  The row of iteration it + PF is
-    // loaded PF iterations ahead; (p, n) and the prefetch position advance
-    // by counting.
-    const int total = NPW * n1;
+    // One flat loop over (panel p, step n in [ns, n1)), n fastest, padded at
+    // the end to a multiple of PF with ghost iterations (p == NP) so that
+    // ring slot i always holds iteration it0 + i.  The row of iteration
+    // it + PF is loaded PF iterations ahead; (p, n) and the prefetch
+    // position advance by counting.  A chunk of a split launch rebuilds G
+    // over the steps before n0 (warm-up): in a loop of its own at each pass
+    // start when its E sums come from emax_kernel (WARM_LOOP: the loop's
+    // deeper ring costs registers, which the launches that fill the chip
+    // cannot spare), else as iterations of this loop that update G only.
+    constexpr bool WARM_LOOP = ESPLIT && !AFF;
+    const int ns = WARM_LOOP ? n0 : 0;
+    const int total = NPW * (n1 - ns);
     const int iters = (total + PF - 1) / PF * PF;
     const int base = lane * CPL;
 
     double Gacc[CPL];
     float buf[PF][CPL];
-    int pf_p = 0, pf_n = 0;                               // prefetch position
+    int pf_p = 0, pf_n = ns;                              // prefetch position
 #pragma unroll
     for (int i = 0; i < PF; ++i) {
         load_step(buf[i], pf_n, pf_p * PW + base, false);
         // keep the priming loads in ring order, as the loop issues them
         __builtin_amdgcn_sched_barrier(0);
-        if (++pf_n == n1) { pf_n = 0; pf_p = min(pf_p + 1, NPW - 1); }
+        if (++pf_n == n1) { pf_n = ns; pf_p = min(pf_p + 1, NPW - 1); }
     }
-    int p = 0, n = 0;
+    int p = 0, n = ns;
     int mlo = __builtin_amdgcn_readlane(mlo_r, 0);
     int mend = __builtin_amdgcn_readlane(mlo_r, 1);
     // Trivial steps.  Where a panel lies wholly past the last bin with mass
@@ -731,15 +777,53 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     float etot_prev = 0.0f, T_prev = 0.0f;
     double gl_prev = 0.0;
 
+    // Warm-up: G over steps 0 .. n0-1 of panel pp (the product only, the
+    // same fma per bin and step as a scored step, so the same bits; a step
+    // whose row cannot change G multiplies by an exact 0 or finds G = 0),
+    // with rows loaded PFW steps ahead: these steps are short and would
+    // otherwise wait on their loads.  Leaves pass_zero for the steps after.
+    constexpr int PFW = ORLOJ_WARMUP_PREFETCH;
+    auto warm_up = [&](int pp) {
+        const int p0w = pp * PW, pbw = p0w + base;
+        float wb[PFW][CPL];
+        bool zero = false;                   // G == 0 over the panel
+#pragma unroll
+        for (int i = 0; i < PFW; ++i) {
+            load_step(wb[i], min(i, n0 - 1), pbw, false);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        for (int w0 = 0; w0 < n0; w0 += PFW) {
+#pragma unroll
+            for (int i = 0; i < PFW; ++i) {
+                const int nw = w0 + i;
+                if (nw < n0) {
+#pragma unroll
+                    for (int j = 0; j < CPL; ++j) {
+                        const float t = (EXACT || pbw + j < K) ? wb[i][j] : 0.0f;
+                        Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
+                    }
+                    zero = zero || min(p0w + PW, K) <= __builtin_bit_cast(int, lo_r.get(nw));
+                }
+#pragma unroll
+                for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(Gacc[j])::"memory");
+                load_step(wb[i], min(nw + PFW, n0 - 1), pbw, zero);
+            }
+        }
+        pass_zero = zero;
+    };
+
     for (int it0 = 0; it0 < iters; it0 += PF) {
 #pragma unroll
         for (int i = 0; i < PF; ++i) {
-            if (n == 0) {
+            if (n == ns) {
                 // a real branch (the asm keeps it from becoming selects)
                 asm volatile("" ::: "memory");
 #pragma unroll
                 for (int j = 0; j < CPL; ++j) Gacc[j] = 1.0;
                 pass_zero = false;
+                if constexpr (WARM_LOOP) {
+                    if (n0 > 0 && p < NPW) warm_up(p);
+                }
                 if constexpr (CR == 1) {
                     // at most 64 members: lane l scores member mlo + l of this
                     // pass at every step, so its plan is read from LDS once
@@ -771,7 +855,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                         const int j = qq * Q::QW + r;
                         const float t = (EXACT || pbase + j < K) ? buf[i][j] : 0.0f;
                         Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
-                        if constexpr (!AFF) gs[r] = qq == 0 ? Gacc[j] : gs[r] + Gacc[j];
+                        if constexpr (!ESPLIT) gs[r] = qq == 0 ? Gacc[j] : gs[r] + Gacc[j];
                         zz = r == 0 ? Gacc[j] : fma(zz, d64, Gacc[j]);
                     }
                     zqv[qq] = (float)zz;
@@ -785,7 +869,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             // G == 0 over the pass from here on: later steps of it need no row
             const bool zero_after = pass_zero || min(p0 + PW, K) <= lo_n;
             load_step(buf[i], pf_n, pf_p * PW + base, zero_after && pf_p == p);
-            if (++pf_n == n1) { pf_n = 0; pf_p = min(pf_p + 1, NPW - 1); }
+            if (++pf_n == n1) { pf_n = ns; pf_p = min(pf_p + 1, NPW - 1); }
             if (p < NPW && real) {                        // else a ghost or warm-up iteration
                 float etot = etot_prev, T = T_prev;
                 double glast_here = gl_prev;
@@ -806,7 +890,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                     T_prev = T;
                 }
                 if (!skip) {
-                    if constexpr (!AFF) {
+                    if constexpr (!ESPLIT) {
                         double gsum = gs[0];
 #pragma unroll
                         for (int r = 1; r < Q::QW; ++r) gsum += gs[r];
@@ -897,11 +981,11 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                     cW.set(n, fmaf(Win, dPW, T));
                     cGl.set(n, glast_here);
                 }
-                if constexpr (!AFF) cE.set(n, cE.get(n) + (double)etot);
+                if constexpr (!ESPLIT) cE.set(n, cE.get(n) + (double)etot);
             }
             pass_zero = zero_after;
             if (++n == n1) {
-                n = 0;
+                n = ns;
                 ++p;
                 mlo = __builtin_amdgcn_readlane(mlo_r, min(p, NP));
                 mend = __builtin_amdgcn_readlane(mlo_r, min(p + 1, NP));
@@ -913,8 +997,9 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     // these panels only add their sums of 1 - G to E[L_B], in a loop of its
     // own: the product and the sum, no discounted prefix, snapshot or
     // carries.  Its ring is primed afresh; the panels' sums are added in
-    // panel order after those of the member panels, as before.
-    if constexpr (!AFF) {
+    // panel order after those of the member panels, as before.  (ESPLIT:
+    // every panel's sums come from emax_kernel.)
+    if constexpr (!ESPLIT) {
         if (LASTP + 1 < NP) {
             constexpr int PFB = ORLOJ_EONLY_PREFETCH;   // its ring is deeper: fewer registers live here
             float bufb[PFB][CPL];
@@ -989,10 +1074,11 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         const int n = r * 64 + lane;
         if (n >= n0 && n < n1) {
             double esum = cE.mine(r);
-            if constexpr (AFF) {
+            if constexpr (ESPLIT) {
                 // the panels' sums in panel order, as this kernel adds them
                 esum = 0.0;
-                const float* ps = a.psum + (size_t)q * (size_t)a.np_e * (size_t)maxcap + n;
+                const size_t pair = AFF ? (size_t)q : (size_t)q * (size_t)a.nbs + (size_t)bi;
+                const float* ps = a.psum + pair * (size_t)a.np_e * (size_t)maxcap + n;
                 for (int pp = 0; pp < a.np_e; ++pp) esum += (double)ps[(size_t)pp * (size_t)maxcap];
             }
             const double el = c0q + w * (0.5 + esum);
@@ -1004,38 +1090,54 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// emax_kernel (affine mode): the sums behind E[L_B].  Under Eq. (3) every
-// batch size's histogram is the same product G_n of the members' solo CDFs
-// on the base grid, mapped onto a wider grid, so E[max] = w (1/2 +
-// sum_k (1 - G_n(x_{k+1}))) needs one product per prefix length n, not one
-// per batch size (Eq. (5) then gives c0 + c1 s E[max]).  One wave per
-// (model, panel) keeps the running product of its panel's bins over the
-// queue's longest prefix and writes each step's panel sum to
-// psum[(q * panels + p) * maxcap + n], rounded as score_kernel rounds its
-// own per-panel sums, so both modes give the same bits where they coincide.
+// emax_kernel: the sums behind E[L_B], one wave per (pair, panel), ahead of
+// score_kernel.  E[L_B] = w (1/2 + sum_k (1 - G_n(x_{k+1}))) (Eq. (5)) needs
+// the panel sums of 1 - G for every prefix length n.  A wave keeps the
+// running product of its panel's bins over the pair's prefixes and writes
+// each step's panel sum to psum[(pair * panels + p) * maxcap + n], rounded
+// as score_kernel rounds its own per-panel sums, so E[L_B] has the same
+// bits either way.
+//   Affine mode: a pair is a model.  Under Eq. (3) every batch size's
+//     histogram is the same product G_n of the members' solo CDFs on the
+//     base grid, mapped onto a wider grid, so E[max] needs one product per
+//     prefix length, not one per batch size (c0 + c1 s E[max]).
+//   Tabulated mode, in launches split into step chunks: a pair is a (model,
+//     batch size).  The panels past every member's deadline then need no
+//     chunk to repeat their products: the score waves walk only the
+//     panels that hold members.
 // Rows are loaded PFE steps ahead; the class and support of step n sit in
 // lane n % 64, so a step's row address needs no memory round trip.
 // ---------------------------------------------------------------------------
-template <int CPL, bool EXACT, int CR>
+template <int CPL, bool EXACT, int CR, bool AFF>
 __global__ __launch_bounds__(64) void emax_kernel(const ScoreArgs a) {
     using Q = Quarters<CPL>;
     constexpr int PW = 64 * CPL;
     constexpr int PFE = 8;
     const int K = a.K;
     const int NP = (K + PW - 1) / PW;
-    const int q = (int)(blockIdx.x / (unsigned)NP);
-    const int p = (int)(blockIdx.x - (unsigned)q * (unsigned)NP);
+    const unsigned pair = blockIdx.x / (unsigned)NP;
+    const int p = (int)(blockIdx.x - pair * (unsigned)NP);
+    int q, bi;
+    size_t qb;                                  // the pair's rows and sums
+    if constexpr (AFF) {
+        q = grid_model(a, pair);
+        bi = a.nbs - 1;                         // the longest prefix (batch sizes increase)
+        qb = (size_t)q;
+    } else {
+        bi = a.nbs - 1 - (int)(pair / (unsigned)a.Mg);   // largest batch sizes first
+        q = grid_model(a, pair % (unsigned)a.Mg);
+        qb = (size_t)q * (size_t)a.nbs + (size_t)bi;
+    }
     const int64_t q0 = a.queue_off[q];
     const int64_t N = a.queue_off[q + 1] - q0;
-    // the longest prefix of any batch size (batch sizes increase)
-    const int64_t cap64 = a.rect ? N : (N < a.bs[a.nbs - 1] ? N : (int64_t)a.bs[a.nbs - 1]);
+    const int64_t cap64 = a.rect ? N : (N < a.bs[bi] ? N : (int64_t)a.bs[bi]);
     if (cap64 <= 0 || cap64 > a.maxcap || cap64 > 64 * CR) return;
     const int ncap = (int)cap64;
     const int lane = threadIdx.x;
     const int pbase = p * PW + lane * CPL;
-    const float* tab_q = a.tab + (size_t)q * (size_t)a.C * (size_t)K;
-    const int32_t* sup_q = a.sup ? a.sup + (size_t)q * (size_t)a.C * 2 : nullptr;
-    float* out = a.psum + ((size_t)q * (size_t)NP + (size_t)p) * (size_t)a.maxcap;
+    const float* tab_q = a.tab + qb * (size_t)a.C * (size_t)K;
+    const int32_t* sup_q = a.sup ? a.sup + qb * (size_t)a.C * 2 : nullptr;
+    float* out = a.psum + (qb * (size_t)NP + (size_t)p) * (size_t)a.maxcap;
 
     LaneCarry<CR> cls_r, lo_r, hi_r;
 #pragma unroll
@@ -1072,6 +1174,12 @@ __global__ __launch_bounds__(64) void emax_kernel(const ScoreArgs a) {
         load(buf[i], min(i, ncap - 1));
         __builtin_amdgcn_sched_barrier(0);
     }
+    // Each step's lane sums are parked in LDS, one row per step, and every
+    // 64 steps lane r adds up row r in the pairwise order in which the wave
+    // scan of score_kernel reaches its last lane (pairs of neighbouring
+    // lanes, then pairs of those, ...), so the panel sums have that
+    // kernel's bits without a cross-lane reduction on every step.
+    __shared__ float s_e[64][65];
     for (int n0 = 0; n0 < ncap; n0 += PFE) {
 #pragma unroll
         for (int i = 0; i < PFE; ++i) {
@@ -1091,22 +1199,39 @@ __global__ __launch_bounds__(64) void emax_kernel(const ScoreArgs a) {
                 double gsum = gs[0];
 #pragma unroll
                 for (int r = 1; r < Q::QW; ++r) gsum += gs[r];
-                const float e = (float)((double)CPL - gsum);    // padding bins hold G = 1
-                const float etot = lane63(wave_scan_sum(e));
-                if (lane == 0) out[n] = etot;
+                s_e[n & 63][lane] = (float)((double)CPL - gsum);   // padding bins hold G = 1
             }
             // refill the slot only after the update has read it
 #pragma unroll
             for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(G[j])::"memory");
             load(buf[i], min(n + PFE, ncap - 1));
         }
+        // a full block of 64 steps, or the last steps: lane r sums step
+        // (block start + r)
+        const int done = n0 + PFE;
+        if ((done & 63) == 0 || done >= ncap) {
+            wave_lds_fence();
+            const int blk = (done - 1) & ~63;
+            const int nr = blk + lane;
+            if (nr < ncap) {
+                float v[32];
+#pragma unroll
+                for (int k = 0; k < 32; ++k) v[k] = s_e[lane][2 * k] + s_e[lane][2 * k + 1];
+#pragma unroll
+                for (int w = 16; w >= 1; w >>= 1)
+#pragma unroll
+                    for (int k = 0; k < w; ++k) v[k] = v[2 * k] + v[2 * k + 1];
+                out[nr] = v[0];
+            }
+            wave_lds_fence();
+        }
     }
 }
 
 // ---------------------------------------------------------------------------
 // select_kernel: one workgroup per model; thread i reads candidates i,
-// i + 256, ... (coalesced) and finds its (batch size, n) from the block
-// starts of the model's batch sizes.
+// i + kSelThreads, ... (coalesced) and finds its (batch size, n) from the
+// block starts of the model's batch sizes.
 // ---------------------------------------------------------------------------
 struct SelectArgs {
     const int64_t* queue_off;
@@ -1116,7 +1241,11 @@ struct SelectArgs {
     int32_t* sel_bs;
     float* sel_score;
     int nbs, rect;
+    int M;
+    int n_act;                 // compact: workgroup g < n_act selects for act[g];
+    int compact;               //   workgroup 0 also clears the models with an empty queue
     int bs[ORLOJ_MAX_BATCH_SIZES];
+    int act[kMaxActive];
 };
 
 struct Best {
@@ -1126,12 +1255,20 @@ struct Best {
 };
 
 __device__ __forceinline__ bool better(const Best& x, const Best& y) {
-    // larger score; exact ties: larger n, then smaller batch size
-    if (x.n == 0) return false;
-    if (y.n == 0) return true;
-    if (x.s != y.s) return x.s > y.s;
-    if (x.n != y.n) return x.n > y.n;
-    return x.bs < y.bs;
+    // larger score; exact ties: larger n, then smaller batch size (n = 0:
+    // no candidate).  Written without branches, and applied with selects
+    // (take_if_better): the branchy form of the update lost the new n on
+    // some paths when compiled for gfx950.
+    const bool sgt = x.s > y.s, seq = x.s == y.s;
+    const bool tie = seq && (x.n > y.n || (x.n == y.n && x.bs < y.bs));
+    return x.n != 0 && (y.n == 0 || sgt || tie);
+}
+
+__device__ __forceinline__ void take_if_better(Best& best, const Best& c) {
+    const bool t = better(c, best);
+    best.s = t ? c.s : best.s;
+    best.n = t ? c.n : best.n;
+    best.bs = t ? c.bs : best.bs;
 }
 
 // 16 waves per model: the kernel is a chain of latencies (block starts,
@@ -1142,8 +1279,21 @@ constexpr int kSelWaves = kSelThreads / 64;
 __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a) {
     __shared__ int64_t s_start[ORLOJ_MAX_BATCH_SIZES + 1];
     __shared__ Best s_best[kSelWaves];
-    const int q = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    if (a.compact) {
+        if (blockIdx.x == 0) {
+            // no batch for the models with an empty queue (not listed)
+            for (int m = tid; m < a.M; m += kSelThreads) {
+                if (a.queue_off[m + 1] == a.queue_off[m]) {
+                    a.sel_n[m] = 0;
+                    a.sel_bs[m] = 0;
+                    a.sel_score[m] = 0.0f;
+                }
+            }
+        }
+        if ((int)blockIdx.x >= a.n_act) return;
+    }
+    const int q = a.compact ? a.act[blockIdx.x] : (int)blockIdx.x;
     __shared__ int64_t s_wsum[kSelWaves];
     const int64_t N = a.queue_off[q + 1] - a.queue_off[q];
     // block starts: an exclusive scan of the prefix caps over the batch
@@ -1164,10 +1314,14 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
     }
     if (tid == 0) s_start[a.nbs] = carry;
     __syncthreads();
-    const int64_t total = s_start[a.nbs];
     const float* S = a.S + a.cand_off[q];
     Best best{0.0f, 0, 0};
+    // candidates i = tid, tid + kSelThreads, ... (coalesced); a candidate's
+    // (batch size, n) from the block starts.  The comparison is a total
+    // order, so the pick does not depend on the order of the visits.
+    const int64_t total = s_start[a.nbs];
     for (int64_t i = tid; i < total; i += kSelThreads) {
+        const float sc = S[i];
         int lo = 0, hi = a.nbs - 1;          // last bi with s_start[bi] <= i
         while (lo < hi) {
             const int mid = (lo + hi + 1) >> 1;
@@ -1175,11 +1329,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
         }
         const int n = (int)(i - s_start[lo]) + 1;
         const int bsz = a.bs[lo];
-        const float s = S[i];
-        if (n <= bsz && s == s) {   // NaN never wins
-            const Best c{s, n, bsz};
-            if (better(c, best)) best = c;
-        }
+        if (n <= bsz && sc == sc)            // NaN never wins
+            take_if_better(best, Best{sc, n, bsz});
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
@@ -1187,21 +1338,31 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
         o.s = __shfl_xor(best.s, off, 64);
         o.n = __shfl_xor(best.n, off, 64);
         o.bs = __shfl_xor(best.bs, off, 64);
-        if (better(o, best)) best = o;
+        take_if_better(best, o);
     }
     if (lane == 0) s_best[wv] = best;
     __syncthreads();
-    if (tid == 0) {
-        for (int w = 1; w < kSelWaves; ++w)
-            if (better(s_best[w], best)) best = s_best[w];
-        if (best.n > 0 && best.s > 0.0f) {
-            a.sel_n[q] = best.n;
-            a.sel_bs[q] = best.bs;
-            a.sel_score[q] = best.s;
-        } else {
-            a.sel_n[q] = 0;
-            a.sel_bs[q] = 0;
-            a.sel_score[q] = 0.0f;
+    if (wv == 0) {
+        // the waves' picks, reduced across the first kSelWaves lanes
+        best = lane < kSelWaves ? s_best[lane] : Best{0.0f, 0, 0};
+#pragma unroll
+        for (int off = kSelWaves / 2; off > 0; off >>= 1) {
+            Best o;
+            o.s = __shfl_xor(best.s, off, 64);
+            o.n = __shfl_xor(best.n, off, 64);
+            o.bs = __shfl_xor(best.bs, off, 64);
+            take_if_better(best, o);
+        }
+        if (lane == 0) {
+            if (best.n > 0 && best.s > 0.0f) {
+                a.sel_n[q] = best.n;
+                a.sel_bs[q] = best.bs;
+                a.sel_score[q] = best.s;
+            } else {
+                a.sel_n[q] = 0;
+                a.sel_bs[q] = 0;
+                a.sel_score[q] = 0.0f;
+            }
         }
     }
 }
@@ -1960,19 +2121,26 @@ int chunk_per_lane(int K) {
 #ifndef ORLOJ_SCORE_PREFETCH
 #define ORLOJ_SCORE_PREFETCH 2   // iterations a row is loaded ahead of its use
 #endif
+#ifndef ORLOJ_SPLIT_PREFETCH
+#define ORLOJ_SPLIT_PREFETCH 4   // the same in launches with an E pre-pass
+#endif
 
-template <int CPL, bool EXACT, int CR, bool AFF>
+template <int CPL, bool EXACT, int CR, bool AFF, bool ESPLIT>
 hipError_t launch_score_v(const ScoreArgs& a, unsigned grid, hipStream_t st) {
-    constexpr int PF = ORLOJ_SCORE_PREFETCH;
+    // the tabulated launches that take their E sums from emax_kernel are
+    // small ones (or split into chunks): few waves per SIMD to hide a row
+    // load's latency, so their ring is deeper
+    constexpr int PF = (ESPLIT && !AFF) ? ORLOJ_SPLIT_PREFETCH : ORLOJ_SCORE_PREFETCH;
     const size_t sm = score_fixed_bytes<CPL>() + (size_t)a.maxcap * score_bytes_per_member();
     static size_t attr_bytes = 0;   // per template instance; device-independent
     if (sm > attr_bytes) {
-        hipError_t e = hipFuncSetAttribute((const void*)score_kernel<CPL, PF, EXACT, CR, AFF>,
+        hipError_t e = hipFuncSetAttribute((const void*)score_kernel<CPL, PF, EXACT, CR, AFF, ESPLIT>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
         if (e != hipSuccess) return e;
         attr_bytes = sm;
     }
-    hipLaunchKernelGGL((score_kernel<CPL, PF, EXACT, CR, AFF>), dim3(grid), dim3(64), sm, st, a);
+    hipLaunchKernelGGL((score_kernel<CPL, PF, EXACT, CR, AFF, ESPLIT>), dim3(grid), dim3(64), sm,
+                       st, a);
     return hipGetLastError();
 }
 
@@ -2008,38 +2176,51 @@ int score_chunk(int K) { return score_chunk_of(K); }
 
 // Step carries: one register per 64 steps (longest prefix up to 64, or up to
 // the compiled limit).
-template <int CPL, bool EXACT, bool AFF>
+template <int CPL, bool EXACT, bool AFF, bool ESPLIT>
 hipError_t launch_score_c(const ScoreArgs& a, unsigned grid, hipStream_t st) {
-    return a.maxcap <= 64 ? launch_score_v<CPL, EXACT, 1, AFF>(a, grid, st)
-                          : launch_score_v<CPL, EXACT, (ORLOJ_MAX_PREFIX + 63) / 64, AFF>(a, grid, st);
+    constexpr int CRL = (ORLOJ_MAX_PREFIX + 63) / 64;
+    return a.maxcap <= 64 ? launch_score_v<CPL, EXACT, 1, AFF, ESPLIT>(a, grid, st)
+                          : launch_score_v<CPL, EXACT, CRL, AFF, ESPLIT>(a, grid, st);
 }
 
-template <int CPL, bool AFF>
+template <int CPL, bool AFF, bool ESPLIT>
 hipError_t launch_score_m(const ScoreArgs& a, unsigned grid, hipStream_t st) {
-    return a.K % (64 * CPL) == 0 ? launch_score_c<CPL, true, AFF>(a, grid, st)
-                                 : launch_score_c<CPL, false, AFF>(a, grid, st);
+    return a.K % (64 * CPL) == 0 ? launch_score_c<CPL, true, AFF, ESPLIT>(a, grid, st)
+                                 : launch_score_c<CPL, false, AFF, ESPLIT>(a, grid, st);
 }
 
+// Affine mode: E sums from emax_kernel.  Tabulated mode: from emax_kernel
+// when the launch is split into step chunks over rows of more than two
+// panels (a.psum set), else summed by the score waves themselves.
 template <int CPL>
 hipError_t launch_score(const ScoreArgs& a, unsigned grid, hipStream_t st) {
-    return a.c1 ? launch_score_m<CPL, true>(a, grid, st) : launch_score_m<CPL, false>(a, grid, st);
+    if (a.c1) return launch_score_m<CPL, true, true>(a, grid, st);
+    return a.psum ? launch_score_m<CPL, false, true>(a, grid, st)
+                  : launch_score_m<CPL, false, false>(a, grid, st);
 }
 
-// emax_kernel (affine mode): its own panel width, the tabulated kernel's, so
-// that its per-panel sums round as that kernel's do.
-template <int CPL>
-hipError_t launch_emax(const ScoreArgs& a, hipStream_t st) {
-    const unsigned g = (unsigned)a.M * (unsigned)a.np_e;
+// emax_kernel: the tabulated kernel's panel width, so that its per-panel
+// sums round as that kernel's do.  One wave per (pair, panel): pairs are
+// models in the affine mode, (model, batch size) pairs in the tabulated one.
+template <int CPL, bool AFF>
+hipError_t launch_emax_m(const ScoreArgs& a, hipStream_t st) {
+    const unsigned pairs = AFF ? (unsigned)a.Mg : (unsigned)a.Mg * (unsigned)a.nbs;
+    const unsigned g = pairs * (unsigned)a.np_e;
     const bool exact = a.K % (64 * CPL) == 0;
+    constexpr int CRL = (ORLOJ_MAX_PREFIX + 63) / 64;
     if (a.maxcap <= 64) {
-        if (exact) hipLaunchKernelGGL((emax_kernel<CPL, true, 1>), dim3(g), dim3(64), 0, st, a);
-        else hipLaunchKernelGGL((emax_kernel<CPL, false, 1>), dim3(g), dim3(64), 0, st, a);
+        if (exact) hipLaunchKernelGGL((emax_kernel<CPL, true, 1, AFF>), dim3(g), dim3(64), 0, st, a);
+        else hipLaunchKernelGGL((emax_kernel<CPL, false, 1, AFF>), dim3(g), dim3(64), 0, st, a);
     } else {
-        constexpr int CR = (ORLOJ_MAX_PREFIX + 63) / 64;
-        if (exact) hipLaunchKernelGGL((emax_kernel<CPL, true, CR>), dim3(g), dim3(64), 0, st, a);
-        else hipLaunchKernelGGL((emax_kernel<CPL, false, CR>), dim3(g), dim3(64), 0, st, a);
+        if (exact) hipLaunchKernelGGL((emax_kernel<CPL, true, CRL, AFF>), dim3(g), dim3(64), 0, st, a);
+        else hipLaunchKernelGGL((emax_kernel<CPL, false, CRL, AFF>), dim3(g), dim3(64), 0, st, a);
     }
     return hipGetLastError();
+}
+
+template <int CPL>
+hipError_t launch_emax(const ScoreArgs& a, hipStream_t st) {
+    return a.c1 ? launch_emax_m<CPL, true>(a, st) : launch_emax_m<CPL, false>(a, st);
 }
 
 template <int VPT>
@@ -2270,16 +2451,19 @@ namespace {
 // steps: max(longest workgroup, all work / slots), where a SIMD is worth
 // 1.5 slots (one wave alone on a SIMD runs at about half the rate three
 // waves sharing it reach together); a chunk size is taken only if it is 10%
-// faster than none.  Measured: this picks the fastest of none, 8, 16 and 32
+// faster than none.  Chunks of 4 only where the warm-up runs in its own
+// loop with a deep prefetch ring (launches with an E pre-pass); elsewhere
+// warm-up steps wait on their row loads.  Measured: this picks the fastest
+// of none, 8, 16 and 32
 // at configurations 1 to 3 and leaves configuration 5's saturated launch
 // and scheduling-loop rounds unsplit.
 int pick_chunk(const orloj_grid* g, const orloj_queues* qs, int mode, int64_t maxcap,
-               int64_t active, int simds, int panels) {
+               int64_t active, int simds, int panels, bool warm_loop) {
     if (2 * active > simds || panels > 2) return 0;
     const double slots = 1.5 * simds;
     constexpr double kWarm = 0.2;
-    constexpr int kCh[4] = {0, 32, 16, 8};
-    double total[4] = {0.0, 0.0, 0.0, 0.0}, longest[4] = {0.0, 0.0, 0.0, 0.0};
+    constexpr int kCh[5] = {0, 32, 16, 8, 4};
+    double total[5] = {0.0, 0.0, 0.0, 0.0, 0.0}, longest[5] = {0.0, 0.0, 0.0, 0.0, 0.0};
     for (int q = 0; q < g->n_models; ++q) {
         const int64_t N = qs->h_queue_off[q + 1] - qs->h_queue_off[q];
         if (N <= 0) continue;
@@ -2287,7 +2471,7 @@ int pick_chunk(const orloj_grid* g, const orloj_queues* qs, int mode, int64_t ma
             const int64_t n = ncap_of(N, g->batch_sizes[bi], mode);
             total[0] += (double)n;
             longest[0] = fmax(longest[0], (double)n);
-            for (int o = 1; o < 4; ++o) {
+            for (int o = 1; o < 5; ++o) {
                 const int64_t ch = kCh[o], k = (n + ch - 1) / ch;
                 total[o] += (double)n + kWarm * ch * (double)(k * (k - 1) / 2);
                 longest[o] = fmax(longest[o], kWarm * ch * (double)(k - 1) + (double)(n - (k - 1) * ch));
@@ -2297,8 +2481,8 @@ int pick_chunk(const orloj_grid* g, const orloj_queues* qs, int mode, int64_t ma
     const double t_none = fmax(longest[0], total[0] / slots);
     double t_best = t_none;
     int best = 0;
-    for (int o = 1; o < 4; ++o) {
-        if (kCh[o] >= maxcap) continue;
+    for (int o = 1; o < 5; ++o) {
+        if (kCh[o] >= maxcap || (kCh[o] < 8 && !warm_loop)) continue;
         const double t = fmax(longest[o], total[o] / slots);
         if (t < 0.9 * t_none && t < t_best) {
             t_best = t;
@@ -2355,9 +2539,13 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
     const int M = grid->n_models;
     if (M == 0) return ORLOJ_OK;
     int64_t maxcap = 0, total = 0, active = 0;
+    int n_act = 0;
+    int act[kMaxActive];
     for (int q = 0; q < M; ++q) {
         const int64_t N = queues->h_queue_off[q + 1] - queues->h_queue_off[q];
         if (N <= 0) continue;
+        if (n_act < kMaxActive) act[n_act] = q;
+        ++n_act;
         for (int bi = 0; bi < grid->n_bs; ++bi) {
             const int64_t c = ncap_of(N, grid->batch_sizes[bi], prefix_mode);
             if (c > maxcap) maxcap = c;
@@ -2375,13 +2563,26 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
     // bins per lane of the score kernel (the affine mode reads only its
     // members' bins, in narrower panels)
     const int cpl = d_c1 ? affine_chunk(grid->n_bins) : score_chunk(grid->n_bins);
+    const int panels = (grid->n_bins + 64 * cpl - 1) / (64 * cpl);
+    // Tabulated rows of more than two panels, in a launch too small to fill
+    // the chip or split into step chunks: every panel's E sums come from
+    // emax_kernel (one wave per (model, batch size, panel), in parallel),
+    // and the score waves walk only the panels that hold members (one, as
+    // far as the chunk cost model knows), so chunks repeat only those.
+    // Chunk setting 0 (never split) keeps the single pass.
+    const int simds = 4 * (ctx->n_cu > 0 ? ctx->n_cu : 256);
+    const bool esplit_ok = !d_c1 && panels > 2;
     const int chunk = ctx->chunk_pref >= 0
                           ? (ctx->chunk_pref < maxcap ? ctx->chunk_pref : 0)
-                          : pick_chunk(grid, queues, prefix_mode, maxcap, active,
-                                       4 * (ctx->n_cu > 0 ? ctx->n_cu : 256),
-                                       (grid->n_bins + 64 * cpl - 1) / (64 * cpl));
+                          : pick_chunk(grid, queues, prefix_mode, maxcap, active, simds,
+                                       esplit_ok ? 1 : panels, esplit_ok);
+    const bool esplit = esplit_ok && (chunk > 0 || (ctx->chunk_pref < 0 && 2 * active <= simds));
     const int nchunk = chunk ? (int)((maxcap + chunk - 1) / chunk) : 1;
-    const int64_t nblk = (int64_t)M * grid->n_bs * nchunk;
+    // only the models with a queue get workgroups, when they are few enough
+    // to list
+    const bool compact = n_act < M && n_act <= kMaxActive;
+    const int Mg = compact ? n_act : M;
+    const int64_t nblk = (int64_t)Mg * grid->n_bs * nchunk;
     if (nblk > 0x7fffffff) return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (model, batch size) pairs");
 
     ScoreArgs a;
@@ -2412,20 +2613,27 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
     a.nbs = grid->n_bs;
     a.rect = prefix_mode;
     a.maxcap = (int)maxcap;
+    a.Mg = Mg;
+    a.compact = compact ? 1 : 0;
     memset(a.bs, 0, sizeof a.bs);
     for (int i = 0; i < grid->n_bs; ++i) a.bs[i] = grid->batch_sizes[i];
+    memset(a.act, 0, sizeof a.act);
+    if (compact)
+        for (int i = 0; i < n_act; ++i) a.act[i] = act[i];
 
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
     a.psum = nullptr;
     a.np_e = 0;
     const int cple = score_chunk(grid->n_bins);
-    if (d_c1) {
-        // emax_kernel's panel sums: [M][panels][maxcap] floats, formed first
+    if (d_c1 || esplit) {
+        // emax_kernel's panel sums, formed first: [pairs][panels][maxcap]
+        // floats, pairs = models (affine) or (model, batch size) pairs
         const int64_t np = (grid->n_bins + 64 * cple - 1) / (64 * cple);
-        if ((int64_t)M * np > 0x7fffffff)
-            return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (model, panel) pairs");
-        const size_t need = (size_t)M * (size_t)np * (size_t)maxcap;
+        const int64_t pairs = d_c1 ? (int64_t)M : (int64_t)M * grid->n_bs;
+        if (pairs * np > 0x7fffffff)
+            return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (pair, panel) pairs");
+        const size_t need = (size_t)pairs * (size_t)np * (size_t)maxcap;
         if (fixed_psum) {
             if (need > fixed_floats)
                 return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED,
@@ -2718,11 +2926,23 @@ int orloj_select_batch(orloj_ctx* ctx, const orloj_grid* grid, const orloj_queue
     a.sel_score = d_sel_score;
     a.nbs = grid->n_bs;
     a.rect = prefix_mode;
+    a.M = M;
     memset(a.bs, 0, sizeof a.bs);
     for (int i = 0; i < grid->n_bs; ++i) a.bs[i] = grid->batch_sizes[i];
+    // the models with a queue, when they are few enough to list: one
+    // workgroup each (workgroup 0 also clears the others)
+    int n_act = 0;
+    for (int q = 0; q < M; ++q)
+        if (queues->h_queue_off[q + 1] > queues->h_queue_off[q]) {
+            if (n_act < kMaxActive) a.act[n_act] = q;
+            ++n_act;
+        }
+    a.compact = n_act < M && n_act <= kMaxActive;
+    a.n_act = n_act;
+    const unsigned g = a.compact ? (unsigned)std::max(n_act, 1) : (unsigned)M;
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-    hipLaunchKernelGGL(select_kernel, dim3((unsigned)M), dim3(kSelThreads), 0, ctx->stream, a);
+    hipLaunchKernelGGL(select_kernel, dim3(g), dim3(kSelThreads), 0, ctx->stream, a);
     e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(ctx, e, "select_kernel launch");
     return ORLOJ_OK;

@@ -2,7 +2,10 @@
 several workgroups, each rebuilding the batch CDF of the prefixes before its
 chunk with warm-up steps.  Every chunk size must give the bits of the
 unsplit launch (the same fma sequence per bin), in both batch laws and both
-prefix modes; the automatic choice is checked against the oracle as well."""
+prefix modes; the automatic choice is checked against the oracle as well.
+Tabulated rows of more than two panels take every panel's E sums from the
+emax_kernel pre-pass when the launch is chunked (the chunks then repeat only
+the member panels): those cases must give the unsplit bits too."""
 import dataclasses
 import sys
 
@@ -99,6 +102,16 @@ def test_config5_models_chunked(ctx):
     aw = W.affine(wl)
     ref = run(aw, ctx, 0)
     same_bits(run(aw, ctx, 16), ref)
+
+
+def test_small_config5_launch_against_the_oracle(ctx):
+    # the scheduling loop's shape: a few idle models, every batch size; the
+    # automatic choice chunks it and takes the E sums from the pre-pass
+    wl = W.make(5, models=[5, 64], workers=8, slo_scale=2.0)
+    got = run(wl, ctx, -1)
+    err = parity.compare(wl, got, oracle.score_workload(wl))
+    say("  cfg5, 2 models, automatic chunks: max errors", err)
+    same_bits(got, run(wl, ctx, 0))
 
 
 def test_bad_chunk_is_rejected(ctx):
