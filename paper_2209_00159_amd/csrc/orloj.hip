@@ -450,6 +450,12 @@ struct LaneCarry {
 #pragma unroll
         for (int r = 0; r < CR; ++r) v[r] = (l + 64 * r) == n ? x : v[r];
     }
+    // step n's value += x (wave-uniform), added by the lane that holds it
+    __device__ __forceinline__ void add(int n, float x) {
+        const int l = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+#pragma unroll
+        for (int r = 0; r < CR; ++r) v[r] = (l + 64 * r) == n ? v[r] + x : v[r];
+    }
     // value of step r * 64 + lane
     __device__ __forceinline__ float mine(int r) const { return v[r]; }
 };
@@ -472,6 +478,19 @@ struct LaneCarry64 {
         const uint32_t l = __builtin_bit_cast(uint32_t, lo.mine(r));
         const uint32_t h = __builtin_bit_cast(uint32_t, hi.mine(r));
         return __builtin_bit_cast(double, ((uint64_t)h << 32) | l);
+    }
+    // step n's value += x (wave-uniform), added by the lane that holds it:
+    // the same fp64 addition as get + set, without reading the lane out
+    __device__ __forceinline__ void add(int n, double x) {
+        const int l = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+#pragma unroll
+        for (int r = 0; r < CR; ++r) {
+            const double v = mine(r) + x;
+            const uint64_t u = __builtin_bit_cast(uint64_t, v);
+            const bool own = (l + 64 * r) == n;
+            lo.v[r] = own ? __builtin_bit_cast(float, (uint32_t)u) : lo.v[r];
+            hi.v[r] = own ? __builtin_bit_cast(float, (uint32_t)(u >> 32)) : hi.v[r];
+        }
     }
 };
 
@@ -718,10 +737,12 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     // Load the lane chunk starting at bin c0 of member n's row; chunks wholly
     // outside the row's support, and every chunk when `none` (the row's
     // values cannot change G), read a constant row instead.
-    auto load_step = [&](float (&v)[CPL], int n, int c0, bool none) {
+    // The member's support bounds go to lo / hi: the ring slot keeps them
+    // for the step that uses the row.
+    auto load_step = [&](float (&v)[CPL], int n, int c0, bool none, int& lo, int& hi) {
         const int c = __builtin_bit_cast(int, cls_r.get(n));
-        const int lo = __builtin_bit_cast(int, lo_r.get(n));
-        const int hi = __builtin_bit_cast(int, hi_r.get(n));
+        lo = __builtin_bit_cast(int, lo_r.get(n));
+        hi = __builtin_bit_cast(int, hi_r.get(n));
         const bool ones = !none && c0 + CPL <= lo, zeros = none || c0 >= hi;
         const float* src = tab_qb + (size_t)c * (size_t)K + c0;
         int lim = K - 1 - c0;
@@ -753,10 +774,11 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
 
     double Gacc[CPL];
     float buf[PF][CPL];
+    int slo[PF], shi[PF];                                 // the slots' support bounds
     int pf_p = 0, pf_n = ns;                              // prefetch position
 #pragma unroll
     for (int i = 0; i < PF; ++i) {
-        load_step(buf[i], pf_n, pf_p * PW + base, false);
+        load_step(buf[i], pf_n, pf_p * PW + base, false, slo[i], shi[i]);
         // keep the priming loads in ring order, as the loop issues them
         __builtin_amdgcn_sched_barrier(0);
         if (++pf_n == n1) { pf_n = ns; pf_p = min(pf_p + 1, NPW - 1); }
@@ -786,10 +808,11 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     auto warm_up = [&](int pp) {
         const int p0w = pp * PW, pbw = p0w + base;
         float wb[PFW][CPL];
+        int wlo[PFW], whi[PFW];
         bool zero = false;                   // G == 0 over the panel
 #pragma unroll
         for (int i = 0; i < PFW; ++i) {
-            load_step(wb[i], min(i, n0 - 1), pbw, false);
+            load_step(wb[i], min(i, n0 - 1), pbw, false, wlo[i], whi[i]);
             __builtin_amdgcn_sched_barrier(0);
         }
         for (int w0 = 0; w0 < n0; w0 += PFW) {
@@ -802,11 +825,11 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                         const float t = (EXACT || pbw + j < K) ? wb[i][j] : 0.0f;
                         Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
                     }
-                    zero = zero || min(p0w + PW, K) <= __builtin_bit_cast(int, lo_r.get(nw));
+                    zero = zero || min(p0w + PW, K) <= wlo[i];
                 }
 #pragma unroll
                 for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(Gacc[j])::"memory");
-                load_step(wb[i], min(nw + PFW, n0 - 1), pbw, zero);
+                load_step(wb[i], min(nw + PFW, n0 - 1), pbw, zero, wlo[i], whi[i]);
             }
         }
         pass_zero = zero;
@@ -833,8 +856,8 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             }
             const int p0 = p * PW;                        // first bin of the panel
             const int pbase = p0 + base;                  // first bin of this lane chunk
-            const int hi_n = __builtin_bit_cast(int, hi_r.get(n));
-            const int lo_n = __builtin_bit_cast(int, lo_r.get(n));
+            const int hi_n = shi[i];
+            const int lo_n = slo[i];
             const int mhi = min(mend, n + 1);             // members of this panel among the first n+1
             const bool real = n >= n0;                    // else a warm-up step
             const bool due = real && mlo < mhi;           // some member is scored at this step
@@ -868,7 +891,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(Gacc[j])::"memory");
             // G == 0 over the pass from here on: later steps of it need no row
             const bool zero_after = pass_zero || min(p0 + PW, K) <= lo_n;
-            load_step(buf[i], pf_n, pf_p * PW + base, zero_after && pf_p == p);
+            load_step(buf[i], pf_n, pf_p * PW + base, zero_after && pf_p == p, slo[i], shi[i]);
             if (++pf_n == n1) { pf_n = ns; pf_p = min(pf_p + 1, NPW - 1); }
             if (p < NPW && real) {                        // else a ghost or warm-up iteration
                 float etot = etot_prev, T = T_prev;
@@ -971,8 +994,8 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                         }
                         pP = wave_scan_sum64(pP);
                         pN = wave_scan_sum(pN);
-                        cP.set(n, cP.get(n) + lane63(pP));
-                        cN.set(n, cN.get(n) + lane63(pN));
+                        cP.add(n, lane63(pP));
+                        cN.add(n, lane63(pN));
                         wave_lds_fence();
                     }
                 }
@@ -981,7 +1004,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                     cW.set(n, fmaf(Win, dPW, T));
                     cGl.set(n, glast_here);
                 }
-                if constexpr (!ESPLIT) cE.set(n, cE.get(n) + (double)etot);
+                if constexpr (!ESPLIT) cE.add(n, (double)etot);
             }
             pass_zero = zero_after;
             if (++n == n1) {
@@ -1003,12 +1026,13 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         if (LASTP + 1 < NP) {
             constexpr int PFB = ORLOJ_EONLY_PREFETCH;   // its ring is deeper: fewer registers live here
             float bufb[PFB][CPL];
+            int blo[PFB], bhi[PFB];
             const int totalB = (NP - LASTP - 1) * n1;
             const int itersB = (totalB + PFB - 1) / PFB * PFB;
             int qf_p = LASTP + 1, qf_n = 0;
 #pragma unroll
             for (int i = 0; i < PFB; ++i) {
-                load_step(bufb[i], qf_n, qf_p * PW + base, false);
+                load_step(bufb[i], qf_n, qf_p * PW + base, false, blo[i], bhi[i]);
                 __builtin_amdgcn_sched_barrier(0);
                 if (++qf_n == n1) { qf_n = 0; qf_p = min(qf_p + 1, NP - 1); }
             }
@@ -1026,8 +1050,8 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                     }
                     const int p0 = pb * PW;
                     const int pbase = p0 + base;
-                    const int hi_n = __builtin_bit_cast(int, hi_r.get(nb));
-                    const int lo_n = __builtin_bit_cast(int, lo_r.get(nb));
+                    const int hi_n = bhi[i];
+                    const int lo_n = blo[i];
                     const bool real = nb >= n0;
                     const bool unchanged = zero_b || p0 >= hi_n;
                     const bool skip = pb >= NP || (real ? (nb > n0 && unchanged) : unchanged);
@@ -1047,7 +1071,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
 #pragma unroll
                     for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(Gacc[j])::"memory");
                     const bool zero_after = zero_b || min(p0 + PW, K) <= lo_n;
-                    load_step(bufb[i], qf_n, qf_p * PW + base, zero_after && qf_p == pb);
+                    load_step(bufb[i], qf_n, qf_p * PW + base, zero_after && qf_p == pb, blo[i], bhi[i]);
                     if (++qf_n == n1) { qf_n = 0; qf_p = min(qf_p + 1, NP - 1); }
                     if (pb < NP && real) {
                         float etot = eprev;
@@ -1059,7 +1083,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                             etot = lane63(wave_scan_sum(e));
                             eprev = etot;
                         }
-                        cE.set(nb, cE.get(nb) + (double)etot);
+                        cE.add(nb, (double)etot);
                     }
                     zero_b = zero_after;
                     if (++nb == n1) { nb = 0; ++pb; }
