@@ -896,8 +896,13 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             if (p < NPW && real) {                        // else a ghost or warm-up iteration
                 float etot = etot_prev, T = T_prev;
                 double glast_here = gl_prev;
-                const float Win = cW.get(n);              // carries in from the previous
-                const double glin64 = cGl.get(n);         // panel pass (zero in the first)
+                // carries in from the previous panel pass (zero in the first)
+                float Win = 0.0f;
+                double glin64 = 0.0;
+                if (p > 0) {
+                    Win = cW.get(n);
+                    glin64 = cGl.get(n);
+                }
                 const float glin = (float)glin64;
                 float A = 0.0f;
                 if (!skip) {
@@ -909,8 +914,10 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                         zqv[qq] = zc;
                     }
                     A = wave_wscan(zc, rp, w15, w31);
-                    T = lane63(A);                        // discounted prefix at the panel end
-                    T_prev = T;
+                    if (p < LASTP) {                      // carried into the next pass
+                        T = lane63(A);                    // discounted prefix at the panel end
+                        T_prev = T;
+                    }
                 }
                 if (!skip) {
                     if constexpr (!ESPLIT) {
@@ -921,8 +928,11 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                         const float e = (float)((double)CPL - gsum);
                         etot = lane63(wave_scan_sum(e));
                     }
-                    glast_here = lane63(Gacc[CPL - 1]);
-                    etot_prev = etot; gl_prev = glast_here;
+                    if (p < LASTP) {                      // carried into the next pass
+                        glast_here = lane63(Gacc[CPL - 1]);
+                        gl_prev = glast_here;
+                    }
+                    etot_prev = etot;
 
                     if (due) {
                         // snapshot of G over the panel, fp64, pairs of bins
