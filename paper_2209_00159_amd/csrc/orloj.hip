@@ -354,8 +354,11 @@ struct Quarters {
 
 // LDS layout of one workgroup (one wave), byte offsets:
 //   GD  g[64 CPL]   snapshot of G over the current panel, fp64; pairs of
-//                   bins interleaved (bins j, j+1 of lane l at pair
-//                   (j/2) 64 + l), so each lane writes 16 consecutive bytes
+//                   bins interleaved over the lanes, bins j, j+1 of lane l
+//                   at pair slot 64 (j/2) + (l ^ (j/2)): a lane writes 16
+//                   consecutive bytes, each write is a permutation of 64
+//                   consecutive slots, and the members that read the
+//                   different pairs of one lane chunk hit different banks
 //   KD  k[4]        constant slots (fp64): 0, 1, gl (G carried in), unused
 //   ZQ  zq[64 NQ]   quarter-end discounted prefixes of each lane chunk (f32)
 //   AA  A[64]       in-panel discounted scan of the lane chunk totals (f32)
@@ -379,8 +382,8 @@ __host__ __device__ constexpr size_t score_bytes_per_member() { return sizeof(Me
 template <int CPL>
 __device__ __forceinline__ int snap_byte(int r) {
     if constexpr (CPL >= 2) {
-        const int l = r / CPL, j = r - l * CPL;
-        return 8 * (((j >> 1) * 64 + l) * 2 + (j & 1));
+        const int l = r / CPL, j = r - l * CPL, jp = j >> 1;
+        return 8 * ((jp * 64 + (l ^ jp)) * 2 + (j & 1));
     } else {
         return 8 * r;
     }
@@ -940,7 +943,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                         if constexpr (CPL >= 2) {
 #pragma unroll
                             for (int j = 0; j < CPL; j += 2) {
-                                const int pair = (j >> 1) * 64 + lane;
+                                const int pair = (j >> 1) * 64 + (lane ^ (j >> 1));
                                 *reinterpret_cast<double2*>(smem_raw + L::GD + 16 * pair) =
                                     make_double2(Gacc[j], Gacc[j + 1]);
                             }
@@ -967,7 +970,10 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                             float g4[4];
                             if constexpr (Q::QW == 4) {
                                 const double2 t0 = *reinterpret_cast<const double2*>(f + mb.o4);
-                                const double2 t1 = *reinterpret_cast<const double2*>(f + mb.o4 + 16 * 64);
+                                // the quarter's second pair: its slot follows
+                                // the first's by 64, with the lane index's
+                                // low bit flipped (the first pair's index is even)
+                                const double2 t1 = *reinterpret_cast<const double2*>(f + ((mb.o4 + 16 * 64) ^ 16));
                                 g4[0] = (float)t0.x; g4[1] = (float)t0.y;
                                 g4[2] = (float)t1.x; g4[3] = (float)t1.y;
                             } else if constexpr (Q::QW == 2) {
