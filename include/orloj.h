@@ -249,9 +249,9 @@ int orloj_score_candidates_affine(orloj_ctx *ctx, const orloj_grid *grid, const 
  * of the context's grown block.  The library looks up that array's address
  * on a device once (the first orloj_create on it) and each device keeps
  * its array until the process ends.  A call needing more than
- * M x ceil(K / 1024) x (the longest prefix) floats of it returns
- * ORLOJ_E_UNSUPPORTED before any launch (configuration 5, 128 x 4 x 64,
- * needs 32 768).  ORLOJ_E_HIP if the array is unavailable on the context's
+ * M x ceil(K / 256) x (the longest prefix) floats of it returns
+ * ORLOJ_E_UNSUPPORTED before any launch (128 models of 4096 bins with
+ * prefixes up to 64 need 128 x 16 x 64 = 131 072).  ORLOJ_E_HIP if the array is unavailable on the context's
  * device.  Every entry a call reads is written earlier in the same call, so
  * nothing needs clearing; but all calls on one device share the one array,
  * so calls that may overlap on a device (other contexts, other streams,

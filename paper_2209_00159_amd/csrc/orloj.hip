@@ -1148,11 +1148,19 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
 // Rows are loaded PFE steps ahead; the class and support of step n sit in
 // lane n % 64, so a step's row address needs no memory round trip.
 // ---------------------------------------------------------------------------
+// Steps loaded ahead by an emax_kernel wave: the loads of a step wait on
+// nothing but the step's class, so a wave of narrow panels (few waves per
+// SIMD) keeps more rows in flight.  A power of two that divides 64.
+#ifndef ORLOJ_EMAX_PREFETCH_OF
+#define ORLOJ_EMAX_PREFETCH_OF(CPL) ((CPL) >= 16 ? 8 : (CPL) >= 8 ? 16 : 32)
+#endif
+
 template <int CPL, bool EXACT, int CR, bool AFF>
 __global__ __launch_bounds__(64) void emax_kernel(const ScoreArgs a) {
     using Q = Quarters<CPL>;
     constexpr int PW = 64 * CPL;
-    constexpr int PFE = 8;
+    constexpr int PFE = ORLOJ_EMAX_PREFETCH_OF(CPL);
+    static_assert(PFE > 0 && 64 % PFE == 0, "a block of 64 steps ends on a prefetch round");
     const int K = a.K;
     const int NP = (K + PW - 1) / PW;
     const unsigned pair = blockIdx.x / (unsigned)NP;
@@ -2665,7 +2673,11 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
     a.psum = nullptr;
     a.np_e = 0;
-    const int cple = score_chunk(grid->n_bins);
+    // emax_kernel's panels: the score waves' own in the tabulated mode (its
+    // sums must round as theirs do); in the affine mode the narrow panels of
+    // the affine score waves, so that four times as many waves share the
+    // products of a model's few hundred prefixes
+    const int cple = d_c1 ? cpl : score_chunk(grid->n_bins);
     if (d_c1 || esplit) {
         // emax_kernel's panel sums, formed first: [pairs][panels][maxcap]
         // floats, pairs = models (affine) or (model, batch size) pairs

@@ -61,7 +61,7 @@ def test_noalloc_matches_the_allocating_entry_point():
 
 def test_noalloc_refuses_calls_beyond_its_scratch():
     ctx = O.Context()
-    # 513 models x 8 panels (8192 bins) x 256-member prefixes > 2^20 floats
+    # 513 models x 32 panels (8192 bins) x 256-member prefixes > 2^20 floats
     wl = W.random_affine(82, n_models=513, queue_lens=[256] * 513, n_bins=8192, n_classes=2,
                          batch_sizes=(1, 256))
     sc = O.Scorer(wl, ctx)
