@@ -225,7 +225,7 @@ int orloj_score_candidates(orloj_ctx *ctx, const orloj_grid *grid, const float *
  * error (orloj_sync); that model's requests then score as dead.
  * The sums of 1 - G behind E[X] do not depend on the batch size, so they
  * are formed once per (model, prefix length) into a scratch block the
- * context owns (M x ceil(K / 1024) x the longest prefix floats).  The
+ * context owns (M x ceil(K / 256) x the longest prefix floats).  The
  * first call that needs a larger block waits for the context's
  * stream, frees the old block and allocates the new one (ORLOJ_E_NOMEM if
  * that fails); the block is reused by later calls and freed by
