@@ -96,6 +96,12 @@ __device__ __forceinline__ int wave_min_i32(int x) {
     return x;
 }
 
+__device__ __forceinline__ int wave_max_i32(int x) {
+#pragma unroll
+    for (int s = 1; s < 64; s <<= 1) x = max(x, __shfl_xor(x, s, 64));
+    return x;
+}
+
 template <int VPT>
 __global__ __launch_bounds__(kThreads) void cdf_kernel(const uint32_t* __restrict__ counts,
                                                        float* __restrict__ out,
@@ -512,6 +518,9 @@ struct LaneCarry64 {
 // warm-up steps that rebuild G over the steps before it.
 #ifndef ORLOJ_EONLY_PREFETCH
 #define ORLOJ_EONLY_PREFETCH 3   // iterations ahead in the E-only panels' loop
+#endif
+#ifndef ORLOJ_EONLY_CACHE
+#define ORLOJ_EONLY_CACHE 3      // classes whose slices the E-only loop keeps in registers
 #endif
 #ifndef ORLOJ_WARMUP_PREFETCH
 #define ORLOJ_WARMUP_PREFETCH 4  // steps ahead in a chunk's warm-up loop
@@ -1041,6 +1050,53 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     if constexpr (!ESPLIT) {
         if (LASTP + 1 < NP) {
             constexpr int PFB = ORLOJ_EONLY_PREFETCH;   // its ring is deeper: fewer registers live here
+            // Classes repeat along a deadline-ordered queue (fast classes
+            // come first), and a repeat's row slice has usually left L2 by
+            // the time the wave reads it again.  The RC classes with the
+            // most members (at most 64 members, one per lane) keep their
+            // slice of the current panel in registers for the pass: the
+            // class's first member in step order loads it through the ring
+            // as any step does and copies it, and its later members read the
+            // copy while the ring loads the constant row for them.  Same
+            // values, same bits.  (Where a step is skipped because G is 0
+            // over the panel, every later step of the pass is skipped too,
+            // so a copy taken then is never read.)
+            constexpr int RC = CR == 1 ? ORLOJ_EONLY_CACHE : 0;
+            constexpr int RCA = RC > 0 ? RC : 1;
+            // step code of member `lane`: RC (not cached), k < RC (a later
+            // member of cached class k), RC + 1 + k (its first member)
+            int rk_r = RC;
+            if constexpr (RC > 0) {
+                const int cl = lane < n1 ? __builtin_bit_cast(int, cls_r.v[0]) : -1 - lane;
+                int cnt = 0, first = 64;        // members with this lane's class, the first of them
+                for (int m = n1 - 1; m >= 0; --m) {
+                    const bool same = __builtin_amdgcn_readlane(cl, m) == cl;
+                    cnt += same ? 1 : 0;
+                    first = same ? m : first;
+                }
+                bool taken = lane >= n1;
+#pragma unroll
+                for (int k = 0; k < RC; ++k) {
+                    // most members first, ties to the earlier member; a
+                    // class with a single member gains nothing
+                    const int key = (taken || cnt < 2) ? -1 : (cnt << 6) | (63 - lane);
+                    const int best = wave_max_i32(key);
+                    if (best >= 0) {
+                        const int ck = __builtin_amdgcn_readlane(cl, 63 - (best & 63));
+                        if (cl == ck) rk_r = first == lane ? RC + 1 + k : k;
+                        taken = taken || cl == ck;
+                    }
+                }
+            }
+            auto code = [&](int n) -> int {
+                if constexpr (RC > 0) return __builtin_amdgcn_readlane(rk_r, n);
+                return RC;
+            };
+            float creg[RCA][CPL];
+#pragma unroll
+            for (int k = 0; k < RCA; ++k)
+#pragma unroll
+                for (int j = 0; j < CPL; ++j) creg[k][j] = 0.0f;
             float bufb[PFB][CPL];
             int blo[PFB], bhi[PFB];
             const int totalB = (NP - LASTP - 1) * n1;
@@ -1048,7 +1104,7 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             int qf_p = LASTP + 1, qf_n = 0;
 #pragma unroll
             for (int i = 0; i < PFB; ++i) {
-                load_step(bufb[i], qf_n, qf_p * PW + base, false, blo[i], bhi[i]);
+                load_step(bufb[i], qf_n, qf_p * PW + base, code(qf_n) < RC, blo[i], bhi[i]);
                 __builtin_amdgcn_sched_barrier(0);
                 if (++qf_n == n1) { qf_n = 0; qf_p = min(qf_p + 1, NP - 1); }
             }
@@ -1058,36 +1114,63 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
             for (int it0 = 0; it0 < itersB; it0 += PFB) {
 #pragma unroll
                 for (int i = 0; i < PFB; ++i) {
+                    const int p0 = pb * PW;
+                    const int pbase = p0 + base;
                     if (nb == 0) {
                         asm volatile("" ::: "memory");
 #pragma unroll
                         for (int j = 0; j < CPL; ++j) Gacc[j] = 1.0;
                         zero_b = false;
                     }
-                    const int p0 = pb * PW;
-                    const int pbase = p0 + base;
                     const int hi_n = bhi[i];
                     const int lo_n = blo[i];
                     const bool real = nb >= n0;
                     const bool unchanged = zero_b || p0 >= hi_n;
                     const bool skip = pb >= NP || (real ? (nb > n0 && unchanged) : unchanged);
                     double gs[Q::QW];
-                    if (!skip) {
+                    // G <- G (1 - t) over the lane's bins, t from the row
+                    // slice (ring slot or cache register)
+                    auto update = [&](const float (&tv)[CPL]) {
 #pragma unroll
                         for (int qq = 0; qq < Q::NQ; ++qq) {
 #pragma unroll
                             for (int r = 0; r < Q::QW; ++r) {
                                 const int j = qq * Q::QW + r;
-                                const float t = (EXACT || pbase + j < K) ? bufb[i][j] : 0.0f;
+                                const float t = (EXACT || pbase + j < K) ? tv[j] : 0.0f;
                                 Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
                                 gs[r] = qq == 0 ? Gacc[j] : gs[r] + Gacc[j];
                             }
                         }
+                    };
+                    const int kc = code(nb);
+                    // a cached class's first member: keep its slice
+#pragma unroll
+                    for (int k = 0; k < RC; ++k) {
+                        if (kc == RC + 1 + k) {
+                            asm volatile("" ::: "memory");
+#pragma unroll
+                            for (int j = 0; j < CPL; ++j) creg[k][j] = bufb[i][j];
+                        }
+                    }
+                    if (!skip) {
+                        bool done = false;
+#pragma unroll
+                        for (int k = 0; k < RC; ++k) {
+                            if (!done && kc == k) {
+                                // a real branch per slot (the asm keeps it
+                                // from becoming per-bin selects)
+                                asm volatile("" ::: "memory");
+                                update(creg[k]);
+                                done = true;
+                            }
+                        }
+                        if (!done) update(bufb[i]);
                     }
 #pragma unroll
                     for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(Gacc[j])::"memory");
                     const bool zero_after = zero_b || min(p0 + PW, K) <= lo_n;
-                    load_step(bufb[i], qf_n, qf_p * PW + base, zero_after && qf_p == pb, blo[i], bhi[i]);
+                    load_step(bufb[i], qf_n, qf_p * PW + base,
+                              (zero_after && qf_p == pb) || code(qf_n) < RC, blo[i], bhi[i]);
                     if (++qf_n == n1) { qf_n = 0; qf_p = min(qf_p + 1, NP - 1); }
                     if (pb < NP && real) {
                         float etot = eprev;

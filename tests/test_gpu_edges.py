@@ -342,3 +342,60 @@ def test_coherent_expected_finish(ctx, n, theta, bs):
     say(f"coherent n={n} theta={theta}: P of the longest prefix {G[0]:.6f}, "
         f"max |dE| {dE.max():.3e} at candidate {int(dE.argmax())}")
     parity.compare(wl, got, ora)
+
+
+# ---------------------------------------------------------------------------
+# The E-only loop's register copies of its most frequent classes' slices.
+# Queues dominated by a few classes (so the cached classes repeat), rows whose
+# mass sits in a window (so whole panels lie before a row's first bin with
+# mass, where G becomes 0, or after its last, where the row is 0): a cached
+# class's first member then falls on skipped steps, and its later members
+# must still see this pass's slice.  Ragged and exact grids, chunked launches
+# whose warm-up steps take the cached path too.
+# ---------------------------------------------------------------------------
+def window_counts(rng, B, C, K, total=TOTAL):
+    """[B, C, K] counts: each row's mass spread over a window of random start
+    and width (some near the grid's start, some near its end)."""
+    out = np.zeros((B, C, K), np.uint32)
+    for b in range(B):
+        for c in range(C):
+            w = int(rng.integers(1, K // 2))
+            a = int(rng.integers(0, K - w))
+            m = rng.random(w) + 0.05
+            cum = np.rint(np.cumsum(m) / m.sum() * total)
+            out[b, c, a:a + w] = np.diff(np.concatenate([[0.0], cum])).astype(np.uint32)
+    return out
+
+
+def repeated_class_case(seed, K):
+    rng = np.random.default_rng(9100 + seed)
+    M, C, bs = 2, 12, (8, 33, 64)
+    counts = np.stack([window_counts(rng, len(bs), C, K) for _ in range(M)])
+    # Zipf-like class draws: three or four classes take most members
+    p = 1.0 / np.arange(1, C + 1) ** 1.6
+    p /= p.sum()
+    queues, nows = [], []
+    for q in range(M):
+        n = 64 + 7 * q
+        cls = rng.permutation(C)[rng.choice(C, size=n, p=p)]
+        d = np.sort(rng.uniform(1.0, 200.0, n))           # in the first panel
+        queues.append((cls, d))
+        nows.append(0.0)
+    return explicit_workload(f"repeat-{seed}-K{K}", counts, bs, [1.0] * M, queues, nows)
+
+
+@gpu
+@pytest.mark.parametrize("K", [4096, 3000, 2048])
+@pytest.mark.parametrize("seed", range(3))
+def test_repeated_classes_cached_slices(ctx, seed, K):
+    wl = repeated_class_case(seed, K)
+    say(f"[repeated-class case] seed={seed} K={K}")
+    ora = oracle.score_workload(wl)
+    _, got = run_gpu(wl, ctx)
+    err = parity.compare(wl, got, ora)
+    say(f"  max errors {err}")
+    _, untrimmed = run_gpu(wl, ctx, trim=False)
+    same_bits(got, untrimmed)
+    for chunk in (0, 8):
+        _, split = run_gpu(wl, ctx, chunk=chunk)
+        same_bits(got, split)
