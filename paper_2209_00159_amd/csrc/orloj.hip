@@ -233,14 +233,37 @@ __device__ __forceinline__ double dpp64(double x) {
     return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
 }
 
-__device__ __forceinline__ double wave_scan_sum64(double x) {
-    x += dpp64<0x111>(x);
-    x += dpp64<0x112>(x);
-    x += dpp64<0x114>(x);
-    x += dpp64<0x118>(x);
-    x += dpp64<0x142, 0xa>(x);
-    x += dpp64<0x143, 0xc>(x);
-    return x;
+// Two wave sums at once.  v_permlane32_swap exchanges the upper half of x
+// with the lower half of y, so after one add lane l < 32 holds x_l + x_(l+32)
+// and lane l >= 32 holds y_(l-32) + y_l; a DPP sum within each half (rows of
+// 16, then row 0 into row 1 and row 2 into row 3) leaves the total of x in
+// lane 31 and that of y in lane 63.  Each total comes out of one fixed tree,
+// whatever the other value is.
+__device__ __forceinline__ float wave_pair_sum(float x, float y) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x),
+                                                    __builtin_bit_cast(unsigned, y), false, false);
+    float z = __builtin_bit_cast(float, (unsigned)r[0]) + __builtin_bit_cast(float, (unsigned)r[1]);
+    z += dpp<0x111>(z);
+    z += dpp<0x112>(z);
+    z += dpp<0x114>(z);
+    z += dpp<0x118>(z);
+    z += dpp<0x142, 0xa>(z);
+    return z;
+}
+
+__device__ __forceinline__ double wave_pair_sum64(double x, double y) {
+    const uint64_t ux = __builtin_bit_cast(uint64_t, x), uy = __builtin_bit_cast(uint64_t, y);
+    const auto lo = __builtin_amdgcn_permlane32_swap((unsigned)ux, (unsigned)uy, false, false);
+    const auto hi = __builtin_amdgcn_permlane32_swap((unsigned)(ux >> 32), (unsigned)(uy >> 32), false, false);
+    const double a = __builtin_bit_cast(double, ((uint64_t)(unsigned)hi[0] << 32) | (unsigned)lo[0]);
+    const double b = __builtin_bit_cast(double, ((uint64_t)(unsigned)hi[1] << 32) | (unsigned)lo[1]);
+    double z = a + b;
+    z += dpp64<0x111>(z);
+    z += dpp64<0x112>(z);
+    z += dpp64<0x114>(z);
+    z += dpp64<0x118>(z);
+    z += dpp64<0x142, 0xa>(z);
+    return z;
 }
 
 // 2^x by the hardware instruction; results below 2^-126 flush to 0.
@@ -423,6 +446,17 @@ __device__ __forceinline__ double lane63(double v) {
     const uint64_t u = __builtin_bit_cast(uint64_t, v);
     const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, 63);
     const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 63);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+// Value of lane L (a constant) in every lane.
+__device__ __forceinline__ float lane_read(float v, int L) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), L));
+}
+__device__ __forceinline__ double lane_read(double v, int L) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, L);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), L);
     return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
 
@@ -847,7 +881,15 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         pass_zero = zero;
     };
 
+    static_assert(PF % 2 == 0, "steps are reduced in pairs");
     for (int it0 = 0; it0 < iters; it0 += PF) {
+        // each scoring step's member sums (0 in lanes without a member) and
+        // its index (-1: no member scored)
+        double redP[PF];
+        float redN[PF];
+        int red_n[PF];
+#pragma unroll
+        for (int i = 0; i < PF; ++i) redP[i] = 0.0, redN[i] = 0.0f, red_n[i] = -1;
 #pragma unroll
         for (int i = 0; i < PF; ++i) {
             if (n == ns) {
@@ -1017,10 +1059,11 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                         } else {
                             for (int m = mlo + lane; m < mhi; m += 64) score_member(s_mem[m], m);
                         }
-                        pP = wave_scan_sum64(pP);
-                        pN = wave_scan_sum(pN);
-                        cP.add(n, lane63(pP));
-                        cN.add(n, lane63(pN));
+                        // reduced across the lanes with the other step of
+                        // its pair, after the pair
+                        redP[i] = pP;
+                        redN[i] = pN;
+                        red_n[i] = n;
                         wave_lds_fence();
                     }
                 }
@@ -1037,6 +1080,24 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
                 ++p;
                 mlo = __builtin_amdgcn_readlane(mlo_r, min(p, NP));
                 mend = __builtin_amdgcn_readlane(mlo_r, min(p + 1, NP));
+            }
+        }
+        // Sum P (fp64) and the priority terms (fp32) over the lanes, two
+        // steps at a time: each step's total comes out of the same tree
+        // whichever step it is paired with.
+#pragma unroll
+        for (int i = 0; i < PF; i += 2) {
+            if (red_n[i] >= 0 || red_n[i + 1] >= 0) {
+                const double zP = wave_pair_sum64(redP[i], redP[i + 1]);
+                const float zN = wave_pair_sum(redN[i], redN[i + 1]);
+                if (red_n[i] >= 0) {
+                    cP.add(red_n[i], lane_read(zP, 31));
+                    cN.add(red_n[i], lane_read(zN, 31));
+                }
+                if (red_n[i + 1] >= 0) {
+                    cP.add(red_n[i + 1], lane_read(zP, 63));
+                    cN.add(red_n[i + 1], lane_read(zN, 63));
+                }
             }
         }
     }
