@@ -300,6 +300,7 @@ struct ScoreArgs {
     float* psum;               // affine mode: [M][np_e][maxcap] panel sums of 1 - G
     int np_e;                  // panels of those sums (emax_kernel's panel width)
     int* err;
+    int defer;                 // 1: write the priority sum to S, leave E[L_B] and S to the selection
     int chunk;                 // prefix lengths scored per workgroup (0: all of them)
     int nchunk;                // workgroups per (model, batch size)
     double b;
@@ -550,6 +551,12 @@ struct LaneCarry64 {
 // deadline need only the sums of 1 - G: a second, lean loop takes them
 // (tabulated mode).  A workgroup may take a chunk of the steps only, after
 // warm-up steps that rebuild G over the steps before it.
+#ifndef ORLOJ_SCORE_PREFETCH
+#define ORLOJ_SCORE_PREFETCH 2   // iterations a row is loaded ahead of its use
+#endif
+#ifndef ORLOJ_SPLIT_PREFETCH
+#define ORLOJ_SPLIT_PREFETCH 4   // the same in launches with an E pre-pass
+#endif
 #ifndef ORLOJ_EONLY_PREFETCH
 #define ORLOJ_EONLY_PREFETCH 3   // iterations ahead in the E-only panels' loop
 #endif
@@ -560,7 +567,7 @@ struct LaneCarry64 {
 #define ORLOJ_WARMUP_PREFETCH 4  // steps ahead in a chunk's warm-up loop
 #endif
 template <int CPL, int PF, bool EXACT, int CR, bool AFF, bool ESPLIT>
-__global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
+__device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bid) {
     static_assert(ESPLIT || !AFF, "the affine mode takes its E sums from emax_kernel");
     using Q = Quarters<CPL>;
     constexpr int PW = 64 * CPL;                   // bins per panel
@@ -578,8 +585,8 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
     // Largest batch sizes first, and their last chunks first: those
     // workgroups run longest.
     const unsigned per_bs = (unsigned)a.Mg * (unsigned)a.nchunk;
-    const int bi = a.nbs - 1 - (int)(blockIdx.x / per_bs);
-    const unsigned rem = blockIdx.x % per_bs;
+    const int bi = a.nbs - 1 - (int)(bid / per_bs);
+    const unsigned rem = bid % per_bs;
     const int kc = a.nchunk - 1 - (int)(rem / (unsigned)a.Mg);
     const int q = grid_model(a, rem % (unsigned)a.Mg);
     const int64_t q0 = a.queue_off[q];
@@ -1258,19 +1265,31 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
         const int n = r * 64 + lane;
         if (n >= n0 && n < n1) {
             double esum = cE.mine(r);
-            if constexpr (ESPLIT) {
+            if (ESPLIT && !a.defer) {
                 // the panels' sums in panel order, as this kernel adds them
                 esum = 0.0;
                 const size_t pair = AFF ? (size_t)q : (size_t)q * (size_t)a.nbs + (size_t)bi;
                 const float* ps = a.psum + pair * (size_t)a.np_e * (size_t)maxcap + n;
                 for (int pp = 0; pp < a.np_e; ++pp) esum += (double)ps[(size_t)pp * (size_t)maxcap];
             }
-            const double el = c0q + w * (0.5 + esum);
             a.E[cand + n] = cP.mine(r);
-            a.EL[cand + n] = (float)el;
-            a.S[cand + n] = (float)((double)cN.mine(r) / el);
+            if (ESPLIT && a.defer) {
+                // the selection finishes E[L_B] and the score from the
+                // panel sums (same expression, same bits): it runs after
+                // emax_kernel's waves, which share this launch
+                a.S[cand + n] = cN.mine(r);
+            } else {
+                const double el = c0q + w * (0.5 + esum);
+                a.EL[cand + n] = (float)el;
+                a.S[cand + n] = (float)((double)cN.mine(r) / el);
+            }
         }
     }
+}
+
+template <int CPL, int PF, bool EXACT, int CR, bool AFF, bool ESPLIT>
+__global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
+    score_wave<CPL, PF, EXACT, CR, AFF, ESPLIT>(a, blockIdx.x);
 }
 
 // ---------------------------------------------------------------------------
@@ -1300,15 +1319,15 @@ __global__ __launch_bounds__(64) void score_kernel(const ScoreArgs a) {
 #endif
 
 template <int CPL, bool EXACT, int CR, bool AFF>
-__global__ __launch_bounds__(64) void emax_kernel(const ScoreArgs a) {
+__device__ __forceinline__ void emax_wave(const ScoreArgs& a, const unsigned bid) {
     using Q = Quarters<CPL>;
     constexpr int PW = 64 * CPL;
     constexpr int PFE = ORLOJ_EMAX_PREFETCH_OF(CPL);
     static_assert(PFE > 0 && 64 % PFE == 0, "a block of 64 steps ends on a prefetch round");
     const int K = a.K;
     const int NP = (K + PW - 1) / PW;
-    const unsigned pair = blockIdx.x / (unsigned)NP;
-    const int p = (int)(blockIdx.x - pair * (unsigned)NP);
+    const unsigned pair = bid / (unsigned)NP;
+    const int p = (int)(bid - pair * (unsigned)NP);
     int q, bi;
     size_t qb;                                  // the pair's rows and sums
     if constexpr (AFF) {
@@ -1420,6 +1439,25 @@ __global__ __launch_bounds__(64) void emax_kernel(const ScoreArgs a) {
     }
 }
 
+template <int CPL, bool EXACT, int CR, bool AFF>
+__global__ __launch_bounds__(64) void emax_kernel(const ScoreArgs a) {
+    emax_wave<CPL, EXACT, CR, AFF>(a, blockIdx.x);
+}
+
+// One launch for a scheduling round's tabulated scoring when the E sums come
+// from emax_kernel's waves: workgroups [0, n_emax) are those waves, the rest
+// score_kernel's (their E[L_B] and scores are finished by the selection,
+// which runs after the launch).  Nothing in the launch waits on anything
+// else in it, so the two kinds of waves run side by side.
+template <int CPL, bool EXACT, int CR>
+__global__ __launch_bounds__(64) void round_kernel(const ScoreArgs a, const unsigned n_emax) {
+    if (blockIdx.x < n_emax) {
+        emax_wave<CPL, EXACT, CR, false>(a, blockIdx.x);
+    } else {
+        score_wave<CPL, ORLOJ_SPLIT_PREFETCH, EXACT, CR, false, true>(a, blockIdx.x - n_emax);
+    }
+}
+
 // ---------------------------------------------------------------------------
 // select_kernel: one workgroup per model; thread i reads candidates i,
 // i + kSelThreads, ... (coalesced) and finds its (batch size, n) from the
@@ -1428,7 +1466,15 @@ __global__ __launch_bounds__(64) void emax_kernel(const ScoreArgs a) {
 struct SelectArgs {
     const int64_t* queue_off;
     const int64_t* cand_off;
-    const float* S;
+    float* S;                  // read; written too when finishing
+    // finishing (a scheduling round whose score launch left it here): each
+    // candidate's E[L_B] and score from emax_kernel's panel sums and the
+    // priority sum the score waves wrote to S
+    int finish;
+    const float* psum;         // [M][nbs][np_e][maxcap]
+    int np_e, maxcap;
+    const double* width;       // [M]
+    float* EL;
     int32_t* sel_n;
     int32_t* sel_bs;
     float* sel_score;
@@ -1512,8 +1558,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
     // (batch size, n) from the block starts.  The comparison is a total
     // order, so the pick does not depend on the order of the visits.
     const int64_t total = s_start[a.nbs];
+    const double wq = a.finish ? a.width[q] : 0.0;
     for (int64_t i = tid; i < total; i += kSelThreads) {
-        const float sc = S[i];
+        float sc = S[i];
         int lo = 0, hi = a.nbs - 1;          // last bi with s_start[bi] <= i
         while (lo < hi) {
             const int mid = (lo + hi + 1) >> 1;
@@ -1521,6 +1568,18 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
         }
         const int n = (int)(i - s_start[lo]) + 1;
         const int bsz = a.bs[lo];
+        if (a.finish) {
+            // E[L_B] = w (1/2 + the panels' sums in panel order) and the
+            // score, as the score waves form them when they finish
+            const float* ps = a.psum + ((size_t)q * (size_t)a.nbs + (size_t)lo) * (size_t)a.np_e *
+                                           (size_t)a.maxcap + (size_t)(n - 1);
+            double esum = 0.0;
+            for (int pp = 0; pp < a.np_e; ++pp) esum += (double)ps[(size_t)pp * (size_t)a.maxcap];
+            const double el = 0.0 + wq * (0.5 + esum);
+            sc = (float)((double)sc / el);
+            a.EL[a.cand_off[q] + i] = (float)el;
+            a.S[a.cand_off[q] + i] = sc;
+        }
         if (n <= bsz && sc == sc)            // NaN never wins
             take_if_better(best, Best{sc, n, bsz});
     }
@@ -2310,12 +2369,6 @@ int chunk_per_lane(int K) {
     return c;
 }
 
-#ifndef ORLOJ_SCORE_PREFETCH
-#define ORLOJ_SCORE_PREFETCH 2   // iterations a row is loaded ahead of its use
-#endif
-#ifndef ORLOJ_SPLIT_PREFETCH
-#define ORLOJ_SPLIT_PREFETCH 4   // the same in launches with an E pre-pass
-#endif
 
 template <int CPL, bool EXACT, int CR, bool AFF, bool ESPLIT>
 hipError_t launch_score_v(const ScoreArgs& a, unsigned grid, hipStream_t st) {
@@ -2413,6 +2466,31 @@ hipError_t launch_emax_m(const ScoreArgs& a, hipStream_t st) {
 template <int CPL>
 hipError_t launch_emax(const ScoreArgs& a, hipStream_t st) {
     return a.c1 ? launch_emax_m<CPL, true>(a, st) : launch_emax_m<CPL, false>(a, st);
+}
+
+template <int CPL, bool EXACT, int CR>
+hipError_t launch_round_v(const ScoreArgs& a, unsigned n_emax, unsigned grid, hipStream_t st) {
+    const size_t sm = score_fixed_bytes<CPL>() + (size_t)a.maxcap * score_bytes_per_member();
+    static size_t attr_bytes = 0;   // per template instance; device-independent
+    if (sm > attr_bytes) {
+        hipError_t e = hipFuncSetAttribute((const void*)round_kernel<CPL, EXACT, CR>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)sm);
+        if (e != hipSuccess) return e;
+        attr_bytes = sm;
+    }
+    hipLaunchKernelGGL((round_kernel<CPL, EXACT, CR>), dim3(grid), dim3(64), sm, st, a, n_emax);
+    return hipGetLastError();
+}
+
+template <int CPL>
+hipError_t launch_round(const ScoreArgs& a, unsigned n_emax, unsigned grid, hipStream_t st) {
+    constexpr int CRL = (ORLOJ_MAX_PREFIX + 63) / 64;
+    const bool exact = a.K % (64 * CPL) == 0;
+    if (a.maxcap <= 64)
+        return exact ? launch_round_v<CPL, true, 1>(a, n_emax, grid, st)
+                     : launch_round_v<CPL, false, 1>(a, n_emax, grid, st);
+    return exact ? launch_round_v<CPL, true, CRL>(a, n_emax, grid, st)
+                 : launch_round_v<CPL, false, CRL>(a, n_emax, grid, st);
 }
 
 template <int VPT>
@@ -2708,6 +2786,14 @@ int ensure_work(orloj_ctx* ctx, size_t bytes) {
     return ORLOJ_OK;
 }
 
+// A scheduling round's tabulated score launch that left E[L_B] and the
+// scores to the selection (orloj_internal_score_select).
+struct Deferred {
+    bool on = false;
+    const float* psum = nullptr;
+    int np_e = 0, maxcap = 0;
+};
+
 // Validation and launch shared by the tabulated and the affine scorer
 // (d_c0 / d_c1 NULL: tabulated).
 // fixed_psum (affine mode only): a caller-fixed block of fixed_floats
@@ -2718,7 +2804,8 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
                  const orloj_queues* queues, double b_expo_per_ms, int32_t prefix_mode,
                  const int64_t* d_cand_off, const int64_t* d_prob_off, float* d_finish_prob,
                  double* d_expected_finish, float* d_expected_latency_ms, float* d_score,
-                 float* fixed_psum = nullptr, size_t fixed_floats = 0) {
+                 float* fixed_psum = nullptr, size_t fixed_floats = 0,
+                 Deferred* defer = nullptr) {
     if (!ctx) return ORLOJ_E_INVALID;
     int rc = check_grid(ctx, grid);
     if (rc) return rc;
@@ -2778,6 +2865,7 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
     if (nblk > 0x7fffffff) return orloj_ctx_fail(ctx, ORLOJ_E_UNSUPPORTED, "too many (model, batch size) pairs");
 
     ScoreArgs a;
+    a.defer = 0;
     a.chunk = chunk;
     a.nchunk = nchunk;
     a.tab = d_ccdf;
@@ -2843,6 +2931,26 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
             a.psum = (float*)ctx->d_work;
         }
         a.np_e = (int)np;
+        if (defer && !d_c1 && cple == cpl) {
+            // a scheduling round: emax_kernel's and score_kernel's waves in
+            // one launch, E[L_B] and the scores finished by the selection
+            a.defer = 1;
+            const unsigned n_emax = (unsigned)(Mg * grid->n_bs) * (unsigned)np;
+            const unsigned g = n_emax + (unsigned)nblk;
+            switch (cpl) {
+                case 1: e = launch_round<1>(a, n_emax, g, ctx->stream); break;
+                case 2: e = launch_round<2>(a, n_emax, g, ctx->stream); break;
+                case 4: e = launch_round<4>(a, n_emax, g, ctx->stream); break;
+                case 8: e = launch_round<8>(a, n_emax, g, ctx->stream); break;
+                default: e = launch_round<16>(a, n_emax, g, ctx->stream); break;
+            }
+            if (e != hipSuccess) return hip_fail(ctx, e, "round_kernel launch");
+            defer->on = true;
+            defer->psum = a.psum;
+            defer->np_e = a.np_e;
+            defer->maxcap = a.maxcap;
+            return ORLOJ_OK;
+        }
         switch (cple) {
             case 1: e = launch_emax<1>(a, ctx->stream); break;
             case 2: e = launch_emax<2>(a, ctx->stream); break;
@@ -2863,6 +2971,63 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
         default: e = launch_score<16>(a, g, ctx->stream); break;
     }
     if (e != hipSuccess) return hip_fail(ctx, e, "score_kernel launch");
+    return ORLOJ_OK;
+}
+
+// orloj_select_batch, and the finishing selection of a scheduling round
+// (fin->on: E[L_B] and the scores are formed here from the panel sums and
+// the priority sums in d_score, and written to d_EL and d_score).
+int select_common(orloj_ctx* ctx, const orloj_grid* grid, const orloj_queues* queues,
+                  int32_t prefix_mode, const int64_t* d_cand_off, float* d_score,
+                  int32_t* d_sel_n, int32_t* d_sel_bs, float* d_sel_score, const Deferred* fin,
+                  float* d_EL) {
+    if (!ctx) return ORLOJ_E_INVALID;
+    int rc = check_grid(ctx, grid);
+    if (rc) return rc;
+    rc = check_queues(ctx, grid, queues);
+    if (rc) return rc;
+    if (prefix_mode != ORLOJ_PREFIX_TRIANGLE && prefix_mode != ORLOJ_PREFIX_RECT)
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "prefix_mode %d", prefix_mode);
+    const int M = grid->n_models;
+    if (M == 0) return ORLOJ_OK;
+    if (!d_cand_off || !d_sel_n || !d_sel_bs || !d_sel_score)
+        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
+    const int64_t total = queues->h_queue_off[M];
+    if (total > 0 && !d_score) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "d_score is NULL");
+    SelectArgs a;
+    a.finish = fin && fin->on ? 1 : 0;
+    a.psum = a.finish ? fin->psum : nullptr;
+    a.np_e = a.finish ? fin->np_e : 0;
+    a.maxcap = a.finish ? fin->maxcap : 0;
+    a.width = grid->d_bin_width_ms;
+    a.EL = d_EL;
+    a.queue_off = queues->d_queue_off;
+    a.cand_off = d_cand_off;
+    a.S = d_score;
+    a.sel_n = d_sel_n;
+    a.sel_bs = d_sel_bs;
+    a.sel_score = d_sel_score;
+    a.nbs = grid->n_bs;
+    a.rect = prefix_mode;
+    a.M = M;
+    memset(a.bs, 0, sizeof a.bs);
+    for (int i = 0; i < grid->n_bs; ++i) a.bs[i] = grid->batch_sizes[i];
+    // the models with a queue, when they are few enough to list: one
+    // workgroup each (workgroup 0 also clears the others)
+    int n_act = 0;
+    for (int q = 0; q < M; ++q)
+        if (queues->h_queue_off[q + 1] > queues->h_queue_off[q]) {
+            if (n_act < kMaxActive) a.act[n_act] = q;
+            ++n_act;
+        }
+    a.compact = n_act < M && n_act <= kMaxActive;
+    a.n_act = n_act;
+    const unsigned g = a.compact ? (unsigned)std::max(n_act, 1) : (unsigned)M;
+    hipError_t e = hipSetDevice(ctx->device);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    hipLaunchKernelGGL(select_kernel, dim3(g), dim3(kSelThreads), 0, ctx->stream, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(ctx, e, "select_kernel launch");
     return ORLOJ_OK;
 }
 
@@ -3100,48 +3265,24 @@ int orloj_accumulate(orloj_ctx* ctx, const orloj_grid* grid, int64_t n_samples,
 int orloj_select_batch(orloj_ctx* ctx, const orloj_grid* grid, const orloj_queues* queues,
                        int32_t prefix_mode, const int64_t* d_cand_off, const float* d_score,
                        int32_t* d_sel_n, int32_t* d_sel_bs, float* d_sel_score) {
-    if (!ctx) return ORLOJ_E_INVALID;
-    int rc = check_grid(ctx, grid);
-    if (rc) return rc;
-    rc = check_queues(ctx, grid, queues);
-    if (rc) return rc;
-    if (prefix_mode != ORLOJ_PREFIX_TRIANGLE && prefix_mode != ORLOJ_PREFIX_RECT)
-        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "prefix_mode %d", prefix_mode);
-    const int M = grid->n_models;
-    if (M == 0) return ORLOJ_OK;
-    if (!d_cand_off || !d_sel_n || !d_sel_bs || !d_sel_score)
-        return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "NULL device buffer");
-    const int64_t total = queues->h_queue_off[M];
-    if (total > 0 && !d_score) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "d_score is NULL");
-    SelectArgs a;
-    a.queue_off = queues->d_queue_off;
-    a.cand_off = d_cand_off;
-    a.S = d_score;
-    a.sel_n = d_sel_n;
-    a.sel_bs = d_sel_bs;
-    a.sel_score = d_sel_score;
-    a.nbs = grid->n_bs;
-    a.rect = prefix_mode;
-    a.M = M;
-    memset(a.bs, 0, sizeof a.bs);
-    for (int i = 0; i < grid->n_bs; ++i) a.bs[i] = grid->batch_sizes[i];
-    // the models with a queue, when they are few enough to list: one
-    // workgroup each (workgroup 0 also clears the others)
-    int n_act = 0;
-    for (int q = 0; q < M; ++q)
-        if (queues->h_queue_off[q + 1] > queues->h_queue_off[q]) {
-            if (n_act < kMaxActive) a.act[n_act] = q;
-            ++n_act;
-        }
-    a.compact = n_act < M && n_act <= kMaxActive;
-    a.n_act = n_act;
-    const unsigned g = a.compact ? (unsigned)std::max(n_act, 1) : (unsigned)M;
-    hipError_t e = hipSetDevice(ctx->device);
-    if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-    hipLaunchKernelGGL(select_kernel, dim3(g), dim3(kSelThreads), 0, ctx->stream, a);
-    e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(ctx, e, "select_kernel launch");
-    return ORLOJ_OK;
+    return select_common(ctx, grid, queues, prefix_mode, d_cand_off, const_cast<float*>(d_score),
+                         d_sel_n, d_sel_bs, d_sel_score, nullptr, nullptr);
 }
 
 }  // extern "C"
+
+int orloj_internal_score_select(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
+                                const int32_t* d_support, const orloj_queues* queues,
+                                double b_expo_per_ms, const int64_t* d_cand_off,
+                                const int64_t* d_prob_off, float* d_finish_prob,
+                                double* d_expected_finish, float* d_expected_latency_ms,
+                                float* d_score, int32_t* d_sel_n, int32_t* d_sel_bs,
+                                float* d_sel_score) {
+    Deferred fin;
+    int rc = score_common(ctx, grid, d_ccdf, d_support, nullptr, nullptr, queues, b_expo_per_ms,
+                          ORLOJ_PREFIX_TRIANGLE, d_cand_off, d_prob_off, d_finish_prob,
+                          d_expected_finish, d_expected_latency_ms, d_score, nullptr, 0, &fin);
+    if (rc) return rc;
+    return select_common(ctx, grid, queues, ORLOJ_PREFIX_TRIANGLE, d_cand_off, d_score, d_sel_n,
+                         d_sel_bs, d_sel_score, &fin, d_expected_latency_ms);
+}

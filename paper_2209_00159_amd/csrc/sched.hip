@@ -6,8 +6,10 @@
 //                          (§3.2 Algorithm 1), and one decision round per
 //                          call: every idle model's queue is staged in
 //                          pinned memory, uploaded in one copy, scored and
-//                          a batch selected per model (orloj_score_candidates
-//                          + orloj_select_batch), the selections read back,
+//                          a batch selected per model (the outputs of
+//                          orloj_score_candidates + orloj_select_batch, the
+//                          E pre-pass sharing the score launch), the
+//                          selections read back,
 //                          and the chosen members popped;
 //   orloj_simulate_trace   a trace-driven run of one worker per model on top
 //                          of it (one batch at a time, §3.1): the arrivals
@@ -165,12 +167,12 @@ int decide(orloj_sched* s, double now, const uint8_t* idle, int32_t* sel_n, int3
         dq.d_cost = nullptr;
         const int64_t* d_coff = reinterpret_cast<const int64_t*>(s->d_stage + o1);
         const int64_t* d_poff = reinterpret_cast<const int64_t*>(s->d_stage + 2 * o1);
-        rc = orloj_score_candidates(ctx, &s->grid, s->d_ccdf, s->d_support, &dq, s->b,
-                                    ORLOJ_PREFIX_TRIANGLE, d_coff, d_poff, s->d_P, s->d_E, s->d_EL,
-                                    s->d_S);
-        if (rc) return drained(rc);
-        rc = orloj_select_batch(ctx, &s->grid, &dq, ORLOJ_PREFIX_TRIANGLE, d_coff, s->d_S, s->d_sel,
-                                s->d_sel + M, reinterpret_cast<float*>(s->d_sel + 2 * M));
+        // scoring and selection: the outputs of orloj_score_candidates and
+        // orloj_select_batch, with the E pre-pass and the score waves of a
+        // small round in one launch
+        rc = orloj_internal_score_select(ctx, &s->grid, s->d_ccdf, s->d_support, &dq, s->b, d_coff,
+                                         d_poff, s->d_P, s->d_E, s->d_EL, s->d_S, s->d_sel,
+                                         s->d_sel + M, reinterpret_cast<float*>(s->d_sel + 2 * M));
         if (rc) return drained(rc);
         // the select kernel writes the selections straight into mapped
         // host memory: no copy, the stream's completion makes them visible

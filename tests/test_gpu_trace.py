@@ -104,3 +104,23 @@ def test_native_runtime_rounds():
     with _pt.raises(O.OrlojError):
         sched.admit([0, 5], [0, 0], [1.0, 2.0])
     assert sched.queue_length(0) == k_cls.size - n
+
+
+def test_native_round_selections_equal_the_public_calls():
+    """The runtime scores a round through its own launch (the E pre-pass and
+    the score waves together, E[L_B] and the scores finished by the
+    selection); its selections must be those of orloj_score_candidates +
+    orloj_select_batch on the same queue, exactly (the same bits decide)."""
+    ctx = O.Context()
+    models = list(range(8))
+    say("config 5 native loop: 8 models, 2000 arrivals, every decision recorded")
+    loop = S.config5_loop(2000, ctx=ctx, models=models, workers=8, native=True, record_every=1,
+                          record_limit=80)
+    st = loop.run()
+    assert len(st.recorded) == 80
+    wl = loop.wl
+    for dec in st.recorded:
+        sub = wl.subset([dec.model]).with_queues([(dec.cls, dec.deadline_ms)], [dec.now_ms])
+        got = O.Scorer(sub, ctx).run()
+        assert (int(got["sel_n"][0]), int(got["sel_bs"][0])) == (dec.sel_n, dec.sel_bs), \
+            (dec.model, dec.now_ms, (dec.sel_n, dec.sel_bs), (got["sel_n"][0], got["sel_bs"][0]))
