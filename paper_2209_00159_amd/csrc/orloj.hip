@@ -778,6 +778,18 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
     const float w31 = exp2_hw(log2d * (float)(CPL * (lane >= 32 ? lane - 31 : 0)));
     const float dQ = exp2_hw(log2d * (float)Q::QW);
     const float dq1 = exp2f(log2d);                   // d in fp32
+    // A member's in-quarter discounted prefix up to bin k-2, the quarter's
+    // r-th bin being bin k-2 (rq = r <= 3): sum over j <= rq of
+    // d^(rq - j) G_j, formed as a dot product with these weights (all 0
+    // when the member needs no quarter term, rq = kNoQuarter).
+    const float dq2 = dq1 * dq1, dq3 = dq2 * dq1;
+    auto quarter_weights = [&](int rq, float (&wv)[4]) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int e = rq - r;
+            wv[r] = (e < 0 || rq > 3) ? 0.0f : e == 0 ? 1.0f : e == 1 ? dq1 : e == 2 ? dq2 : dq3;
+        }
+    };
     const float dPW = exp2_hw(log2d * (float)PW);
 
     // Home panel of the last member (the latest deadline): past it no member
@@ -796,7 +808,11 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
         const int c = __builtin_bit_cast(int, cls_r.get(n));
         lo = __builtin_bit_cast(int, lo_r.get(n));
         hi = __builtin_bit_cast(int, hi_r.get(n));
-        const bool ones = !none && c0 + CPL <= lo, zeros = none || c0 >= hi;
+        // The affine mode's solo table (M x C rows) stays in the Infinity
+        // Cache, so it reads every chunk rather than spend a per-lane test
+        // and select on each load; entries outside the support are exactly
+        // 1 and 0 either way.
+        const bool ones = !AFF && !none && c0 + CPL <= lo, zeros = none || (!AFF && c0 >= hi);
         const float* src = tab_qb + (size_t)c * (size_t)K + c0;
         int lim = K - 1 - c0;
         if (ones || zeros) {
@@ -848,6 +864,8 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
     // skipped.
     bool pass_zero = false;                  // G == 0 on every bin of this pass's panel
     Member pass_mb;                          // CR == 1: this lane's member of the pass
+    double pass_th = 0.0;                    //   and its position in bin k, fp64,
+    float pass_wq[4] = {0.0f, 0.0f, 0.0f, 0.0f};   // and its quarter weights
     bool pass_valid = false;
     float etot_prev = 0.0f, T_prev = 0.0f;
     double gl_prev = 0.0;
@@ -913,6 +931,8 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
                     // pass at every step, so its plan is read from LDS once
                     pass_valid = mlo + lane < mend;
                     pass_mb = s_mem[min(mlo + lane, n1 - 1)];
+                    pass_th = (double)pass_mb.theta + (double)pass_mb.thlo;
+                    quarter_weights(pass_mb.rq, pass_wq);
                 }
             }
             const int p0 = p * PW;                        // first bin of the panel
@@ -1016,7 +1036,7 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
                         double pP = 0.0;
                         float pN = 0.0f;
                         const int nn = n + 1;
-                        auto score_member = [&](const Member& mb, int m) {
+                        auto score_member = [&](const Member& mb, int m, double th, const float (&wq4)[4]) {
                             const unsigned char* f = smem_raw;
                             auto atf = [&](int off) { return *reinterpret_cast<const float*>(f + off); };
                             auto atd = [&](int off) { return *reinterpret_cast<const double*>(f + off); };
@@ -1043,17 +1063,13 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
                                 g4[1] = g4[2] = g4[3] = 0.0f;
                             }
                             // discounted prefix of the quarter up to bin k-2
-                            // (0 when the member needs no quarter term)
-                            const int rq = mb.rq;
-                            float z4 = rq <= 3 ? g4[0] : 0.0f;
-#pragma unroll
-                            for (int r = 1; r < 4; ++r) z4 = r <= rq && rq <= 3 ? fmaf(z4, dq1, g4[r]) : z4;
+                            // (weights 0 when the member needs no quarter term)
+                            const float z4 = fmaf(wq4[0], g4[0], fmaf(wq4[1], g4[1], fmaf(wq4[2], g4[2], wq4[3] * g4[3])));
                             const float zin = fmaf(mb.fq, zq0, z4);
                             const float Zv = fmaf(mb.cW, Win, fmaf(mb.cG, glin, fmaf(mb.cA, al0, zin)));
                             const float gk = (float)gk64, gk1 = (float)gk164;
                             const float h = gk1 - gk;
                             // P in fp64: the expected finish count sums it
-                            const double th = (double)mb.theta + (double)mb.thlo;
                             const double P64 = fma(th, gk164 - gk64, gk64);
                             const float num = mb.cost * fmaf(mb.cg, fmaf(-omd, Zv, gk), h * mb.psi);
                             a.P[prob + (int64_t)n * nn / 2 + m] = (float)P64;
@@ -1062,9 +1078,14 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
                         };
                         if constexpr (CR == 1) {
                             // the lane's member of this pass, already in registers
-                            if (pass_valid && mlo + lane < mhi) score_member(pass_mb, mlo + lane);
+                            if (pass_valid && mlo + lane < mhi) score_member(pass_mb, mlo + lane, pass_th, pass_wq);
                         } else {
-                            for (int m = mlo + lane; m < mhi; m += 64) score_member(s_mem[m], m);
+                            for (int m = mlo + lane; m < mhi; m += 64) {
+                                const Member mb = s_mem[m];
+                                float wq4[4];
+                                quarter_weights(mb.rq, wq4);
+                                score_member(mb, m, (double)mb.theta + (double)mb.thlo, wq4);
+                            }
                         }
                         // reduced across the lanes with the other step of
                         // its pair, after the pair
