@@ -204,13 +204,30 @@ __device__ __forceinline__ float dpp(float x) {
 // Inclusive wave64 scan with geometric weights: lane L ends with
 // sum_{L' <= L} x_{L'} r^(L - L').  rp[i] = r^(2^i); w15 = r^((L & 15) + 1);
 // w31 = r^(L - 31) for lanes >= 32.
+// Each stage is x <- x' r + x with x' the DPP-moved x (0 where a lane has no
+// source, and rows outside the row mask keep x): one v_fmac_f32 with the
+// DPP move on its first source.  The compiler emits a separate move and
+// fma per stage, so the stages are written out; a VALU write of a VGPR
+// needs two wait states before a DPP read of it (s_nop 1), and the last
+// stage is followed by two as well, since the compiler cannot see into the
+// block when it places the next reader.
 __device__ __forceinline__ float wave_wscan(float x, const float (&rp)[4], float w15, float w31) {
-    x = fmaf(dpp<0x111>(x), rp[0], x);
-    x = fmaf(dpp<0x112>(x), rp[1], x);
-    x = fmaf(dpp<0x114>(x), rp[2], x);
-    x = fmaf(dpp<0x118>(x), rp[3], x);
-    x = fmaf(dpp<0x142, 0xa>(x), w15, x);
-    x = fmaf(dpp<0x143, 0xc>(x), w31, x);
+    asm volatile(
+        "s_nop 1\n\t"
+        "v_fmac_f32_dpp %0, %0, %1 row_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+        "s_nop 1\n\t"
+        "v_fmac_f32_dpp %0, %0, %2 row_shr:2 row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+        "s_nop 1\n\t"
+        "v_fmac_f32_dpp %0, %0, %3 row_shr:4 row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+        "s_nop 1\n\t"
+        "v_fmac_f32_dpp %0, %0, %4 row_shr:8 row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+        "s_nop 1\n\t"
+        "v_fmac_f32_dpp %0, %0, %5 row_bcast:15 row_mask:0xa bank_mask:0xf bound_ctrl:1\n\t"
+        "s_nop 1\n\t"
+        "v_fmac_f32_dpp %0, %0, %6 row_bcast:31 row_mask:0xc bank_mask:0xf bound_ctrl:1\n\t"
+        "s_nop 1"
+        : "+v"(x)
+        : "v"(rp[0]), "v"(rp[1]), "v"(rp[2]), "v"(rp[3]), "v"(w15), "v"(w31));
     return x;
 }
 
@@ -1073,8 +1090,10 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
                             const double P64 = fma(th, gk164 - gk64, gk64);
                             const float num = mb.cost * fmaf(mb.cg, fmaf(-omd, Zv, gk), h * mb.psi);
                             a.P[prob + (int64_t)n * nn / 2 + m] = (float)P64;
-                            pP += P64;
-                            pN += num;
+                            // (one member per lane and pass when CR == 1:
+                            // its values, not a sum with 0)
+                            pP = CR == 1 ? P64 : pP + P64;
+                            pN = CR == 1 ? num : pN + num;
                         };
                         if constexpr (CR == 1) {
                             // the lane's member of this pass, already in registers
