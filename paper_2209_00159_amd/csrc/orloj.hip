@@ -1511,6 +1511,12 @@ struct SelectArgs {
     // candidate's E[L_B] and score from emax_kernel's panel sums and the
     // priority sum the score waves wrote to S
     int finish;
+    // scheduling rounds (mapped host memory, or NULL): after its writes,
+    // each workgroup g makes them visible to the host and writes `round`
+    // to done[g], so the host can see the round finish without waiting for
+    // the stream
+    int32_t* done;
+    int32_t round;
     const float* psum;         // [M][nbs][np_e][maxcap]
     int np_e, maxcap;
     const double* width;       // [M]
@@ -1569,7 +1575,14 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
                 }
             }
         }
-        if ((int)blockIdx.x >= a.n_act) return;
+        if ((int)blockIdx.x >= a.n_act) {
+            if (a.done) {                    // the clears above, then the flag
+                __threadfence_system();
+                __syncthreads();
+                if (tid == 0) __hip_atomic_store(&a.done[blockIdx.x], a.round, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+            }
+            return;
+        }
     }
     const int q = a.compact ? a.act[blockIdx.x] : (int)blockIdx.x;
     __shared__ int64_t s_wsum[kSelWaves];
@@ -1655,6 +1668,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
                 a.sel_score[q] = 0.0f;
             }
         }
+    }
+    if (a.done) {                            // every thread's writes, then the flag
+        __threadfence_system();
+        __syncthreads();
+        if (tid == 0) __hip_atomic_store(&a.done[blockIdx.x], a.round, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     }
 }
 
@@ -3020,7 +3038,7 @@ int score_common(orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf,
 int select_common(orloj_ctx* ctx, const orloj_grid* grid, const orloj_queues* queues,
                   int32_t prefix_mode, const int64_t* d_cand_off, float* d_score,
                   int32_t* d_sel_n, int32_t* d_sel_bs, float* d_sel_score, const Deferred* fin,
-                  float* d_EL) {
+                  float* d_EL, int32_t* d_done = nullptr, int32_t round = 0, int* n_groups = nullptr) {
     if (!ctx) return ORLOJ_E_INVALID;
     int rc = check_grid(ctx, grid);
     if (rc) return rc;
@@ -3036,6 +3054,8 @@ int select_common(orloj_ctx* ctx, const orloj_grid* grid, const orloj_queues* qu
     if (total > 0 && !d_score) return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "d_score is NULL");
     SelectArgs a;
     a.finish = fin && fin->on ? 1 : 0;
+    a.done = d_done;
+    a.round = round;
     a.psum = a.finish ? fin->psum : nullptr;
     a.np_e = a.finish ? fin->np_e : 0;
     a.maxcap = a.finish ? fin->maxcap : 0;
@@ -3063,6 +3083,7 @@ int select_common(orloj_ctx* ctx, const orloj_grid* grid, const orloj_queues* qu
     a.compact = n_act < M && n_act <= kMaxActive;
     a.n_act = n_act;
     const unsigned g = a.compact ? (unsigned)std::max(n_act, 1) : (unsigned)M;
+    if (n_groups) *n_groups = (int)g;
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
     hipLaunchKernelGGL(select_kernel, dim3(g), dim3(kSelThreads), 0, ctx->stream, a);
@@ -3317,12 +3338,12 @@ int orloj_internal_score_select(orloj_ctx* ctx, const orloj_grid* grid, const fl
                                 const int64_t* d_prob_off, float* d_finish_prob,
                                 double* d_expected_finish, float* d_expected_latency_ms,
                                 float* d_score, int32_t* d_sel_n, int32_t* d_sel_bs,
-                                float* d_sel_score) {
+                                float* d_sel_score, int32_t* d_done, int32_t round, int* n_groups) {
     Deferred fin;
     int rc = score_common(ctx, grid, d_ccdf, d_support, nullptr, nullptr, queues, b_expo_per_ms,
                           ORLOJ_PREFIX_TRIANGLE, d_cand_off, d_prob_off, d_finish_prob,
                           d_expected_finish, d_expected_latency_ms, d_score, nullptr, 0, &fin);
     if (rc) return rc;
     return select_common(ctx, grid, queues, ORLOJ_PREFIX_TRIANGLE, d_cand_off, d_score, d_sel_n,
-                         d_sel_bs, d_sel_score, &fin, d_expected_latency_ms);
+                         d_sel_bs, d_sel_score, &fin, d_expected_latency_ms, d_done, round, n_groups);
 }

@@ -42,11 +42,14 @@ static inline int orloj_ctx_fail(orloj_ctx* ctx, int code, const char* fmt, ...)
 // bit for bit.  In launches that take their E sums from emax_kernel, that
 // kernel's waves and the score waves share one launch, and the selection
 // forms E[L_B] and the scores from the panel sums before its argmax.
+// d_done (mapped host memory, or NULL): each select workgroup g writes
+// `round` to d_done[g] once its writes are visible to the host;
+// *n_groups receives the number of select workgroups.
 __attribute__((visibility("hidden"))) int orloj_internal_score_select(
     orloj_ctx* ctx, const orloj_grid* grid, const float* d_ccdf, const int32_t* d_support,
     const orloj_queues* queues, double b_expo_per_ms, const int64_t* d_cand_off,
     const int64_t* d_prob_off, float* d_finish_prob, double* d_expected_finish,
     float* d_expected_latency_ms, float* d_score, int32_t* d_sel_n, int32_t* d_sel_bs,
-    float* d_sel_score);
+    float* d_sel_score, int32_t* d_done, int32_t round, int* n_groups);
 
 #endif

@@ -75,6 +75,9 @@ struct orloj_sched {
     float* d_S = nullptr;
     int32_t* h_sel = nullptr;      // pinned, mapped [3M]: n, batch size, score bits
     int32_t* d_sel = nullptr;      // the device's address of h_sel
+    int32_t* h_done = nullptr;     // pinned, mapped: select workgroup g writes the round number
+    int32_t* d_done = nullptr;
+    int32_t round = 0;
     double device_s = 0.0;         // time spent in upload + launches + download
 
     int64_t* off() { return reinterpret_cast<int64_t*>(h_stage); }
@@ -92,6 +95,7 @@ void sched_free(orloj_sched* s) {
     if (s->ctx) (void)hipSetDevice(s->ctx->device);
     if (s->h_stage) (void)hipHostFree(s->h_stage);
     if (s->h_sel) (void)hipHostFree(s->h_sel);
+    if (s->h_done) (void)hipHostFree(s->h_done);
     for (void* p : {(void*)s->d_stage, (void*)s->d_P, (void*)s->d_E, (void*)s->d_EL,
                     (void*)s->d_S})
         if (p) (void)hipFree(p);
@@ -170,14 +174,33 @@ int decide(orloj_sched* s, double now, const uint8_t* idle, int32_t* sel_n, int3
         // scoring and selection: the outputs of orloj_score_candidates and
         // orloj_select_batch, with the E pre-pass and the score waves of a
         // small round in one launch
+        const int32_t round = ++s->round;
+        int groups = 0;
         rc = orloj_internal_score_select(ctx, &s->grid, s->d_ccdf, s->d_support, &dq, s->b, d_coff,
                                          d_poff, s->d_P, s->d_E, s->d_EL, s->d_S, s->d_sel,
-                                         s->d_sel + M, reinterpret_cast<float*>(s->d_sel + 2 * M));
+                                         s->d_sel + M, reinterpret_cast<float*>(s->d_sel + 2 * M),
+                                         s->d_done, round, &groups);
         if (rc) return drained(rc);
-        // the select kernel writes the selections straight into mapped
-        // host memory: no copy, the stream's completion makes them visible
-        e = hipStreamSynchronize(ctx->stream);
-        if (e != hipSuccess) return hip_err(ctx, e, "orloj_sched_decide: reading the selections");
+        // the select kernel writes the selections straight into mapped host
+        // memory and then, per workgroup, the round's number: the host spins
+        // on those (the stream's completion signal comes later); after 5 ms
+        // without them (a failed launch) it waits for the stream, which
+        // reports the error
+        bool seen = false;
+        {
+            const auto t1 = std::chrono::steady_clock::now();
+            for (;;) {
+                bool all = true;
+                for (int g = 0; g < groups && all; ++g)
+                    all = __atomic_load_n(&s->h_done[g], __ATOMIC_ACQUIRE) == round;
+                if (all) { seen = true; break; }
+                if (std::chrono::steady_clock::now() - t1 > std::chrono::milliseconds(5)) break;
+            }
+        }
+        if (!seen) {
+            e = hipStreamSynchronize(ctx->stream);
+            if (e != hipSuccess) return hip_err(ctx, e, "orloj_sched_decide: reading the selections");
+        }
         s->device_s += std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
         for (int q = 0; q < M; ++q) {
             sel_n[q] = s->h_sel[q];
@@ -271,6 +294,9 @@ int orloj_sched_create(orloj_sched** out, orloj_ctx* ctx, const orloj_grid* grid
     if (e == hipSuccess) e = hipHostMalloc((void**)&s->h_stage, s->stage_bytes, hipHostMallocDefault);
     if (e == hipSuccess) e = hipHostMalloc((void**)&s->h_sel, sizeof(int32_t) * 3 * M, hipHostMallocMapped);
     if (e == hipSuccess) e = hipHostGetDevicePointer((void**)&s->d_sel, s->h_sel, 0);
+    if (e == hipSuccess) e = hipHostMalloc((void**)&s->h_done, sizeof(int32_t) * (M + 1), hipHostMallocMapped);
+    if (e == hipSuccess) e = hipHostGetDevicePointer((void**)&s->d_done, s->h_done, 0);
+    if (e == hipSuccess) memset(s->h_done, 0, sizeof(int32_t) * (M + 1));
     if (e == hipSuccess) e = hipMalloc((void**)&s->d_stage, s->stage_bytes);
     if (e == hipSuccess) e = hipMalloc((void**)&s->d_P, sizeof(float) * n_p);
     if (e == hipSuccess) e = hipMalloc((void**)&s->d_E, sizeof(double) * n_c);
