@@ -1574,10 +1574,12 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
                     a.sel_score[m] = 0.0f;
                 }
             }
+            // the clears reach the host before this workgroup's flag (only
+            // the waves that wrote need the fence)
+            if (a.done && tid < a.M) __threadfence_system();
         }
         if ((int)blockIdx.x >= a.n_act) {
-            if (a.done) {                    // the clears above, then the flag
-                __threadfence_system();
+            if (a.done) {
                 __syncthreads();
                 if (tid == 0) __hip_atomic_store(&a.done[blockIdx.x], a.round, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
             }
@@ -1669,10 +1671,15 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
             }
         }
     }
-    if (a.done) {                            // every thread's writes, then the flag
-        __threadfence_system();
+    if (a.done) {
+        // the selection (lane 0 of wave 0, above) and any clears of
+        // workgroup 0 (fenced by their waves, ordered by this barrier) reach
+        // the host before the flag
         __syncthreads();
-        if (tid == 0) __hip_atomic_store(&a.done[blockIdx.x], a.round, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        if (tid == 0) {
+            __threadfence_system();
+            __hip_atomic_store(&a.done[blockIdx.x], a.round, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
     }
 }
 
