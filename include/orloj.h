@@ -383,9 +383,12 @@ int orloj_accumulate(orloj_ctx *ctx, const orloj_grid *grid, int64_t n_samples,
  * to orloj_sched_decide: for every idle model it drops the requests that can
  * no longer finish, stages the model's first s_max requests (s_max = the
  * largest batch size: no longer prefix is a candidate), uploads every idle
- * model's queue in one copy from pinned memory, runs orloj_score_candidates
- * and orloj_select_batch (TRIANGLE prefixes) in one launch each, reads the
- * selections back and removes the selected members from their queues.
+ * model's queue in one copy from pinned memory, scores and selects (the
+ * outputs of orloj_score_candidates and orloj_select_batch, TRIANGLE
+ * prefixes, bit for bit; in a round small enough to take its E sums from a
+ * pre-pass, that pre-pass shares the score launch and the selection kernel
+ * finishes E[L_B] and the scores), reads the selections back and removes
+ * the selected members from their queues.
  *
  * orloj_sched_create copies the grid (its d_bin_width_ms must stay valid)
  * and keeps d_ccdf / d_support (orloj_build_cdfs' table of the model's
@@ -407,9 +410,12 @@ int orloj_accumulate(orloj_ctx *ctx, const orloj_grid *grid, int64_t n_samples,
  * *h_n_dropped (optional) is incremented by the requests dropped; the
  * removed members in queue order, model by model, in h_batch_off[M+1],
  * h_batch_class[], h_batch_deadline[] (optional, room for M * s_max).  The
- * call returns after the selections are on the host (it synchronises the
- * context's stream); data errors of the scoring kernels are reported by
- * the next orloj_sync.
+ * call returns after the selections are on the host: the selection kernel
+ * flags each of its workgroups into pinned host memory once its writes are
+ * visible there, and the call spins on those flags (after 5 ms without them
+ * it synchronises the context's stream, which reports launch errors); work
+ * of the round may still be retiring on the stream when it returns.  Data
+ * errors of the scoring kernels are reported by the next orloj_sync.
  *
  * orloj_sched_queue_length: pending requests of a model (-1 if out of range).
  */
