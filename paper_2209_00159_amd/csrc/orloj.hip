@@ -620,6 +620,12 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
     const int n0 = kc * CH;
     if (n0 >= ncap) return;
     const int n1 = min(ncap, n0 + CH);
+    // The longest workgroups set a saturated launch's length (their steps
+    // run one after another while shorter ones share their SIMD): they
+    // take issue priority over the short ones, graded by their step count.
+    if (n1 - n0 >= 48) __builtin_amdgcn_s_setprio(3);
+    else if (n1 - n0 >= 32) __builtin_amdgcn_s_setprio(2);
+    else if (n1 - n0 >= 16) __builtin_amdgcn_s_setprio(1);
 
     // Affine mode (Eq. (3)): a batch of size s whose slowest member takes l
     // runs c0 + c1 s l, so its latency histogram is the base grid's with
