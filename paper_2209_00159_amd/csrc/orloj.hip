@@ -1532,8 +1532,8 @@ struct SelectArgs {
     float* sel_score;
     int nbs, rect;
     int M;
-    int n_act;                 // compact: workgroup g < n_act selects for act[g];
-    int compact;               //   workgroup 0 also clears the models with an empty queue
+    int n_act;                 // compact: workgroup g < n_act selects for act[g],
+    int compact;               //   workgroup n_act clears the models with an empty queue
     int bs[ORLOJ_MAX_BATCH_SIZES];
     int act[kMaxActive];
 };
@@ -1570,27 +1570,25 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
     __shared__ int64_t s_start[ORLOJ_MAX_BATCH_SIZES + 1];
     __shared__ Best s_best[kSelWaves];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    if (a.compact) {
-        if (blockIdx.x == 0) {
-            // no batch for the models with an empty queue (not listed)
-            for (int m = tid; m < a.M; m += kSelThreads) {
-                if (a.queue_off[m + 1] == a.queue_off[m]) {
-                    a.sel_n[m] = 0;
-                    a.sel_bs[m] = 0;
-                    a.sel_score[m] = 0.0f;
-                }
+    if (a.compact && (int)blockIdx.x >= a.n_act) {
+        // the workgroup after the selecting ones: no batch for the models
+        // with an empty queue (not listed).  Its clears, and their fence,
+        // run beside the selections.
+        for (int m = tid; m < a.M; m += kSelThreads) {
+            if (a.queue_off[m + 1] == a.queue_off[m]) {
+                a.sel_n[m] = 0;
+                a.sel_bs[m] = 0;
+                a.sel_score[m] = 0.0f;
             }
-            // the clears reach the host before this workgroup's flag (only
-            // the waves that wrote need the fence)
-            if (a.done && tid < a.M) __threadfence_system();
         }
-        if ((int)blockIdx.x >= a.n_act) {
-            if (a.done) {
-                __syncthreads();
-                if (tid == 0) __hip_atomic_store(&a.done[blockIdx.x], a.round, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-            }
-            return;
+        if (a.done) {
+            // the clears reach the host before the flag (every thread that
+            // cleared fences its own writes)
+            if (tid < a.M) __threadfence_system();
+            __syncthreads();
+            if (tid == 0) __hip_atomic_store(&a.done[blockIdx.x], a.round, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
         }
+        return;
     }
     const int q = a.compact ? a.act[blockIdx.x] : (int)blockIdx.x;
     __shared__ int64_t s_wsum[kSelWaves];
@@ -1678,10 +1676,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs a)
         }
     }
     if (a.done) {
-        // the selection (lane 0 of wave 0, above) and any clears of
-        // workgroup 0 (fenced by their waves, ordered by this barrier) reach
-        // the host before the flag
-        __syncthreads();
+        // the selection (written by thread 0, above) reaches the host before
+        // the flag
         if (tid == 0) {
             __threadfence_system();
             __hip_atomic_store(&a.done[blockIdx.x], a.round, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
@@ -3086,7 +3082,7 @@ int select_common(orloj_ctx* ctx, const orloj_grid* grid, const orloj_queues* qu
     memset(a.bs, 0, sizeof a.bs);
     for (int i = 0; i < grid->n_bs; ++i) a.bs[i] = grid->batch_sizes[i];
     // the models with a queue, when they are few enough to list: one
-    // workgroup each (workgroup 0 also clears the others)
+    // workgroup each, and one more that clears the others
     int n_act = 0;
     for (int q = 0; q < M; ++q)
         if (queues->h_queue_off[q + 1] > queues->h_queue_off[q]) {
@@ -3095,7 +3091,7 @@ int select_common(orloj_ctx* ctx, const orloj_grid* grid, const orloj_queues* qu
         }
     a.compact = n_act < M && n_act <= kMaxActive;
     a.n_act = n_act;
-    const unsigned g = a.compact ? (unsigned)std::max(n_act, 1) : (unsigned)M;
+    const unsigned g = a.compact ? (unsigned)(n_act + 1) : (unsigned)M;
     if (n_groups) *n_groups = (int)g;
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
