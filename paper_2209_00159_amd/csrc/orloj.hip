@@ -580,6 +580,9 @@ struct LaneCarry64 {
 #ifndef ORLOJ_EONLY_CACHE
 #define ORLOJ_EONLY_CACHE 3      // classes whose slices the E-only loop keeps in registers
 #endif
+#ifndef ORLOJ_EONLY_LDS_CACHE
+#define ORLOJ_EONLY_LDS_CACHE 3  // further classes whose slices it keeps in LDS
+#endif
 #ifndef ORLOJ_WARMUP_PREFETCH
 #define ORLOJ_WARMUP_PREFETCH 4  // steps ahead in a chunk's warm-up loop
 #endif
@@ -1175,12 +1178,25 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
             // values, same bits.  (Where a step is skipped because G is 0
             // over the panel, every later step of the pass is skipped too,
             // so a copy taken then is never read.)
+            // The next RL classes keep theirs in LDS, in the space of the
+            // member panels' snapshot, prefixes and plans (unused from here
+            // on), as far as this launch's LDS holds them: the first member
+            // writes its slice there, and later members read it back into
+            // their ring slot (loaded with the constant row) at their step.
+            // The LDS read is issued at the step rather than with the ring's
+            // loads: a ring filled from two kinds of loads would make every
+            // step wait for all of the ring's memory loads.
             constexpr int RC = CR == 1 ? ORLOJ_EONLY_CACHE : 0;
+            constexpr int RL = CR == 1 && CPL % 4 == 0 ? ORLOJ_EONLY_LDS_CACHE : 0;
+            constexpr int NC = RC + RL;
             constexpr int RCA = RC > 0 ? RC : 1;
-            // step code of member `lane`: RC (not cached), k < RC (a later
-            // member of cached class k), RC + 1 + k (its first member)
-            int rk_r = RC;
-            if constexpr (RC > 0) {
+            constexpr int SLOT = 4 * PW;                        // bytes of one slice
+            const int rl = min(RL, (int)((score_fixed_bytes<CPL>() + (size_t)maxcap * score_bytes_per_member()) / SLOT));
+            // step code of member `lane`: NC (read from memory), k < NC (a
+            // later member of cached class k: registers below RC, LDS from
+            // RC), NC + 1 + k (the first member of class k)
+            int rk_r = NC;
+            if constexpr (NC > 0) {
                 const int cl = lane < n1 ? __builtin_bit_cast(int, cls_r.v[0]) : -1 - lane;
                 int cnt = 0, first = 64;        // members with this lane's class, the first of them
                 for (int m = n1 - 1; m >= 0; --m) {
@@ -1190,21 +1206,32 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
                 }
                 bool taken = lane >= n1;
 #pragma unroll
-                for (int k = 0; k < RC; ++k) {
+                for (int k = 0; k < NC; ++k) {
                     // most members first, ties to the earlier member; a
                     // class with a single member gains nothing
-                    const int key = (taken || cnt < 2) ? -1 : (cnt << 6) | (63 - lane);
+                    const int key = (taken || cnt < 2 || k >= RC + rl) ? -1 : (cnt << 6) | (63 - lane);
                     const int best = wave_max_i32(key);
                     if (best >= 0) {
                         const int ck = __builtin_amdgcn_readlane(cl, 63 - (best & 63));
-                        if (cl == ck) rk_r = first == lane ? RC + 1 + k : k;
+                        if (cl == ck)
+                            rk_r = first == lane ? NC + 1 + k : k;
                         taken = taken || cl == ck;
                     }
                 }
             }
             auto code = [&](int n) -> int {
-                if constexpr (RC > 0) return __builtin_amdgcn_readlane(rk_r, n);
-                return RC;
+                if constexpr (NC > 0) return __builtin_amdgcn_readlane(rk_r, n);
+                return NC;
+            };
+            // slice k of the LDS classes: float4 j of lane l at 1024 j + 16 l
+            // (each access a run of 64 consecutive 16-byte words)
+            auto lds_slice = [&](int k, int j) {
+                return reinterpret_cast<float4*>(smem_raw + (size_t)k * SLOT + 1024 * j + 16 * lane);
+            };
+            // the ring's load for step n: the constant row for a later member
+            // of a cached class (and where `none`), else memory
+            auto load_e = [&](float (&v)[CPL], int n, int c0, bool none, int& lo, int& hi) {
+                load_step(v, n, c0, none || code(n) < NC, lo, hi);
             };
             float creg[RCA][CPL];
 #pragma unroll
@@ -1218,7 +1245,7 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
             int qf_p = LASTP + 1, qf_n = 0;
 #pragma unroll
             for (int i = 0; i < PFB; ++i) {
-                load_step(bufb[i], qf_n, qf_p * PW + base, code(qf_n) < RC, blo[i], bhi[i]);
+                load_e(bufb[i], qf_n, qf_p * PW + base, false, blo[i], bhi[i]);
                 __builtin_amdgcn_sched_barrier(0);
                 if (++qf_n == n1) { qf_n = 0; qf_p = min(qf_p + 1, NP - 1); }
             }
@@ -1260,10 +1287,19 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
                     // a cached class's first member: keep its slice
 #pragma unroll
                     for (int k = 0; k < RC; ++k) {
-                        if (kc == RC + 1 + k) {
+                        if (kc == NC + 1 + k) {
                             asm volatile("" ::: "memory");
 #pragma unroll
                             for (int j = 0; j < CPL; ++j) creg[k][j] = bufb[i][j];
+                        }
+                    }
+                    if constexpr (RL > 0) {
+                        if (kc >= NC + 1 + RC) {
+                            asm volatile("" ::: "memory");
+#pragma unroll
+                            for (int j = 0; j < CPL / 4; ++j)
+                                *lds_slice(kc - NC - 1 - RC, j) =
+                                    make_float4(bufb[i][4 * j], bufb[i][4 * j + 1], bufb[i][4 * j + 2], bufb[i][4 * j + 3]);
                         }
                     }
                     if (!skip) {
@@ -1278,13 +1314,23 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
                                 done = true;
                             }
                         }
+                        if constexpr (RL > 0) {
+                            if (!done && kc >= RC && kc < NC) {
+                                asm volatile("" ::: "memory");
+#pragma unroll
+                                for (int j = 0; j < CPL / 4; ++j) {
+                                    const float4 t = *lds_slice(kc - RC, j);
+                                    bufb[i][4 * j] = t.x; bufb[i][4 * j + 1] = t.y;
+                                    bufb[i][4 * j + 2] = t.z; bufb[i][4 * j + 3] = t.w;
+                                }
+                            }
+                        }
                         if (!done) update(bufb[i]);
                     }
 #pragma unroll
                     for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(Gacc[j])::"memory");
                     const bool zero_after = zero_b || min(p0 + PW, K) <= lo_n;
-                    load_step(bufb[i], qf_n, qf_p * PW + base,
-                              (zero_after && qf_p == pb) || code(qf_n) < RC, blo[i], bhi[i]);
+                    load_e(bufb[i], qf_n, qf_p * PW + base, zero_after && qf_p == pb, blo[i], bhi[i]);
                     if (++qf_n == n1) { qf_n = 0; qf_p = min(qf_p + 1, NP - 1); }
                     if (pb < NP && real) {
                         float etot = eprev;
