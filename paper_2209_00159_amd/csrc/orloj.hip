@@ -578,7 +578,7 @@ struct LaneCarry64 {
 #define ORLOJ_EONLY_PREFETCH 3   // iterations ahead in the E-only panels' loop
 #endif
 #ifndef ORLOJ_EONLY_CACHE
-#define ORLOJ_EONLY_CACHE 3      // classes whose slices the E-only loop keeps in registers
+#define ORLOJ_EONLY_CACHE 2      // classes whose slices the E-only loop keeps in registers
 #endif
 #ifndef ORLOJ_EONLY_LDS_CACHE
 #define ORLOJ_EONLY_LDS_CACHE 3  // further classes whose slices it keeps in LDS
