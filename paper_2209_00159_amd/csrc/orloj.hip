@@ -487,6 +487,9 @@ __device__ __forceinline__ void wave_lds_fence() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
 }
 
+template <bool B>
+struct BoolTag { static constexpr bool value = B; };
+
 // Per-step state carried from one panel pass to the next, spread over the
 // lanes: step n lives in lane n % 64 of register n / 64.  Reads and writes
 // take a wave-uniform step index.
@@ -738,645 +741,665 @@ __device__ __forceinline__ void score_wave(const ScoreArgs& a, const unsigned bi
         mb.oz = (uint16_t)oz; mb.oa = (uint16_t)oa;
         return mb;
     };
-    // The prologue is a chain of memory round trips, which the launches too
-    // small to fill the chip wait on: the loads that do not depend on each
-    // other are issued together.  This batch size's block of candidates and
-    // member slots starts after those of the batch sizes before it (one per
-    // lane, summed across the wave).
-    int64_t cand = a.cand_off[q], prob = a.prob_off[q];
-    {
-        uint64_t dc = 0, dp = 0;
-        for (int j0 = 0; j0 < bi; j0 += 64) {
-            const int j = j0 + lane;
-            if (j < bi) {
-                const int64_t c = a.rect ? N : (N < a.bs[j] ? N : (int64_t)a.bs[j]);
-                dc += (uint64_t)c;
-                dp += (uint64_t)(c * (c + 1) / 2);
-            }
-        }
-        cand += (int64_t)wave_sum_u64(dc, lane);
-        prob += (int64_t)wave_sum_u64(dp, lane);
-    }
-    // rows of this (model, batch size); affine mode has one set per model
-    const size_t qb = AFF ? (size_t)q : (size_t)q * (size_t)a.nbs + (size_t)bi;
-    const float* tab_qb = a.tab + qb * (size_t)a.C * (size_t)K;
-
-    // class and support of member n in lane n % 64 of register n / 64, and
-    // the members' plans, in one pass
-    LaneCarry<CR> cls_r, lo_r, hi_r;
-    const int32_t* sup_qb = a.sup ? a.sup + qb * (size_t)a.C * 2 : nullptr;
-#pragma unroll
-    for (int r = 0; r < CR; ++r) {
-        const int m = r * 64 + lane;
-        int c = a.cls[q0 + min(m, n1 - 1)];
-        if (c < 0 || c >= a.C) c = 0;                     // flagged by its plan
-        cls_r.v[r] = __builtin_bit_cast(float, c);
-        lo_r.v[r] = __builtin_bit_cast(float, sup_qb ? sup_qb[2 * c] : 0);
-        hi_r.v[r] = __builtin_bit_cast(float, sup_qb ? sup_qb[2 * c + 1] : K);
-        if (m < n1) s_mem[m] = make_plan(m, true);
-    }
-    if (lane == 0) {
-        s_kd[0] = 0.0;
-        s_kd[1] = 1.0;
-        s_kd[2] = 0.0;
-        s_kd[3] = 0.0;
-    }
-    if (lane < 4) s_fz[lane] = 0.0f;
-    wave_lds_fence();
-    // first member of each panel p <= NP in lane p (home panels are
-    // non-decreasing in m); lanes past NP hold n1
-    int mlo_r = n1;
-    for (int p = 0; p <= NP; ++p) {
-        int cnt = 0;
-        for (int m0 = 0; m0 < n1; m0 += 64) {
-            const int m = m0 + lane;
-            const bool below = m < n1 && s_mem[m].hp < p;
-            cnt += __builtin_popcountll(__ballot(below));
-        }
-        mlo_r = lane == p ? cnt : mlo_r;
-    }
-
-    // ---- scan constants
-    float rp[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) rp[i] = exp2_hw(log2d * (float)(CPL << i));
-    const float w15 = exp2_hw(log2d * (float)(CPL * ((lane & 15) + 1)));
-    const float w31 = exp2_hw(log2d * (float)(CPL * (lane >= 32 ? lane - 31 : 0)));
-    const float dQ = exp2_hw(log2d * (float)Q::QW);
-    const float dq1 = exp2f(log2d);                   // d in fp32
-    // A member's in-quarter discounted prefix up to bin k-2, the quarter's
-    // r-th bin being bin k-2 (rq = r <= 3): sum over j <= rq of
-    // d^(rq - j) G_j, formed as a dot product with these weights (all 0
-    // when the member needs no quarter term, rq = kNoQuarter).
-    const float dq2 = dq1 * dq1, dq3 = dq2 * dq1;
-    auto quarter_weights = [&](int rq, float (&wv)[4]) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int e = rq - r;
-            wv[r] = (e < 0 || rq > 3) ? 0.0f : e == 0 ? 1.0f : e == 1 ? dq1 : e == 2 ? dq2 : dq3;
-        }
-    };
-    const float dPW = exp2_hw(log2d * (float)PW);
-
-    // Home panel of the last member (the latest deadline): past it no member
-    // needs G or the discounted prefix, only E[L_B] needs the sums of 1 - G.
-    // The main loop walks the panels up to LASTP; the tabulated mode then
-    // sums the rest (E-only panels) in a loop of its own, the affine mode
-    // takes them from emax_kernel.
-    const int LASTP = __builtin_amdgcn_readfirstlane((int)s_mem[n1 - 1].hp);
-    const int NPW = LASTP + 1;
-    // Load the lane chunk starting at bin c0 of member n's row; chunks wholly
-    // outside the row's support, and every chunk when `none` (the row's
-    // values cannot change G), read a constant row instead.
-    // The member's support bounds go to lo / hi: the ring slot keeps them
-    // for the step that uses the row.
-    auto load_step = [&](float (&v)[CPL], int n, int c0, bool none, int& lo, int& hi) {
-        const int c = __builtin_bit_cast(int, cls_r.get(n));
-        lo = __builtin_bit_cast(int, lo_r.get(n));
-        hi = __builtin_bit_cast(int, hi_r.get(n));
-        // The affine mode's solo table (M x C rows) stays in the Infinity
-        // Cache, so it reads every chunk rather than spend a per-lane test
-        // and select on each load; entries outside the support are exactly
-        // 1 and 0 either way.
-        const bool ones = !AFF && !none && c0 + CPL <= lo, zeros = none || (!AFF && c0 >= hi);
-        const float* src = tab_qb + (size_t)c * (size_t)K + c0;
-        int lim = K - 1 - c0;
-        if (ones || zeros) {
-            src = a.fill + (ones ? 16 : 0);
-            lim = CPL - 1;
-        }
-        load_chunk<CPL, EXACT>(v, src, lim);
-    };
-
-    LaneCarry<CR> cW, cN;
-    LaneCarry64<CR> cE, cP, cGl;
-    cW.zero(); cGl.zero(); cN.zero(); cE.zero(); cP.zero();
-
-    // One flat loop over (panel p, step n in [ns, n1)), n fastest, padded at
-    // the end to a multiple of PF with ghost iterations (p == NP) so that
-    // ring slot i always holds iteration it0 + i.  The row of iteration
-    // it + PF is loaded PF iterations ahead; (p, n) and the prefetch
-    // position advance by counting.  A chunk of a split launch rebuilds G
-    // over the steps before n0 (warm-up): in a loop of its own at each pass
-    // start when its E sums come from emax_kernel (WARM_LOOP: the loop's
-    // deeper ring costs registers, which the launches that fill the chip
-    // cannot spare), else as iterations of this loop that update G only.
-    constexpr bool WARM_LOOP = ESPLIT && !AFF;
-    const int ns = WARM_LOOP ? n0 : 0;
-    const int total = NPW * (n1 - ns);
-    const int iters = (total + PF - 1) / PF * PF;
-    const int base = lane * CPL;
-
-    double Gacc[CPL];
-    float buf[PF][CPL];
-    int slo[PF], shi[PF];                                 // the slots' support bounds
-    int pf_p = 0, pf_n = ns;                              // prefetch position
-#pragma unroll
-    for (int i = 0; i < PF; ++i) {
-        load_step(buf[i], pf_n, pf_p * PW + base, false, slo[i], shi[i]);
-        // keep the priming loads in ring order, as the loop issues them
-        __builtin_amdgcn_sched_barrier(0);
-        if (++pf_n == n1) { pf_n = ns; pf_p = min(pf_p + 1, NPW - 1); }
-    }
-    int p = 0, n = ns;
-    int mlo = __builtin_amdgcn_readlane(mlo_r, 0);
-    int mend = __builtin_amdgcn_readlane(mlo_r, 1);
-    // Trivial steps.  Where a panel lies wholly past the last bin with mass
-    // of member n's row (every 1 - F there is exactly 0), or where G is
-    // already exactly 0 over the whole panel (an earlier member's row had
-    // no mass up to its end), step n leaves G unchanged bit for bit; if no
-    // member of the panel needs scoring at that step, its panel sums are
-    // those of step n-1 and the update, its loads and its reductions are
-    // skipped.
-    bool pass_zero = false;                  // G == 0 on every bin of this pass's panel
-    Member pass_mb;                          // CR == 1: this lane's member of the pass
-    double pass_th = 0.0;                    //   and its position in bin k, fp64,
-    float pass_wq[4] = {0.0f, 0.0f, 0.0f, 0.0f};   // and its quarter weights
-    bool pass_valid = false;
-    float etot_prev = 0.0f, T_prev = 0.0f;
-    double gl_prev = 0.0;
-
-    // Warm-up: G over steps 0 .. n0-1 of panel pp (the product only, the
-    // same fma per bin and step as a scored step, so the same bits; a step
-    // whose row cannot change G multiplies by an exact 0 or finds G = 0),
-    // with rows loaded PFW steps ahead: these steps are short and would
-    // otherwise wait on their loads.  Leaves pass_zero for the steps after.
-    constexpr int PFW = ORLOJ_WARMUP_PREFETCH;
-    auto warm_up = [&](int pp) {
-        const int p0w = pp * PW, pbw = p0w + base;
-        float wb[PFW][CPL];
-        int wlo[PFW], whi[PFW];
-        bool zero = false;                   // G == 0 over the panel
-#pragma unroll
-        for (int i = 0; i < PFW; ++i) {
-            load_step(wb[i], min(i, n0 - 1), pbw, false, wlo[i], whi[i]);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        for (int w0 = 0; w0 < n0; w0 += PFW) {
-#pragma unroll
-            for (int i = 0; i < PFW; ++i) {
-                const int nw = w0 + i;
-                if (nw < n0) {
-#pragma unroll
-                    for (int j = 0; j < CPL; ++j) {
-                        const float t = (EXACT || pbw + j < K) ? wb[i][j] : 0.0f;
-                        Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
-                    }
-                    zero = zero || min(p0w + PW, K) <= wlo[i];
+    // Everything from here on is compiled twice: for the waves whose members
+    // all lie in panel 0 (ONE: no carries between panel passes, every step
+    // scores members; at configuration 5 that is every wave) and for the
+    // rest.  The branch comes before any per-lane state, so the two versions
+    // share no registers' worth of live values.  The last member's plan
+    // gives its home panel, as it does below.
+    const int lastp = __builtin_amdgcn_readfirstlane((int)make_plan(n1 - 1, false).hp);
+    auto rest = [&](auto one_tag) {
+        constexpr bool ONE = decltype(one_tag)::value;
+        // The prologue is a chain of memory round trips, which the launches too
+        // small to fill the chip wait on: the loads that do not depend on each
+        // other are issued together.  This batch size's block of candidates and
+        // member slots starts after those of the batch sizes before it (one per
+        // lane, summed across the wave).
+        int64_t cand = a.cand_off[q], prob = a.prob_off[q];
+        {
+            uint64_t dc = 0, dp = 0;
+            for (int j0 = 0; j0 < bi; j0 += 64) {
+                const int j = j0 + lane;
+                if (j < bi) {
+                    const int64_t c = a.rect ? N : (N < a.bs[j] ? N : (int64_t)a.bs[j]);
+                    dc += (uint64_t)c;
+                    dp += (uint64_t)(c * (c + 1) / 2);
                 }
-#pragma unroll
-                for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(Gacc[j])::"memory");
-                load_step(wb[i], min(nw + PFW, n0 - 1), pbw, zero, wlo[i], whi[i]);
             }
+            cand += (int64_t)wave_sum_u64(dc, lane);
+            prob += (int64_t)wave_sum_u64(dp, lane);
         }
-        pass_zero = zero;
-    };
+        // rows of this (model, batch size); affine mode has one set per model
+        const size_t qb = AFF ? (size_t)q : (size_t)q * (size_t)a.nbs + (size_t)bi;
+        const float* tab_qb = a.tab + qb * (size_t)a.C * (size_t)K;
 
-    static_assert(PF % 2 == 0, "steps are reduced in pairs");
-    for (int it0 = 0; it0 < iters; it0 += PF) {
-        // each scoring step's member sums (0 in lanes without a member) and
-        // its index (-1: no member scored)
-        double redP[PF];
-        float redN[PF];
-        int red_n[PF];
+        // class and support of member n in lane n % 64 of register n / 64, and
+        // the members' plans, in one pass
+        LaneCarry<CR> cls_r, lo_r, hi_r;
+        const int32_t* sup_qb = a.sup ? a.sup + qb * (size_t)a.C * 2 : nullptr;
 #pragma unroll
-        for (int i = 0; i < PF; ++i) redP[i] = 0.0, redN[i] = 0.0f, red_n[i] = -1;
+        for (int r = 0; r < CR; ++r) {
+            const int m = r * 64 + lane;
+            int c = a.cls[q0 + min(m, n1 - 1)];
+            if (c < 0 || c >= a.C) c = 0;                     // flagged by its plan
+            cls_r.v[r] = __builtin_bit_cast(float, c);
+            lo_r.v[r] = __builtin_bit_cast(float, sup_qb ? sup_qb[2 * c] : 0);
+            hi_r.v[r] = __builtin_bit_cast(float, sup_qb ? sup_qb[2 * c + 1] : K);
+            if (m < n1) s_mem[m] = make_plan(m, true);
+        }
+        if (lane == 0) {
+            s_kd[0] = 0.0;
+            s_kd[1] = 1.0;
+            s_kd[2] = 0.0;
+            s_kd[3] = 0.0;
+        }
+        if (lane < 4) s_fz[lane] = 0.0f;
+        wave_lds_fence();
+        // Home panel of the last member (the latest deadline): past it no member
+        // needs G or the discounted prefix, only E[L_B] needs the sums of 1 - G.
+        // The main loop walks the panels up to LASTP; the tabulated mode then
+        // sums the rest (E-only panels) in a loop of its own, the affine mode
+        // takes them from emax_kernel.
+        const int LASTP = ONE ? 0 : __builtin_amdgcn_readfirstlane((int)s_mem[n1 - 1].hp);
+        const int NPW = LASTP + 1;
+        // first member of each panel p in lane p (home panels are non-decreasing
+        // in m): counted up to LASTP; every member's home panel lies before the
+        // later ones, so their lanes hold n1
+        int mlo_r = n1;
+        for (int p = 0; p <= LASTP; ++p) {
+            int cnt = 0;
+            for (int m0 = 0; m0 < n1; m0 += 64) {
+                const int m = m0 + lane;
+                const bool below = m < n1 && s_mem[m].hp < p;
+                cnt += __builtin_popcountll(__ballot(below));
+            }
+            mlo_r = lane == p ? cnt : mlo_r;
+        }
+
+        // ---- scan constants
+        float rp[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) rp[i] = exp2_hw(log2d * (float)(CPL << i));
+        const float w15 = exp2_hw(log2d * (float)(CPL * ((lane & 15) + 1)));
+        const float w31 = exp2_hw(log2d * (float)(CPL * (lane >= 32 ? lane - 31 : 0)));
+        const float dQ = exp2_hw(log2d * (float)Q::QW);
+        const float dq1 = exp2f(log2d);                   // d in fp32
+        // A member's in-quarter discounted prefix up to bin k-2, the quarter's
+        // r-th bin being bin k-2 (rq = r <= 3): sum over j <= rq of
+        // d^(rq - j) G_j, formed as a dot product with these weights (all 0
+        // when the member needs no quarter term, rq = kNoQuarter).
+        const float dq2 = dq1 * dq1, dq3 = dq2 * dq1;
+        auto quarter_weights = [&](int rq, float (&wv)[4]) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int e = rq - r;
+                wv[r] = (e < 0 || rq > 3) ? 0.0f : e == 0 ? 1.0f : e == 1 ? dq1 : e == 2 ? dq2 : dq3;
+            }
+        };
+        const float dPW = exp2_hw(log2d * (float)PW);
+
+        // Load the lane chunk starting at bin c0 of member n's row; chunks wholly
+        // outside the row's support, and every chunk when `none` (the row's
+        // values cannot change G), read a constant row instead.
+        // The member's support bounds go to lo / hi: the ring slot keeps them
+        // for the step that uses the row.
+        auto load_step = [&](float (&v)[CPL], int n, int c0, bool none, int& lo, int& hi) {
+            const int c = __builtin_bit_cast(int, cls_r.get(n));
+            lo = __builtin_bit_cast(int, lo_r.get(n));
+            hi = __builtin_bit_cast(int, hi_r.get(n));
+            // The affine mode's solo table (M x C rows) stays in the Infinity
+            // Cache, so it reads every chunk rather than spend a per-lane test
+            // and select on each load; entries outside the support are exactly
+            // 1 and 0 either way.
+            const bool ones = !AFF && !none && c0 + CPL <= lo, zeros = none || (!AFF && c0 >= hi);
+            const float* src = tab_qb + (size_t)c * (size_t)K + c0;
+            int lim = K - 1 - c0;
+            if (ones || zeros) {
+                src = a.fill + (ones ? 16 : 0);
+                lim = CPL - 1;
+            }
+            load_chunk<CPL, EXACT>(v, src, lim);
+        };
+
+        LaneCarry<CR> cW, cN;
+        LaneCarry64<CR> cE, cP, cGl;
+        cW.zero(); cGl.zero(); cN.zero(); cE.zero(); cP.zero();
+
+        // One flat loop over (panel p, step n in [ns, n1)), n fastest, padded at
+        // the end to a multiple of PF with ghost iterations (p == NP) so that
+        // ring slot i always holds iteration it0 + i.  The row of iteration
+        // it + PF is loaded PF iterations ahead; (p, n) and the prefetch
+        // position advance by counting.  A chunk of a split launch rebuilds G
+        // over the steps before n0 (warm-up): in a loop of its own at each pass
+        // start when its E sums come from emax_kernel (WARM_LOOP: the loop's
+        // deeper ring costs registers, which the launches that fill the chip
+        // cannot spare), else as iterations of this loop that update G only.
+        constexpr bool WARM_LOOP = ESPLIT && !AFF;
+        const int ns = WARM_LOOP ? n0 : 0;
+        const int total = NPW * (n1 - ns);
+        const int iters = (total + PF - 1) / PF * PF;
+        const int base = lane * CPL;
+
+        double Gacc[CPL];
+        float buf[PF][CPL];
+        int slo[PF], shi[PF];                                 // the slots' support bounds
+        int pf_p = 0, pf_n = ns;                              // prefetch position
 #pragma unroll
         for (int i = 0; i < PF; ++i) {
-            if (n == ns) {
-                // a real branch (the asm keeps it from becoming selects)
-                asm volatile("" ::: "memory");
-#pragma unroll
-                for (int j = 0; j < CPL; ++j) Gacc[j] = 1.0;
-                pass_zero = false;
-                if constexpr (WARM_LOOP) {
-                    if (n0 > 0 && p < NPW) warm_up(p);
-                }
-                if constexpr (CR == 1) {
-                    // at most 64 members: lane l scores member mlo + l of this
-                    // pass at every step, so its plan is read from LDS once
-                    pass_valid = mlo + lane < mend;
-                    pass_mb = s_mem[min(mlo + lane, n1 - 1)];
-                    pass_th = (double)pass_mb.theta + (double)pass_mb.thlo;
-                    quarter_weights(pass_mb.rq, pass_wq);
-                }
-            }
-            const int p0 = p * PW;                        // first bin of the panel
-            const int pbase = p0 + base;                  // first bin of this lane chunk
-            const int hi_n = shi[i];
-            const int lo_n = slo[i];
-            const int mhi = min(mend, n + 1);             // members of this panel among the first n+1
-            const bool real = n >= n0;                    // else a warm-up step
-            const bool due = real && mlo < mhi;           // some member is scored at this step
-            // G unchanged by this step (a panel past the row's support, or G
-            // already 0 on it): a warm-up step then does nothing, a scored
-            // step after the chunk's first reuses the previous step's sums
-            const bool unchanged = pass_zero || p0 >= hi_n;
-            const bool skip = p >= NPW || (real ? (n > n0 && unchanged && !due) : unchanged);
-            // G <- G * F = G - G (1 - F), in fp64; per-quarter sums
-            double gs[Q::QW];
-            float zqv[Q::NQ];
-            if (!skip) {
-#pragma unroll
-                for (int qq = 0; qq < Q::NQ; ++qq) {
-                    double zz = 0.0;
-#pragma unroll
-                    for (int r = 0; r < Q::QW; ++r) {
-                        const int j = qq * Q::QW + r;
-                        const float t = (EXACT || pbase + j < K) ? buf[i][j] : 0.0f;
-                        Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
-                        if constexpr (!ESPLIT) gs[r] = qq == 0 ? Gacc[j] : gs[r] + Gacc[j];
-                        zz = r == 0 ? Gacc[j] : fma(zz, d64, Gacc[j]);
-                    }
-                    zqv[qq] = (float)zz;
-                }
-            }
-            // the slot is refilled only after the update has consumed it, so
-            // the ring keeps its registers (no copies, no wait on the loads
-            // just issued)
-#pragma unroll
-            for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(Gacc[j])::"memory");
-            // G == 0 over the pass from here on: later steps of it need no row
-            const bool zero_after = pass_zero || min(p0 + PW, K) <= lo_n;
-            load_step(buf[i], pf_n, pf_p * PW + base, zero_after && pf_p == p, slo[i], shi[i]);
+            load_step(buf[i], pf_n, pf_p * PW + base, false, slo[i], shi[i]);
+            // keep the priming loads in ring order, as the loop issues them
+            __builtin_amdgcn_sched_barrier(0);
             if (++pf_n == n1) { pf_n = ns; pf_p = min(pf_p + 1, NPW - 1); }
-            if (p < NPW && real) {                        // else a ghost or warm-up iteration
-                float etot = etot_prev, T = T_prev;
-                double glast_here = gl_prev;
-                // carries in from the previous panel pass (zero in the first)
-                float Win = 0.0f;
-                double glin64 = 0.0;
-                if (p > 0) {
-                    Win = cW.get(n);
-                    glin64 = cGl.get(n);
-                }
-                const float glin = (float)glin64;
-                float A = 0.0f;
-                if (!skip) {
-                    // quarter ends of the in-chunk discounted prefix, and its total
-                    float zc = zqv[0];
-#pragma unroll
-                    for (int qq = 1; qq < Q::NQ; ++qq) {
-                        zc = fmaf(zc, dQ, zqv[qq]);
-                        zqv[qq] = zc;
-                    }
-                    A = wave_wscan(zc, rp, w15, w31);
-                    if (p < LASTP) {                      // carried into the next pass
-                        T = lane63(A);                    // discounted prefix at the panel end
-                        T_prev = T;
-                    }
-                }
-                if (!skip) {
-                    if constexpr (!ESPLIT) {
-                        double gsum = gs[0];
-#pragma unroll
-                        for (int r = 1; r < Q::QW; ++r) gsum += gs[r];
-                        // 1 - G summed over the lane's bins (padding bins hold G = 1)
-                        const float e = (float)((double)CPL - gsum);
-                        etot = lane63(wave_scan_sum(e));
-                    }
-                    if (p < LASTP) {                      // carried into the next pass
-                        glast_here = lane63(Gacc[CPL - 1]);
-                        gl_prev = glast_here;
-                    }
-                    etot_prev = etot;
-
-                    if (due) {
-                        // snapshot of G over the panel, fp64, pairs of bins
-                        // interleaved over the lanes (16-byte writes)
-                        if constexpr (CPL >= 2) {
-#pragma unroll
-                            for (int j = 0; j < CPL; j += 2) {
-                                const int pair = (j >> 1) * 64 + (lane ^ (j >> 1));
-                                *reinterpret_cast<double2*>(smem_raw + L::GD + 16 * pair) =
-                                    make_double2(Gacc[j], Gacc[j + 1]);
-                            }
-                        } else {
-                            *reinterpret_cast<double*>(smem_raw + L::GD + 8 * lane) = Gacc[0];
-                        }
-#pragma unroll
-                        for (int qq = 0; qq < Q::NQ; ++qq) s_zq[lane * Q::NQ + qq] = zqv[qq];
-                        s_A[lane] = A;
-                        if (lane == 0) s_kd[2] = glin64;
-                        wave_lds_fence();
-                        double pP = 0.0;
-                        float pN = 0.0f;
-                        const int nn = n + 1;
-                        auto score_member = [&](const Member& mb, int m, double th, const float (&wq4)[4]) {
-                            const unsigned char* f = smem_raw;
-                            auto atf = [&](int off) { return *reinterpret_cast<const float*>(f + off); };
-                            auto atd = [&](int off) { return *reinterpret_cast<const double*>(f + off); };
-                            const double gk64 = atd(mb.o0);
-                            const double gk164 = atd(mb.o1);
-                            const float al0 = atf(mb.oa);
-                            const float zq0 = atf(mb.oz);
-                            // the quarter's G values (fp32 terms of the priority)
-                            float g4[4];
-                            if constexpr (Q::QW == 4) {
-                                const double2 t0 = *reinterpret_cast<const double2*>(f + mb.o4);
-                                // the quarter's second pair: its slot follows
-                                // the first's by 64, with the lane index's
-                                // low bit flipped (the first pair's index is even)
-                                const double2 t1 = *reinterpret_cast<const double2*>(f + ((mb.o4 + 16 * 64) ^ 16));
-                                g4[0] = (float)t0.x; g4[1] = (float)t0.y;
-                                g4[2] = (float)t1.x; g4[3] = (float)t1.y;
-                            } else if constexpr (Q::QW == 2) {
-                                const double2 t0 = *reinterpret_cast<const double2*>(f + mb.o4);
-                                g4[0] = (float)t0.x; g4[1] = (float)t0.y;
-                                g4[2] = g4[3] = 0.0f;
-                            } else {
-                                g4[0] = (float)atd(mb.o4);
-                                g4[1] = g4[2] = g4[3] = 0.0f;
-                            }
-                            // discounted prefix of the quarter up to bin k-2
-                            // (weights 0 when the member needs no quarter term)
-                            const float z4 = fmaf(wq4[0], g4[0], fmaf(wq4[1], g4[1], fmaf(wq4[2], g4[2], wq4[3] * g4[3])));
-                            const float zin = fmaf(mb.fq, zq0, z4);
-                            const float Zv = fmaf(mb.cW, Win, fmaf(mb.cG, glin, fmaf(mb.cA, al0, zin)));
-                            const float gk = (float)gk64, gk1 = (float)gk164;
-                            const float h = gk1 - gk;
-                            // P in fp64: the expected finish count sums it
-                            const double P64 = fma(th, gk164 - gk64, gk64);
-                            const float num = mb.cost * fmaf(mb.cg, fmaf(-omd, Zv, gk), h * mb.psi);
-                            a.P[prob + (int64_t)n * nn / 2 + m] = (float)P64;
-                            // (one member per lane and pass when CR == 1:
-                            // its values, not a sum with 0)
-                            pP = CR == 1 ? P64 : pP + P64;
-                            pN = CR == 1 ? num : pN + num;
-                        };
-                        if constexpr (CR == 1) {
-                            // the lane's member of this pass, already in registers
-                            if (pass_valid && mlo + lane < mhi) score_member(pass_mb, mlo + lane, pass_th, pass_wq);
-                        } else {
-                            for (int m = mlo + lane; m < mhi; m += 64) {
-                                const Member mb = s_mem[m];
-                                float wq4[4];
-                                quarter_weights(mb.rq, wq4);
-                                score_member(mb, m, (double)mb.theta + (double)mb.thlo, wq4);
-                            }
-                        }
-                        // reduced across the lanes with the other step of
-                        // its pair, after the pair
-                        redP[i] = pP;
-                        redN[i] = pN;
-                        red_n[i] = n;
-                        wave_lds_fence();
-                    }
-                }
-                // carries out to the next panel pass, per-step sums
-                if (p < LASTP) {
-                    cW.set(n, fmaf(Win, dPW, T));
-                    cGl.set(n, glast_here);
-                }
-                if constexpr (!ESPLIT) cE.add(n, (double)etot);
-            }
-            pass_zero = zero_after;
-            if (++n == n1) {
-                n = ns;
-                ++p;
-                mlo = __builtin_amdgcn_readlane(mlo_r, min(p, NP));
-                mend = __builtin_amdgcn_readlane(mlo_r, min(p + 1, NP));
-            }
         }
-        // Sum P (fp64) and the priority terms (fp32) over the lanes, two
-        // steps at a time: each step's total comes out of the same tree
-        // whichever step it is paired with.
-#pragma unroll
-        for (int i = 0; i < PF; i += 2) {
-            if (red_n[i] >= 0 || red_n[i + 1] >= 0) {
-                const double zP = wave_pair_sum64(redP[i], redP[i + 1]);
-                const float zN = wave_pair_sum(redN[i], redN[i + 1]);
-                if (red_n[i] >= 0) {
-                    cP.add(red_n[i], lane_read(zP, 31));
-                    cN.add(red_n[i], lane_read(zN, 31));
-                }
-                if (red_n[i + 1] >= 0) {
-                    cP.add(red_n[i + 1], lane_read(zP, 63));
-                    cN.add(red_n[i + 1], lane_read(zN, 63));
-                }
-            }
-        }
-    }
+        int p = 0, n = ns;
+        int mlo = __builtin_amdgcn_readlane(mlo_r, 0);
+        int mend = __builtin_amdgcn_readlane(mlo_r, 1);
+        // Trivial steps.  Where a panel lies wholly past the last bin with mass
+        // of member n's row (every 1 - F there is exactly 0), or where G is
+        // already exactly 0 over the whole panel (an earlier member's row had
+        // no mass up to its end), step n leaves G unchanged bit for bit; if no
+        // member of the panel needs scoring at that step, its panel sums are
+        // those of step n-1 and the update, its loads and its reductions are
+        // skipped.
+        bool pass_zero = false;                  // G == 0 on every bin of this pass's panel
+        Member pass_mb;                          // CR == 1: this lane's member of the pass
+        double pass_th = 0.0;                    //   and its position in bin k, fp64,
+        float pass_wq[4] = {0.0f, 0.0f, 0.0f, 0.0f};   // and its quarter weights
+        bool pass_valid = false;
+        float etot_prev = 0.0f, T_prev = 0.0f;
+        double gl_prev = 0.0;
 
-    // ---- E-only panels (tabulated mode): past LASTP no member reads G, so
-    // these panels only add their sums of 1 - G to E[L_B], in a loop of its
-    // own: the product and the sum, no discounted prefix, snapshot or
-    // carries.  Its ring is primed afresh; the panels' sums are added in
-    // panel order after those of the member panels, as before.  (ESPLIT:
-    // every panel's sums come from emax_kernel.)
-    if constexpr (!ESPLIT) {
-        if (LASTP + 1 < NP) {
-            constexpr int PFB = ORLOJ_EONLY_PREFETCH;   // its ring is deeper: fewer registers live here
-            // Classes repeat along a deadline-ordered queue (fast classes
-            // come first), and a repeat's row slice has usually left L2 by
-            // the time the wave reads it again.  The RC classes with the
-            // most members (at most 64 members, one per lane) keep their
-            // slice of the current panel in registers for the pass: the
-            // class's first member in step order loads it through the ring
-            // as any step does and copies it, and its later members read the
-            // copy while the ring loads the constant row for them.  Same
-            // values, same bits.  (Where a step is skipped because G is 0
-            // over the panel, every later step of the pass is skipped too,
-            // so a copy taken then is never read.)
-            // The next RL classes keep theirs in LDS, in the space of the
-            // member panels' snapshot, prefixes and plans (unused from here
-            // on), as far as this launch's LDS holds them: the first member
-            // writes its slice there, and later members read it back into
-            // their ring slot (loaded with the constant row) at their step.
-            // The LDS read is issued at the step rather than with the ring's
-            // loads: a ring filled from two kinds of loads would make every
-            // step wait for all of the ring's memory loads.
-            constexpr int RC = CR == 1 ? ORLOJ_EONLY_CACHE : 0;
-            constexpr int RL = CR == 1 && CPL % 4 == 0 ? ORLOJ_EONLY_LDS_CACHE : 0;
-            constexpr int NC = RC + RL;
-            constexpr int RCA = RC > 0 ? RC : 1;
-            constexpr int SLOT = 4 * PW;                        // bytes of one slice
-            const int rl = min(RL, (int)((score_fixed_bytes<CPL>() + (size_t)maxcap * score_bytes_per_member()) / SLOT));
-            // step code of member `lane`: NC (read from memory), k < NC (a
-            // later member of cached class k: registers below RC, LDS from
-            // RC), NC + 1 + k (the first member of class k)
-            int rk_r = NC;
-            if constexpr (NC > 0) {
-                const int cl = lane < n1 ? __builtin_bit_cast(int, cls_r.v[0]) : -1 - lane;
-                int cnt = 0, first = 64;        // members with this lane's class, the first of them
-                for (int m = n1 - 1; m >= 0; --m) {
-                    const bool same = __builtin_amdgcn_readlane(cl, m) == cl;
-                    cnt += same ? 1 : 0;
-                    first = same ? m : first;
-                }
-                bool taken = lane >= n1;
+        // Warm-up: G over steps 0 .. n0-1 of panel pp (the product only, the
+        // same fma per bin and step as a scored step, so the same bits; a step
+        // whose row cannot change G multiplies by an exact 0 or finds G = 0),
+        // with rows loaded PFW steps ahead: these steps are short and would
+        // otherwise wait on their loads.  Leaves pass_zero for the steps after.
+        constexpr int PFW = ORLOJ_WARMUP_PREFETCH;
+        auto warm_up = [&](int pp) {
+            const int p0w = pp * PW, pbw = p0w + base;
+            float wb[PFW][CPL];
+            int wlo[PFW], whi[PFW];
+            bool zero = false;                   // G == 0 over the panel
 #pragma unroll
-                for (int k = 0; k < NC; ++k) {
-                    // most members first, ties to the earlier member; a
-                    // class with a single member gains nothing
-                    const int key = (taken || cnt < 2 || k >= RC + rl) ? -1 : (cnt << 6) | (63 - lane);
-                    const int best = wave_max_i32(key);
-                    if (best >= 0) {
-                        const int ck = __builtin_amdgcn_readlane(cl, 63 - (best & 63));
-                        if (cl == ck)
-                            rk_r = first == lane ? NC + 1 + k : k;
-                        taken = taken || cl == ck;
-                    }
-                }
-            }
-            auto code = [&](int n) -> int {
-                if constexpr (NC > 0) return __builtin_amdgcn_readlane(rk_r, n);
-                return NC;
-            };
-            // slice k of the LDS classes: float4 j of lane l at 1024 j + 16 l
-            // (each access a run of 64 consecutive 16-byte words)
-            auto lds_slice = [&](int k, int j) {
-                return reinterpret_cast<float4*>(smem_raw + (size_t)k * SLOT + 1024 * j + 16 * lane);
-            };
-            // the ring's load for step n: the constant row for a later member
-            // of a cached class (and where `none`), else memory
-            auto load_e = [&](float (&v)[CPL], int n, int c0, bool none, int& lo, int& hi) {
-                load_step(v, n, c0, none || code(n) < NC, lo, hi);
-            };
-            float creg[RCA][CPL];
-#pragma unroll
-            for (int k = 0; k < RCA; ++k)
-#pragma unroll
-                for (int j = 0; j < CPL; ++j) creg[k][j] = 0.0f;
-            float bufb[PFB][CPL];
-            int blo[PFB], bhi[PFB];
-            const int totalB = (NP - LASTP - 1) * n1;
-            const int itersB = (totalB + PFB - 1) / PFB * PFB;
-            int qf_p = LASTP + 1, qf_n = 0;
-#pragma unroll
-            for (int i = 0; i < PFB; ++i) {
-                load_e(bufb[i], qf_n, qf_p * PW + base, false, blo[i], bhi[i]);
+            for (int i = 0; i < PFW; ++i) {
+                load_step(wb[i], min(i, n0 - 1), pbw, false, wlo[i], whi[i]);
                 __builtin_amdgcn_sched_barrier(0);
-                if (++qf_n == n1) { qf_n = 0; qf_p = min(qf_p + 1, NP - 1); }
             }
-            int pb = LASTP + 1, nb = 0;
-            bool zero_b = false;
-            float eprev = 0.0f;
-            for (int it0 = 0; it0 < itersB; it0 += PFB) {
+            for (int w0 = 0; w0 < n0; w0 += PFW) {
 #pragma unroll
-                for (int i = 0; i < PFB; ++i) {
-                    const int p0 = pb * PW;
-                    const int pbase = p0 + base;
-                    if (nb == 0) {
-                        asm volatile("" ::: "memory");
+                for (int i = 0; i < PFW; ++i) {
+                    const int nw = w0 + i;
+                    if (nw < n0) {
 #pragma unroll
-                        for (int j = 0; j < CPL; ++j) Gacc[j] = 1.0;
-                        zero_b = false;
-                    }
-                    const int hi_n = bhi[i];
-                    const int lo_n = blo[i];
-                    const bool real = nb >= n0;
-                    const bool unchanged = zero_b || p0 >= hi_n;
-                    const bool skip = pb >= NP || (real ? (nb > n0 && unchanged) : unchanged);
-                    double gs[Q::QW];
-                    // G <- G (1 - t) over the lane's bins, t from the row
-                    // slice (ring slot or cache register)
-                    auto update = [&](const float (&tv)[CPL]) {
-#pragma unroll
-                        for (int qq = 0; qq < Q::NQ; ++qq) {
-#pragma unroll
-                            for (int r = 0; r < Q::QW; ++r) {
-                                const int j = qq * Q::QW + r;
-                                const float t = (EXACT || pbase + j < K) ? tv[j] : 0.0f;
-                                Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
-                                gs[r] = qq == 0 ? Gacc[j] : gs[r] + Gacc[j];
-                            }
+                        for (int j = 0; j < CPL; ++j) {
+                            const float t = (EXACT || pbw + j < K) ? wb[i][j] : 0.0f;
+                            Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
                         }
-                    };
-                    const int kc = code(nb);
-                    // a cached class's first member: keep its slice
-#pragma unroll
-                    for (int k = 0; k < RC; ++k) {
-                        if (kc == NC + 1 + k) {
-                            asm volatile("" ::: "memory");
-#pragma unroll
-                            for (int j = 0; j < CPL; ++j) creg[k][j] = bufb[i][j];
-                        }
-                    }
-                    if constexpr (RL > 0) {
-                        if (kc >= NC + 1 + RC) {
-                            asm volatile("" ::: "memory");
-#pragma unroll
-                            for (int j = 0; j < CPL / 4; ++j)
-                                *lds_slice(kc - NC - 1 - RC, j) =
-                                    make_float4(bufb[i][4 * j], bufb[i][4 * j + 1], bufb[i][4 * j + 2], bufb[i][4 * j + 3]);
-                        }
-                    }
-                    if (!skip) {
-                        bool done = false;
-#pragma unroll
-                        for (int k = 0; k < RC; ++k) {
-                            if (!done && kc == k) {
-                                // a real branch per slot (the asm keeps it
-                                // from becoming per-bin selects)
-                                asm volatile("" ::: "memory");
-                                update(creg[k]);
-                                done = true;
-                            }
-                        }
-                        if constexpr (RL > 0) {
-                            if (!done && kc >= RC && kc < NC) {
-                                asm volatile("" ::: "memory");
-#pragma unroll
-                                for (int j = 0; j < CPL / 4; ++j) {
-                                    const float4 t = *lds_slice(kc - RC, j);
-                                    bufb[i][4 * j] = t.x; bufb[i][4 * j + 1] = t.y;
-                                    bufb[i][4 * j + 2] = t.z; bufb[i][4 * j + 3] = t.w;
-                                }
-                            }
-                        }
-                        if (!done) update(bufb[i]);
+                        zero = zero || min(p0w + PW, K) <= wlo[i];
                     }
 #pragma unroll
                     for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(Gacc[j])::"memory");
-                    const bool zero_after = zero_b || min(p0 + PW, K) <= lo_n;
-                    load_e(bufb[i], qf_n, qf_p * PW + base, zero_after && qf_p == pb, blo[i], bhi[i]);
-                    if (++qf_n == n1) { qf_n = 0; qf_p = min(qf_p + 1, NP - 1); }
-                    if (pb < NP && real) {
-                        float etot = eprev;
-                        if (!skip) {
+                    load_step(wb[i], min(nw + PFW, n0 - 1), pbw, zero, wlo[i], whi[i]);
+                }
+            }
+            pass_zero = zero;
+        };
+
+        static_assert(PF % 2 == 0, "steps are reduced in pairs");
+        for (int it0 = 0; it0 < iters; it0 += PF) {
+            // each scoring step's member sums (0 in lanes without a member) and
+            // its index (-1: no member scored)
+            double redP[PF];
+            float redN[PF];
+            int red_n[PF];
+#pragma unroll
+            for (int i = 0; i < PF; ++i) redP[i] = 0.0, redN[i] = 0.0f, red_n[i] = -1;
+#pragma unroll
+            for (int i = 0; i < PF; ++i) {
+                if (n == ns) {
+                    // a real branch (the asm keeps it from becoming selects)
+                    asm volatile("" ::: "memory");
+#pragma unroll
+                    for (int j = 0; j < CPL; ++j) Gacc[j] = 1.0;
+                    pass_zero = false;
+                    if constexpr (WARM_LOOP) {
+                        if (n0 > 0 && p < NPW) warm_up(p);
+                    }
+                    if constexpr (CR == 1) {
+                        // at most 64 members: lane l scores member mlo + l of this
+                        // pass at every step, so its plan is read from LDS once
+                        pass_valid = mlo + lane < mend;
+                        pass_mb = s_mem[min(mlo + lane, n1 - 1)];
+                        pass_th = (double)pass_mb.theta + (double)pass_mb.thlo;
+                        quarter_weights(pass_mb.rq, pass_wq);
+                    }
+                }
+                const int p0 = ONE ? 0 : p * PW;              // first bin of the panel
+                const int pbase = p0 + base;                  // first bin of this lane chunk
+                const int hi_n = shi[i];
+                const int lo_n = slo[i];
+                // members of this panel among the first n+1 (ONE: all of them)
+                const int mhi = ONE ? n + 1 : min(mend, n + 1);
+                const bool real = n >= n0;                    // else a warm-up step
+                const bool due = real && (ONE || mlo < mhi);  // some member is scored at this step
+                // G unchanged by this step (a panel past the row's support, or G
+                // already 0 on it): a warm-up step then does nothing, a scored
+                // step after the chunk's first reuses the previous step's sums
+                const bool unchanged = pass_zero || p0 >= hi_n;
+                const bool skip = p >= NPW || (real ? (n > n0 && unchanged && !due) : unchanged);
+                // G <- G * F = G - G (1 - F), in fp64; per-quarter sums
+                double gs[Q::QW];
+                float zqv[Q::NQ];
+                if (!skip) {
+#pragma unroll
+                    for (int qq = 0; qq < Q::NQ; ++qq) {
+                        double zz = 0.0;
+#pragma unroll
+                        for (int r = 0; r < Q::QW; ++r) {
+                            const int j = qq * Q::QW + r;
+                            const float t = (EXACT || pbase + j < K) ? buf[i][j] : 0.0f;
+                            Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
+                            if constexpr (!ESPLIT) gs[r] = qq == 0 ? Gacc[j] : gs[r] + Gacc[j];
+                            zz = r == 0 ? Gacc[j] : fma(zz, d64, Gacc[j]);
+                        }
+                        zqv[qq] = (float)zz;
+                    }
+                }
+                // the slot is refilled only after the update has consumed it, so
+                // the ring keeps its registers (no copies, no wait on the loads
+                // just issued)
+#pragma unroll
+                for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(Gacc[j])::"memory");
+                // G == 0 over the pass from here on: later steps of it need no row
+                const bool zero_after = pass_zero || min(p0 + PW, K) <= lo_n;
+                load_step(buf[i], pf_n, pf_p * PW + base, zero_after && pf_p == p, slo[i], shi[i]);
+                if (++pf_n == n1) { pf_n = ns; pf_p = ONE ? 0 : min(pf_p + 1, NPW - 1); }
+                if (p < NPW && real) {                        // else a ghost or warm-up iteration
+                    float etot = etot_prev, T = T_prev;
+                    double glast_here = gl_prev;
+                    // carries in from the previous panel pass (zero in the first)
+                    float Win = 0.0f;
+                    double glin64 = 0.0;
+                    if (!ONE && p > 0) {
+                        Win = cW.get(n);
+                        glin64 = cGl.get(n);
+                    }
+                    const float glin = (float)glin64;
+                    float A = 0.0f;
+                    if (!skip) {
+                        // quarter ends of the in-chunk discounted prefix, and its total
+                        float zc = zqv[0];
+#pragma unroll
+                        for (int qq = 1; qq < Q::NQ; ++qq) {
+                            zc = fmaf(zc, dQ, zqv[qq]);
+                            zqv[qq] = zc;
+                        }
+                        A = wave_wscan(zc, rp, w15, w31);
+                        if (!ONE && p < LASTP) {              // carried into the next pass
+                            T = lane63(A);                    // discounted prefix at the panel end
+                            T_prev = T;
+                        }
+                    }
+                    if (!skip) {
+                        if constexpr (!ESPLIT) {
                             double gsum = gs[0];
 #pragma unroll
                             for (int r = 1; r < Q::QW; ++r) gsum += gs[r];
+                            // 1 - G summed over the lane's bins (padding bins hold G = 1)
                             const float e = (float)((double)CPL - gsum);
                             etot = lane63(wave_scan_sum(e));
-                            eprev = etot;
                         }
-                        cE.add(nb, (double)etot);
+                        if (!ONE && p < LASTP) {              // carried into the next pass
+                            glast_here = lane63(Gacc[CPL - 1]);
+                            gl_prev = glast_here;
+                        }
+                        etot_prev = etot;
+
+                        if (due) {
+                            // snapshot of G over the panel, fp64, pairs of bins
+                            // interleaved over the lanes (16-byte writes)
+                            if constexpr (CPL >= 2) {
+#pragma unroll
+                                for (int j = 0; j < CPL; j += 2) {
+                                    const int pair = (j >> 1) * 64 + (lane ^ (j >> 1));
+                                    *reinterpret_cast<double2*>(smem_raw + L::GD + 16 * pair) =
+                                        make_double2(Gacc[j], Gacc[j + 1]);
+                                }
+                            } else {
+                                *reinterpret_cast<double*>(smem_raw + L::GD + 8 * lane) = Gacc[0];
+                            }
+#pragma unroll
+                            for (int qq = 0; qq < Q::NQ; ++qq) s_zq[lane * Q::NQ + qq] = zqv[qq];
+                            s_A[lane] = A;
+                            if (!ONE && lane == 0) s_kd[2] = glin64;   // (ONE: stays 0)
+                            wave_lds_fence();
+                            double pP = 0.0;
+                            float pN = 0.0f;
+                            const int nn = n + 1;
+                            auto score_member = [&](const Member& mb, int m, double th, const float (&wq4)[4]) {
+                                const unsigned char* f = smem_raw;
+                                auto atf = [&](int off) { return *reinterpret_cast<const float*>(f + off); };
+                                auto atd = [&](int off) { return *reinterpret_cast<const double*>(f + off); };
+                                const double gk64 = atd(mb.o0);
+                                const double gk164 = atd(mb.o1);
+                                const float al0 = atf(mb.oa);
+                                const float zq0 = atf(mb.oz);
+                                // the quarter's G values (fp32 terms of the priority)
+                                float g4[4];
+                                if constexpr (Q::QW == 4) {
+                                    const double2 t0 = *reinterpret_cast<const double2*>(f + mb.o4);
+                                    // the quarter's second pair: its slot follows
+                                    // the first's by 64, with the lane index's
+                                    // low bit flipped (the first pair's index is even)
+                                    const double2 t1 = *reinterpret_cast<const double2*>(f + ((mb.o4 + 16 * 64) ^ 16));
+                                    g4[0] = (float)t0.x; g4[1] = (float)t0.y;
+                                    g4[2] = (float)t1.x; g4[3] = (float)t1.y;
+                                } else if constexpr (Q::QW == 2) {
+                                    const double2 t0 = *reinterpret_cast<const double2*>(f + mb.o4);
+                                    g4[0] = (float)t0.x; g4[1] = (float)t0.y;
+                                    g4[2] = g4[3] = 0.0f;
+                                } else {
+                                    g4[0] = (float)atd(mb.o4);
+                                    g4[1] = g4[2] = g4[3] = 0.0f;
+                                }
+                                // discounted prefix of the quarter up to bin k-2
+                                // (weights 0 when the member needs no quarter term)
+                                const float z4 = fmaf(wq4[0], g4[0], fmaf(wq4[1], g4[1], fmaf(wq4[2], g4[2], wq4[3] * g4[3])));
+                                const float zin = fmaf(mb.fq, zq0, z4);
+                                // (ONE: no pass before this one, so no carried
+                                // terms: their weights are 0 and the rest is
+                                // >= +0, so dropping them keeps the bits)
+                                const float Zv = ONE ? fmaf(mb.cA, al0, zin)
+                                                     : fmaf(mb.cW, Win, fmaf(mb.cG, glin, fmaf(mb.cA, al0, zin)));
+                                const float gk = (float)gk64, gk1 = (float)gk164;
+                                const float h = gk1 - gk;
+                                // P in fp64: the expected finish count sums it
+                                const double P64 = fma(th, gk164 - gk64, gk64);
+                                const float num = mb.cost * fmaf(mb.cg, fmaf(-omd, Zv, gk), h * mb.psi);
+                                a.P[prob + (int64_t)n * nn / 2 + m] = (float)P64;
+                                // (one member per lane and pass when CR == 1:
+                                // its values, not a sum with 0)
+                                pP = CR == 1 ? P64 : pP + P64;
+                                pN = CR == 1 ? num : pN + num;
+                            };
+                            if constexpr (CR == 1) {
+                                // the lane's member of this pass, already in registers
+                                if (pass_valid && mlo + lane < mhi) score_member(pass_mb, mlo + lane, pass_th, pass_wq);
+                            } else {
+                                for (int m = mlo + lane; m < mhi; m += 64) {
+                                    const Member mb = s_mem[m];
+                                    float wq4[4];
+                                    quarter_weights(mb.rq, wq4);
+                                    score_member(mb, m, (double)mb.theta + (double)mb.thlo, wq4);
+                                }
+                            }
+                            // reduced across the lanes with the other step of
+                            // its pair, after the pair
+                            redP[i] = pP;
+                            redN[i] = pN;
+                            red_n[i] = n;
+                            wave_lds_fence();
+                        }
                     }
-                    zero_b = zero_after;
-                    if (++nb == n1) { nb = 0; ++pb; }
+                    // carries out to the next panel pass, per-step sums
+                    if (!ONE && p < LASTP) {
+                        cW.set(n, fmaf(Win, dPW, T));
+                        cGl.set(n, glast_here);
+                    }
+                    if constexpr (!ESPLIT) cE.add(n, (double)etot);
+                }
+                pass_zero = zero_after;
+                if (++n == n1) {
+                    n = ns;
+                    ++p;
+                    if (!ONE) {
+                        mlo = __builtin_amdgcn_readlane(mlo_r, min(p, NP));
+                        mend = __builtin_amdgcn_readlane(mlo_r, min(p + 1, NP));
+                    }
+                }
+            }
+            // Sum P (fp64) and the priority terms (fp32) over the lanes, two
+            // steps at a time: each step's total comes out of the same tree
+            // whichever step it is paired with.
+#pragma unroll
+            for (int i = 0; i < PF; i += 2) {
+                if (red_n[i] >= 0 || red_n[i + 1] >= 0) {
+                    const double zP = wave_pair_sum64(redP[i], redP[i + 1]);
+                    const float zN = wave_pair_sum(redN[i], redN[i + 1]);
+                    if (red_n[i] >= 0) {
+                        cP.add(red_n[i], lane_read(zP, 31));
+                        cN.add(red_n[i], lane_read(zN, 31));
+                    }
+                    if (red_n[i + 1] >= 0) {
+                        cP.add(red_n[i + 1], lane_read(zP, 63));
+                        cN.add(red_n[i + 1], lane_read(zN, 63));
+                    }
                 }
             }
         }
-    }
 
-    // ---- candidate outputs: lane l holds steps l, l + 64, ...
+        // ---- E-only panels (tabulated mode): past LASTP no member reads G, so
+        // these panels only add their sums of 1 - G to E[L_B], in a loop of its
+        // own: the product and the sum, no discounted prefix, snapshot or
+        // carries.  Its ring is primed afresh; the panels' sums are added in
+        // panel order after those of the member panels, as before.  (ESPLIT:
+        // every panel's sums come from emax_kernel.)
+        if constexpr (!ESPLIT) {
+            if (LASTP + 1 < NP) {
+                constexpr int PFB = ORLOJ_EONLY_PREFETCH;   // its ring is deeper: fewer registers live here
+                // Classes repeat along a deadline-ordered queue (fast classes
+                // come first), and a repeat's row slice has usually left L2 by
+                // the time the wave reads it again.  The RC classes with the
+                // most members (at most 64 members, one per lane) keep their
+                // slice of the current panel in registers for the pass: the
+                // class's first member in step order loads it through the ring
+                // as any step does and copies it, and its later members read the
+                // copy while the ring loads the constant row for them.  Same
+                // values, same bits.  (Where a step is skipped because G is 0
+                // over the panel, every later step of the pass is skipped too,
+                // so a copy taken then is never read.)
+                // The next RL classes keep theirs in LDS, in the space of the
+                // member panels' snapshot, prefixes and plans (unused from here
+                // on), as far as this launch's LDS holds them: the first member
+                // writes its slice there, and later members read it back into
+                // their ring slot (loaded with the constant row) at their step.
+                // The LDS read is issued at the step rather than with the ring's
+                // loads: a ring filled from two kinds of loads would make every
+                // step wait for all of the ring's memory loads.
+                constexpr int RC = CR == 1 ? ORLOJ_EONLY_CACHE : 0;
+                constexpr int RL = CR == 1 && CPL % 4 == 0 ? ORLOJ_EONLY_LDS_CACHE : 0;
+                constexpr int NC = RC + RL;
+                constexpr int RCA = RC > 0 ? RC : 1;
+                constexpr int SLOT = 4 * PW;                        // bytes of one slice
+                const int rl = min(RL, (int)((score_fixed_bytes<CPL>() + (size_t)maxcap * score_bytes_per_member()) / SLOT));
+                // step code of member `lane`: NC (read from memory), k < NC (a
+                // later member of cached class k: registers below RC, LDS from
+                // RC), NC + 1 + k (the first member of class k)
+                int rk_r = NC;
+                if constexpr (NC > 0) {
+                    const int cl = lane < n1 ? __builtin_bit_cast(int, cls_r.v[0]) : -1 - lane;
+                    int cnt = 0, first = 64;        // members with this lane's class, the first of them
+                    for (int m = n1 - 1; m >= 0; --m) {
+                        const bool same = __builtin_amdgcn_readlane(cl, m) == cl;
+                        cnt += same ? 1 : 0;
+                        first = same ? m : first;
+                    }
+                    bool taken = lane >= n1;
 #pragma unroll
-    for (int r = 0; r < CR; ++r) {
-        const int n = r * 64 + lane;
-        if (n >= n0 && n < n1) {
-            double esum = cE.mine(r);
-            if (ESPLIT && !a.defer) {
-                // the panels' sums in panel order, as this kernel adds them
-                esum = 0.0;
-                const size_t pair = AFF ? (size_t)q : (size_t)q * (size_t)a.nbs + (size_t)bi;
-                const float* ps = a.psum + pair * (size_t)a.np_e * (size_t)maxcap + n;
-                for (int pp = 0; pp < a.np_e; ++pp) esum += (double)ps[(size_t)pp * (size_t)maxcap];
-            }
-            a.E[cand + n] = cP.mine(r);
-            if (ESPLIT && a.defer) {
-                // the selection finishes E[L_B] and the score from the
-                // panel sums (same expression, same bits): it runs after
-                // emax_kernel's waves, which share this launch
-                a.S[cand + n] = cN.mine(r);
-            } else {
-                const double el = c0q + w * (0.5 + esum);
-                a.EL[cand + n] = (float)el;
-                a.S[cand + n] = (float)((double)cN.mine(r) / el);
+                    for (int k = 0; k < NC; ++k) {
+                        // most members first, ties to the earlier member; a
+                        // class with a single member gains nothing
+                        const int key = (taken || cnt < 2 || k >= RC + rl) ? -1 : (cnt << 6) | (63 - lane);
+                        const int best = wave_max_i32(key);
+                        if (best >= 0) {
+                            const int ck = __builtin_amdgcn_readlane(cl, 63 - (best & 63));
+                            if (cl == ck)
+                                rk_r = first == lane ? NC + 1 + k : k;
+                            taken = taken || cl == ck;
+                        }
+                    }
+                }
+                auto code = [&](int n) -> int {
+                    if constexpr (NC > 0) return __builtin_amdgcn_readlane(rk_r, n);
+                    return NC;
+                };
+                // slice k of the LDS classes: float4 j of lane l at 1024 j + 16 l
+                // (each access a run of 64 consecutive 16-byte words)
+                auto lds_slice = [&](int k, int j) {
+                    return reinterpret_cast<float4*>(smem_raw + (size_t)k * SLOT + 1024 * j + 16 * lane);
+                };
+                // the ring's load for step n: the constant row for a later member
+                // of a cached class (and where `none`), else memory
+                auto load_e = [&](float (&v)[CPL], int n, int c0, bool none, int& lo, int& hi) {
+                    load_step(v, n, c0, none || code(n) < NC, lo, hi);
+                };
+                float creg[RCA][CPL];
+#pragma unroll
+                for (int k = 0; k < RCA; ++k)
+#pragma unroll
+                    for (int j = 0; j < CPL; ++j) creg[k][j] = 0.0f;
+                float bufb[PFB][CPL];
+                int blo[PFB], bhi[PFB];
+                const int totalB = (NP - LASTP - 1) * n1;
+                const int itersB = (totalB + PFB - 1) / PFB * PFB;
+                int qf_p = LASTP + 1, qf_n = 0;
+#pragma unroll
+                for (int i = 0; i < PFB; ++i) {
+                    load_e(bufb[i], qf_n, qf_p * PW + base, false, blo[i], bhi[i]);
+                    __builtin_amdgcn_sched_barrier(0);
+                    if (++qf_n == n1) { qf_n = 0; qf_p = min(qf_p + 1, NP - 1); }
+                }
+                int pb = LASTP + 1, nb = 0;
+                bool zero_b = false;
+                float eprev = 0.0f;
+                for (int it0 = 0; it0 < itersB; it0 += PFB) {
+#pragma unroll
+                    for (int i = 0; i < PFB; ++i) {
+                        const int p0 = pb * PW;
+                        const int pbase = p0 + base;
+                        if (nb == 0) {
+                            asm volatile("" ::: "memory");
+#pragma unroll
+                            for (int j = 0; j < CPL; ++j) Gacc[j] = 1.0;
+                            zero_b = false;
+                        }
+                        const int hi_n = bhi[i];
+                        const int lo_n = blo[i];
+                        const bool real = nb >= n0;
+                        const bool unchanged = zero_b || p0 >= hi_n;
+                        const bool skip = pb >= NP || (real ? (nb > n0 && unchanged) : unchanged);
+                        double gs[Q::QW];
+                        // G <- G (1 - t) over the lane's bins, t from the row
+                        // slice (ring slot or cache register)
+                        auto update = [&](const float (&tv)[CPL]) {
+#pragma unroll
+                            for (int qq = 0; qq < Q::NQ; ++qq) {
+#pragma unroll
+                                for (int r = 0; r < Q::QW; ++r) {
+                                    const int j = qq * Q::QW + r;
+                                    const float t = (EXACT || pbase + j < K) ? tv[j] : 0.0f;
+                                    Gacc[j] = fma(-Gacc[j], (double)t, Gacc[j]);
+                                    gs[r] = qq == 0 ? Gacc[j] : gs[r] + Gacc[j];
+                                }
+                            }
+                        };
+                        const int kc = code(nb);
+                        // a cached class's first member: keep its slice
+#pragma unroll
+                        for (int k = 0; k < RC; ++k) {
+                            if (kc == NC + 1 + k) {
+                                asm volatile("" ::: "memory");
+#pragma unroll
+                                for (int j = 0; j < CPL; ++j) creg[k][j] = bufb[i][j];
+                            }
+                        }
+                        if constexpr (RL > 0) {
+                            if (kc >= NC + 1 + RC) {
+                                asm volatile("" ::: "memory");
+#pragma unroll
+                                for (int j = 0; j < CPL / 4; ++j)
+                                    *lds_slice(kc - NC - 1 - RC, j) =
+                                        make_float4(bufb[i][4 * j], bufb[i][4 * j + 1], bufb[i][4 * j + 2], bufb[i][4 * j + 3]);
+                            }
+                        }
+                        if (!skip) {
+                            bool done = false;
+#pragma unroll
+                            for (int k = 0; k < RC; ++k) {
+                                if (!done && kc == k) {
+                                    // a real branch per slot (the asm keeps it
+                                    // from becoming per-bin selects)
+                                    asm volatile("" ::: "memory");
+                                    update(creg[k]);
+                                    done = true;
+                                }
+                            }
+                            if constexpr (RL > 0) {
+                                if (!done && kc >= RC && kc < NC) {
+                                    asm volatile("" ::: "memory");
+#pragma unroll
+                                    for (int j = 0; j < CPL / 4; ++j) {
+                                        const float4 t = *lds_slice(kc - RC, j);
+                                        bufb[i][4 * j] = t.x; bufb[i][4 * j + 1] = t.y;
+                                        bufb[i][4 * j + 2] = t.z; bufb[i][4 * j + 3] = t.w;
+                                    }
+                                }
+                            }
+                            if (!done) update(bufb[i]);
+                        }
+#pragma unroll
+                        for (int j = 0; j < CPL; ++j) asm volatile("" : "+v"(Gacc[j])::"memory");
+                        const bool zero_after = zero_b || min(p0 + PW, K) <= lo_n;
+                        load_e(bufb[i], qf_n, qf_p * PW + base, zero_after && qf_p == pb, blo[i], bhi[i]);
+                        if (++qf_n == n1) { qf_n = 0; qf_p = min(qf_p + 1, NP - 1); }
+                        if (pb < NP && real) {
+                            float etot = eprev;
+                            if (!skip) {
+                                double gsum = gs[0];
+#pragma unroll
+                                for (int r = 1; r < Q::QW; ++r) gsum += gs[r];
+                                const float e = (float)((double)CPL - gsum);
+                                etot = lane63(wave_scan_sum(e));
+                                eprev = etot;
+                            }
+                            cE.add(nb, (double)etot);
+                        }
+                        zero_b = zero_after;
+                        if (++nb == n1) { nb = 0; ++pb; }
+                    }
+                }
             }
         }
-    }
+
+        // ---- candidate outputs: lane l holds steps l, l + 64, ...
+#pragma unroll
+        for (int r = 0; r < CR; ++r) {
+            const int n = r * 64 + lane;
+            if (n >= n0 && n < n1) {
+                double esum = cE.mine(r);
+                if (ESPLIT && !a.defer) {
+                    // the panels' sums in panel order, as this kernel adds them
+                    esum = 0.0;
+                    const size_t pair = AFF ? (size_t)q : (size_t)q * (size_t)a.nbs + (size_t)bi;
+                    const float* ps = a.psum + pair * (size_t)a.np_e * (size_t)maxcap + n;
+                    for (int pp = 0; pp < a.np_e; ++pp) esum += (double)ps[(size_t)pp * (size_t)maxcap];
+                }
+                a.E[cand + n] = cP.mine(r);
+                if (ESPLIT && a.defer) {
+                    // the selection finishes E[L_B] and the score from the
+                    // panel sums (same expression, same bits): it runs after
+                    // emax_kernel's waves, which share this launch
+                    a.S[cand + n] = cN.mine(r);
+                } else {
+                    const double el = c0q + w * (0.5 + esum);
+                    a.EL[cand + n] = (float)el;
+                    a.S[cand + n] = (float)((double)cN.mine(r) / el);
+                }
+            }
+        }
+    };
+    if (lastp == 0) rest(BoolTag<true>{});
+    else rest(BoolTag<false>{});
 }
 
 template <int CPL, int PF, bool EXACT, int CR, bool AFF, bool ESPLIT>
