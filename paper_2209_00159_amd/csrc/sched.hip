@@ -375,24 +375,45 @@ int orloj_simulate_trace(orloj_sched* s, const orloj_trace* trace, double tick_m
     for (int64_t i = 1; i < trace->n; ++i)
         if (!(trace->h_release_ms[i] >= trace->h_release_ms[i - 1]))
             return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "orloj_simulate_trace: releases not sorted");
-    // cumulative solo histograms for sampling member latencies
+    // cumulative solo histograms for sampling member latencies, and for
+    // each row a guide of kGuide buckets of the draw u: guide[g] is the bin
+    // that the draw ceil(g T / kGuide) falls in (T the row's total), so the
+    // bin of a draw in bucket g lies in [guide[g], guide[g + 1]].  The search
+    // then touches one or two cache lines of the row instead of a dozen
+    // (the rows of all models and classes are far larger than the caches).
+    constexpr int kGuide = 256;
     std::vector<uint64_t> cum;
+    std::vector<uint32_t> guide;
     try {
         cum.resize((size_t)M * C * K);
+        guide.resize((size_t)M * C * (kGuide + 1));
     } catch (...) {
         return orloj_ctx_fail(ctx, ORLOJ_E_NOMEM, "orloj_simulate_trace: sampling tables");
     }
     for (size_t r = 0; r < (size_t)M * C; ++r) {
         uint64_t acc = 0;
-        for (int k = 0; k < K; ++k) cum[r * K + k] = (acc += h_solo_counts[r * K + k]);
+        uint64_t* row = cum.data() + r * K;
+        for (int k = 0; k < K; ++k) row[k] = (acc += h_solo_counts[r * K + k]);
         if (acc == 0)
             return orloj_ctx_fail(ctx, ORLOJ_E_INVALID, "orloj_simulate_trace: empty solo histogram");
+        uint32_t* gd = guide.data() + r * (kGuide + 1);
+        for (int g = 0; g <= kGuide; ++g) {
+            const uint64_t ulo = (uint64_t)(((unsigned __int128)g * acc + kGuide - 1) / kGuide);
+            gd[g] = (uint32_t)(std::upper_bound(row, row + K, ulo) - row);
+        }
     }
     Rng rng{seed};
     auto sample = [&](int q, int c) {
-        const uint64_t* row = cum.data() + ((size_t)q * C + c) * K;
-        const uint64_t u = rng.below(row[K - 1]);
-        const int k = (int)(std::upper_bound(row, row + K, u) - row);
+        const size_t r = (size_t)q * C + c;
+        const uint64_t* row = cum.data() + r * K;
+        const uint64_t tot = row[K - 1];
+        const uint64_t u = rng.below(tot);
+        // the first bin whose cumulative count exceeds u (std::upper_bound
+        // over the whole row gives the same bin)
+        const int g = (int)(((unsigned __int128)u * kGuide) / tot);
+        const uint32_t* gd = guide.data() + r * (kGuide + 1);
+        const int lo = (int)gd[g], hi = std::min((int)gd[g + 1] + 1, K);
+        const int k = (int)(std::upper_bound(row + lo, row + hi, u) - row);
         return ((double)k + rng.unit()) * h_bin_width_ms[q];
     };
 
