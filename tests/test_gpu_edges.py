@@ -384,6 +384,43 @@ def repeated_class_case(seed, K):
     return explicit_workload(f"repeat-{seed}-K{K}", counts, bs, [1.0] * M, queues, nows)
 
 
+def mixed_panel_case(seed, K):
+    """Repeated classes with deadlines over the first three panels: the
+    launch's short prefixes end in panel 0 (the kernel body for one member
+    panel) and its long ones in later panels (the general body), and its
+    largest prefix (57 members) leaves LDS for two cached slices, not three."""
+    rng = np.random.default_rng(9200 + seed)
+    M, C, bs = 3, 12, (8, 16, 33, 57)
+    counts = np.stack([window_counts(rng, len(bs), C, K) for _ in range(M)])
+    p = 1.0 / np.arange(1, C + 1) ** 1.2
+    p /= p.sum()
+    queues, nows = [], []
+    for q in range(M):
+        n = 57 + 5 * q
+        cls = rng.permutation(C)[rng.choice(C, size=n, p=p)]
+        d = np.sort(rng.uniform(1.0, 0.7 * K, n))          # panels 0 .. 2 (1-ms bins)
+        queues.append((cls, d))
+        nows.append(0.0)
+    return explicit_workload(f"mixed-{seed}-K{K}", counts, bs, [1.0] * M, queues, nows)
+
+
+@gpu
+@pytest.mark.parametrize("K", [4096, 3000])
+@pytest.mark.parametrize("seed", range(3))
+def test_mixed_member_panels_cached_slices(ctx, seed, K):
+    wl = mixed_panel_case(seed, K)
+    say(f"[mixed-panel case] seed={seed} K={K}")
+    ora = oracle.score_workload(wl)
+    _, got = run_gpu(wl, ctx)
+    err = parity.compare(wl, got, ora)
+    say(f"  max errors {err}")
+    _, untrimmed = run_gpu(wl, ctx, trim=False)
+    same_bits(got, untrimmed)
+    for chunk in (0, 8):
+        _, split = run_gpu(wl, ctx, chunk=chunk)
+        same_bits(got, split)
+
+
 @gpu
 @pytest.mark.parametrize("K", [4096, 3000, 2048])
 @pytest.mark.parametrize("seed", range(3))
