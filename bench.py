@@ -382,7 +382,11 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    # The first launches of a fresh process run slow and the time per launch
+    # settles over about 50 of them (score kernel at configuration 5: 0.37 ms
+    # for the first, 0.33 by the tenth, 0.32 from about the fortieth), so the
+    # untimed warm-up is long enough for that by default.
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--config", type=int, default=5)
     ap.add_argument("--cpu-models", type=int, default=128,
                     help="most models the CPU oracle sample may take (each leg stops after ~10 s)")
