@@ -122,3 +122,15 @@ def test_traffic_sums_the_kernels_of_one_call(tmp_path):
     # means per dispatch: 200 + 2000 KiB, scaled by 2 (fetch) and 1 (write)
     assert float(d["fetch_bytes_per_launch"]) == 2200 * 1024 * 2.0
     assert float(d["traffic_bytes_per_launch"]) == 2200 * 1024 * 3.0
+
+
+def test_committed_traffic_summaries_match_the_kernel_source():
+    """The benchmark's roofline.traffic comes from the committed FETCH/WRITE
+    summaries only while they were taken on the kernel source as it stands
+    (its hash without comments and whitespace); a kernel change without a
+    fresh profile would leave the benchmark line without traffic."""
+    import bench
+    for mode in ("tabulated", "affine"):
+        t = bench.measured_traffic(mode)
+        assert t is not None, f"profiles/ {mode} traffic summary is stale or missing"
+        assert t > 0
